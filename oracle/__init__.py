@@ -1,0 +1,172 @@
+"""CPU oracle for the Garfield aggregation rules (test infrastructure only).
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package. The product path (the HIP library and its
+Python binding) never touches it, and the two share no code.
+
+``garfield_oracle.cpp`` is the fp64 C++/OpenMP implementation of each rule as
+Section 3.1 of the paper defines it; this module only marshals numpy arrays to
+it. ``bruteforce.py`` is an independent exact-rational implementation used to
+pin the oracle on tiny inputs.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "garfield_oracle.cpp")
+_LIB = os.path.join(_HERE, "libgarfield_oracle.so")
+
+OK, EINVAL, EREQ = 0, 1, 2
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with g++ (no fast-math: sums keep their order)."""
+    if force or not os.path.exists(_LIB):
+        cmd = ["g++", "-O2", "-std=c++17", "-fopenmp", "-fPIC", "-shared",
+               "-Wall", "-Wextra", "-o", _LIB + ".tmp", _SRC]
+        subprocess.run(cmd, check=True)
+        os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        lib = ctypes.CDLL(_LIB)
+        f32p = ctypes.POINTER(ctypes.c_float)
+        f64p = ctypes.POINTER(ctypes.c_double)
+        i32p = ctypes.POINTER(ctypes.c_int32)
+        i64p = ctypes.POINTER(ctypes.c_int64)
+        c_int, c_i64 = ctypes.c_int, ctypes.c_int64
+        lib.oracle_pairwise_sqdist.argtypes = [f32p, c_int, c_i64, f64p]
+        lib.oracle_krum_scores.argtypes = [f32p, c_int, c_int, c_i64, f64p]
+        lib.oracle_multikrum.argtypes = [f32p, c_int, c_int, c_i64, c_int, f32p, i32p, f64p]
+        lib.oracle_median.argtypes = [f32p, c_int, c_int, c_i64, i32p, c_int, f32p]
+        lib.oracle_bulyan.argtypes = [f32p, c_int, c_int, c_i64, f32p, i32p, i32p, f64p]
+        lib.oracle_mda.argtypes = [f32p, c_int, c_int, c_i64, f32p, i32p, f64p, f64p, i64p]
+        for fn in (lib.oracle_pairwise_sqdist, lib.oracle_krum_scores, lib.oracle_multikrum,
+                   lib.oracle_median, lib.oracle_bulyan, lib.oracle_mda):
+            fn.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+class OracleError(ValueError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: oracle status {code}")
+        self.code = code
+
+
+def _ptr(a, ctype):
+    if a is None:
+        return None
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+def _rows(x):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim != 2:
+        raise ValueError("expected an n x d array")
+    return x
+
+
+def _check(code, what):
+    if code != OK:
+        raise OracleError(code, what)
+
+
+def pairwise_sqdist(x) -> np.ndarray:
+    """n x n fp64 matrix of squared Euclidean distances."""
+    x = _rows(x)
+    n, d = x.shape
+    D = np.zeros((n, n), dtype=np.float64)
+    _check(_load().oracle_pairwise_sqdist(_ptr(x, ctypes.c_float), n, d,
+                                          _ptr(D, ctypes.c_double)), "pairwise_sqdist")
+    return D
+
+
+def krum_scores(x, f: int) -> np.ndarray:
+    x = _rows(x)
+    n, d = x.shape
+    s = np.zeros(n, dtype=np.float64)
+    _check(_load().oracle_krum_scores(_ptr(x, ctypes.c_float), n, f, d,
+                                      _ptr(s, ctypes.c_double)), "krum_scores")
+    return s
+
+
+def multikrum(x, f: int, m: int | None = None, return_scores: bool = False):
+    """(aggregate fp32 [d], sel int32 [m] ascending[, scores fp64 [n]])."""
+    x = _rows(x)
+    n, d = x.shape
+    mm = (n - f) if (m is None or m <= 0) else m
+    out = np.zeros(d, dtype=np.float32)
+    sel = np.zeros(max(mm, 1), dtype=np.int32)
+    scores = np.zeros(n, dtype=np.float64)
+    _check(_load().oracle_multikrum(_ptr(x, ctypes.c_float), n, f, d, 0 if m is None else m,
+                                    _ptr(out, ctypes.c_float), _ptr(sel, ctypes.c_int32),
+                                    _ptr(scores, ctypes.c_double)), "multikrum")
+    sel = sel[:mm]
+    return (out, sel, scores) if return_scores else (out, sel)
+
+
+def krum(x, f: int, return_scores: bool = False):
+    return multikrum(x, f, 1, return_scores)
+
+
+def median(x, f: int = 0, rows=None) -> np.ndarray:
+    x = _rows(x)
+    n, d = x.shape
+    out = np.zeros(d, dtype=np.float32)
+    if rows is None:
+        code = _load().oracle_median(_ptr(x, ctypes.c_float), n, f, d, None, n,
+                                     _ptr(out, ctypes.c_float))
+    else:
+        r = np.ascontiguousarray(rows, dtype=np.int32)
+        code = _load().oracle_median(_ptr(x, ctypes.c_float), n, f, d,
+                                     _ptr(r, ctypes.c_int32), len(r), _ptr(out, ctypes.c_float))
+    _check(code, "median")
+    return out
+
+
+def bulyan(x, f: int, return_rounds: bool = False):
+    """(aggregate, sel ascending[, picks in order, round scores theta x n])."""
+    x = _rows(x)
+    n, d = x.shape
+    theta = n - 2 * f
+    out = np.zeros(d, dtype=np.float32)
+    sel = np.zeros(max(theta, 1), dtype=np.int32)
+    picks = np.zeros(max(theta, 1), dtype=np.int32)
+    rs = np.zeros((max(theta, 1), n), dtype=np.float64)
+    _check(_load().oracle_bulyan(_ptr(x, ctypes.c_float), n, f, d, _ptr(out, ctypes.c_float),
+                                 _ptr(sel, ctypes.c_int32), _ptr(picks, ctypes.c_int32),
+                                 _ptr(rs, ctypes.c_double)), "bulyan")
+    if return_rounds:
+        return out, sel[:theta], picks[:theta], rs[:theta]
+    return out, sel[:theta]
+
+
+def mda(x, f: int, return_diameters: bool = False):
+    """(aggregate, sel ascending[, best diameter, next larger diameter, #subsets at best])."""
+    x = _rows(x)
+    n, d = x.shape
+    out = np.zeros(d, dtype=np.float32)
+    sel = np.zeros(max(n - f, 1), dtype=np.int32)
+    best = np.zeros(1, dtype=np.float64)
+    second = np.zeros(1, dtype=np.float64)
+    nbest = np.zeros(1, dtype=np.int64)
+    _check(_load().oracle_mda(_ptr(x, ctypes.c_float), n, f, d, _ptr(out, ctypes.c_float),
+                              _ptr(sel, ctypes.c_int32), _ptr(best, ctypes.c_double),
+                              _ptr(second, ctypes.c_double), _ptr(nbest, ctypes.c_int64)), "mda")
+    if return_diameters:
+        return out, sel[:n - f], float(best[0]), float(second[0]), int(nbest[0])
+    return out, sel[:n - f]

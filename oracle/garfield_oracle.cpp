@@ -1,0 +1,296 @@
+// Plain CPU oracle for the Garfield gradient aggregation rules (GARs).
+//
+// TEST INFRASTRUCTURE ONLY. Nothing on the product path may link, load or call
+// this file; only the test suite, the smoke check and the benchmark's CPU
+// baseline leg use it. It shares no code with the HIP library.
+//
+// Conventions (one rule for every function below):
+//   * inputs are n x d fp32 vectors, row-major (row i starts at x + i*d);
+//   * every value is widened exactly to fp64 and all arithmetic is fp64;
+//   * aggregates are rounded once, to nearest-even fp32, at the very end;
+//   * index outputs are sets, written in ascending order;
+//   * the only parallelism is the one the paper gives for its CPU median
+//     (each core takes a contiguous share of coordinates, Section 4.3), and a
+//     parallel loop over independent vector pairs for the distances. Neither
+//     changes the order of any floating-point sum.
+//
+// Readings of the paper used where it is silent (each is listed in the design
+// notes of the repository):
+//   R1  Krum's distance is the squared Euclidean distance.
+//   R2  Krum's score sums the n-f-2 smallest distances to the *other* vectors,
+//       added in ascending order.
+//   R3  ties in a score ordering are broken towards the lower index.
+//   R4  Multi-Krum is one-shot: the m lowest (score, index) pairs; m defaults
+//       to n-f.
+//   R5  the median of an even count is the mean of the two middle values.
+//   R6  Bulyan: theta = n-2f rounds of Krum on the not-yet-selected set with
+//       n_R-f-2 neighbours (clamped at 0), then per coordinate the
+//       beta = theta-2f values closest to the median under the key
+//       (|v - med|, v), averaged.
+//   R7  MDA enumerates the subsets of size n-f in lexicographic order and keeps
+//       the first one of strictly smaller diameter (diameter = largest squared
+//       distance inside the subset).
+//
+// Status codes match the library's: 0 ok, 1 invalid argument, 2 n too small
+// for the rule's requirement in f.
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <utility>
+#include <vector>
+
+namespace {
+
+constexpr int kOk = 0;
+constexpr int kInval = 1;
+constexpr int kReq = 2;
+
+inline double at(const float* x, int64_t d, int i, int64_t c) {
+  return static_cast<double>(x[static_cast<int64_t>(i) * d + c]);
+}
+
+// Squared Euclidean distance between rows i and j, summed over c = 0..d-1 in
+// order (Section 3.1, items 2-4 use this distance).
+double sqdist(const float* x, int64_t d, int i, int j) {
+  double s = 0.0;
+  for (int64_t c = 0; c < d; ++c) {
+    const double t = at(x, d, i, c) - at(x, d, j, c);
+    s += t * t;
+  }
+  return s;
+}
+
+// Full symmetric distance matrix with a zero diagonal.
+void distance_matrix(const float* x, int n, int64_t d, double* D) {
+  std::vector<std::pair<int, int>> pairs;
+  for (int i = 0; i < n; ++i)
+    for (int j = i + 1; j < n; ++j) pairs.emplace_back(i, j);
+  for (int i = 0; i < n; ++i) D[i * n + i] = 0.0;
+  const int64_t np = static_cast<int64_t>(pairs.size());
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t p = 0; p < np; ++p) {
+    const int i = pairs[p].first, j = pairs[p].second;
+    const double s = sqdist(x, d, i, j);
+    D[i * n + j] = s;
+    D[j * n + i] = s;
+  }
+}
+
+// Krum score of row i against the candidate set `cand` (which contains i):
+// the sum of the k smallest distances from i to the other candidates, added
+// in ascending order (Section 3.1 item 2, readings R1-R2).
+double krum_score(const double* D, int n, const std::vector<int>& cand, int i, int k) {
+  std::vector<double> dist;
+  for (int j : cand)
+    if (j != i) dist.push_back(D[i * n + j]);
+  std::sort(dist.begin(), dist.end());
+  double s = 0.0;
+  for (int t = 0; t < k && t < static_cast<int>(dist.size()); ++t) s += dist[t];
+  return s;
+}
+
+// Mean of the rows in `rows` (ascending), per coordinate, rounded once.
+void mean_rows(const float* x, int64_t d, const std::vector<int>& rows, float* out) {
+  const double count = static_cast<double>(rows.size());
+#pragma omp parallel for schedule(static)
+  for (int64_t c = 0; c < d; ++c) {
+    double s = 0.0;
+    for (int i : rows) s += at(x, d, i, c);
+    out[c] = static_cast<float>(s / count);
+  }
+}
+
+// Median of k values: middle element for odd k, mean of the two middle
+// elements for even k (Section 3.1 item 1, reading R5).
+double median_of(std::vector<double>& v) {
+  std::sort(v.begin(), v.end());
+  const size_t k = v.size();
+  if (k % 2 == 1) return v[k / 2];
+  return (v[k / 2 - 1] + v[k / 2]) / 2.0;
+}
+
+}  // namespace
+
+extern "C" {
+
+// D (n*n fp64) = pairwise squared Euclidean distances.
+int oracle_pairwise_sqdist(const float* x, int n, int64_t d, double* D) {
+  if (n < 1 || d < 0 || !D || (d > 0 && !x)) return kInval;
+  distance_matrix(x, n, d, D);
+  return kOk;
+}
+
+// Krum scores of all n rows with k = n - f - 2 neighbours.
+int oracle_krum_scores(const float* x, int n, int f, int64_t d, double* scores) {
+  if (n < 1 || f < 0 || d < 0 || !scores || (d > 0 && !x)) return kInval;
+  if (n < 2 * f + 3) return kReq;
+  std::vector<double> D(static_cast<size_t>(n) * n);
+  distance_matrix(x, n, d, D.data());
+  std::vector<int> all(n);
+  for (int i = 0; i < n; ++i) all[i] = i;
+  for (int i = 0; i < n; ++i) scores[i] = krum_score(D.data(), n, all, i, n - f - 2);
+  return kOk;
+}
+
+// Multi-Krum (Section 3.1 item 2): the m rows with the lowest (score, index),
+// then their mean. m <= 0 selects the default n - f. Krum is m = 1.
+// `scores` (n fp64) is optional.
+int oracle_multikrum(const float* x, int n, int f, int64_t d, int m, float* out,
+                     int32_t* sel, double* scores) {
+  if (n < 1 || f < 0 || d < 0 || !sel || (d > 0 && (!x || !out))) return kInval;
+  if (n < 2 * f + 3) return kReq;
+  if (m <= 0) m = n - f;
+  if (m > n - f) return kInval;
+  std::vector<double> D(static_cast<size_t>(n) * n);
+  distance_matrix(x, n, d, D.data());
+  std::vector<int> all(n);
+  for (int i = 0; i < n; ++i) all[i] = i;
+  std::vector<std::pair<double, int>> ranked;
+  for (int i = 0; i < n; ++i) {
+    const double s = krum_score(D.data(), n, all, i, n - f - 2);
+    if (scores) scores[i] = s;
+    ranked.emplace_back(s, i);
+  }
+  std::sort(ranked.begin(), ranked.end());  // (score, index): ties -> lower index
+  std::vector<int> chosen;
+  for (int t = 0; t < m; ++t) chosen.push_back(ranked[t].second);
+  std::sort(chosen.begin(), chosen.end());
+  for (int t = 0; t < m; ++t) sel[t] = chosen[t];
+  mean_rows(x, d, chosen, out);
+  return kOk;
+}
+
+// Coordinate-wise median (Section 3.1 item 1) over the k rows listed in
+// `rows`, or over all n rows when rows is null (then k must be n).
+int oracle_median(const float* x, int n, int f, int64_t d, const int32_t* rows, int k,
+                  float* out) {
+  if (n < 1 || f < 0 || d < 0 || (d > 0 && (!x || !out))) return kInval;
+  if (n < 2 * f + 1) return kReq;
+  std::vector<int> use;
+  if (rows) {
+    if (k < 1) return kInval;
+    for (int t = 0; t < k; ++t) {
+      if (rows[t] < 0 || rows[t] >= n) return kInval;
+      use.push_back(rows[t]);
+    }
+  } else {
+    if (k != n && k > 0) return kInval;
+    for (int i = 0; i < n; ++i) use.push_back(i);
+  }
+  // Contiguous coordinate share per core, as in the paper's CPU median.
+#pragma omp parallel
+  {
+    std::vector<double> v(use.size());
+#pragma omp for schedule(static)
+    for (int64_t c = 0; c < d; ++c) {
+      for (size_t t = 0; t < use.size(); ++t) v[t] = at(x, d, use[t], c);
+      out[c] = static_cast<float>(median_of(v));
+    }
+  }
+  return kOk;
+}
+
+// Bulyan (Section 3.1 item 4, reading R6). `sel` receives the theta selected
+// rows in ascending order; `picks` (optional, theta entries) the same rows in
+// the order they were picked; `round_scores` (optional, theta*n fp64) the
+// Krum score of every row in each round, +inf for rows already picked.
+int oracle_bulyan(const float* x, int n, int f, int64_t d, float* out, int32_t* sel,
+                  int32_t* picks, double* round_scores) {
+  if (n < 1 || f < 0 || d < 0 || !sel || (d > 0 && (!x || !out))) return kInval;
+  if (n < 4 * f + 3) return kReq;
+  const int theta = n - 2 * f;
+  const int beta = theta - 2 * f;
+  std::vector<double> D(static_cast<size_t>(n) * n);
+  distance_matrix(x, n, d, D.data());
+  std::vector<int> remaining(n);
+  for (int i = 0; i < n; ++i) remaining[i] = i;
+  std::vector<int> chosen;
+  for (int r = 0; r < theta; ++r) {
+    const int k = std::max(static_cast<int>(remaining.size()) - f - 2, 0);
+    double best = 0.0;
+    int best_i = -1;
+    if (round_scores)
+      for (int i = 0; i < n; ++i) round_scores[static_cast<int64_t>(r) * n + i] = 1.0 / 0.0;
+    for (int i : remaining) {  // ascending, so strict < keeps the lower index on ties
+      const double s = krum_score(D.data(), n, remaining, i, k);
+      if (round_scores) round_scores[static_cast<int64_t>(r) * n + i] = s;
+      if (best_i < 0 || s < best) {
+        best = s;
+        best_i = i;
+      }
+    }
+    if (picks) picks[r] = best_i;
+    chosen.push_back(best_i);
+    remaining.erase(std::find(remaining.begin(), remaining.end(), best_i));
+  }
+  std::sort(chosen.begin(), chosen.end());
+  for (int t = 0; t < theta; ++t) sel[t] = chosen[t];
+#pragma omp parallel
+  {
+    std::vector<double> v(theta);
+    std::vector<std::pair<double, double>> key(theta);
+#pragma omp for schedule(static)
+    for (int64_t c = 0; c < d; ++c) {
+      for (int t = 0; t < theta; ++t) v[t] = at(x, d, chosen[t], c);
+      std::vector<double> tmp(v);
+      const double med = median_of(tmp);
+      for (int t = 0; t < theta; ++t) {
+        const double dist = v[t] > med ? v[t] - med : med - v[t];
+        key[t] = std::make_pair(dist, v[t]);
+      }
+      std::sort(key.begin(), key.end());
+      double s = 0.0;
+      for (int t = 0; t < beta; ++t) s += key[t].second;
+      out[c] = static_cast<float>(s / static_cast<double>(beta));
+    }
+  }
+  return kOk;
+}
+
+// Minimum-diameter averaging (Section 3.1 item 3, reading R7). `best_diam`
+// and `second_diam` (optional) receive the smallest diameter and the smallest
+// diameter strictly larger than it (+inf if none). `n_best` (optional)
+// receives how many subsets reach the smallest diameter.
+int oracle_mda(const float* x, int n, int f, int64_t d, float* out, int32_t* sel,
+               double* best_diam, double* second_diam, int64_t* n_best) {
+  if (n < 1 || f < 0 || d < 0 || !sel || (d > 0 && (!x || !out))) return kInval;
+  if (n < 2 * f + 1) return kReq;
+  const int s = n - f;
+  std::vector<double> D(static_cast<size_t>(n) * n);
+  distance_matrix(x, n, d, D.data());
+  // Lexicographic enumeration of s-subsets of {0..n-1}.
+  std::vector<int> idx(s);
+  for (int t = 0; t < s; ++t) idx[t] = t;
+  std::vector<int> best_set(idx);
+  double best = 1.0 / 0.0, second = 1.0 / 0.0;
+  int64_t count_best = 0;
+  while (true) {
+    double diam = 0.0;
+    for (int a = 0; a < s; ++a)
+      for (int b = a + 1; b < s; ++b) diam = std::max(diam, D[idx[a] * n + idx[b]]);
+    if (diam < best) {
+      second = best;
+      best = diam;
+      best_set = idx;
+      count_best = 1;
+    } else if (diam == best) {
+      ++count_best;
+    } else if (diam < second) {
+      second = diam;
+    }
+    int t = s - 1;
+    while (t >= 0 && idx[t] == n - s + t) --t;
+    if (t < 0) break;
+    ++idx[t];
+    for (int u = t + 1; u < s; ++u) idx[u] = idx[u - 1] + 1;
+  }
+  for (int t = 0; t < s; ++t) sel[t] = best_set[t];
+  if (best_diam) *best_diam = best;
+  if (second_diam) *second_diam = second;
+  if (n_best) *n_best = count_best;
+  mean_rows(x, d, best_set, out);
+  return kOk;
+}
+
+}  // extern "C"
