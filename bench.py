@@ -1,0 +1,245 @@
+#!/usr/bin/env python3
+"""Benchmark one aggregation step on one MI355X and print one JSON line.
+
+Metric: GAR input GB/s = n * d * 4 B / (time of one whole step), with the n x d
+input already resident in HBM, plus that rate as a fraction of the 8 TB/s HBM
+peak. A step is one full pass of the rule(s) the workload names (distances,
+selection and aggregation, all in libgarfield's HIP kernels), launched on
+torch's current stream. The default workload is the ResNet-18-sized
+Multi-Krum set (n = 11, f = 2, m = 9, d = 11,173,962).
+
+Alongside the metric the line carries:
+  * roofline: the kernel that took the most time, its algorithmic bytes per
+    launch divided by its average duration (HIP events recorded around each
+    launch by the library, over a second pass of the same timed steps);
+  * cpu_baseline: the CPU oracle timed on this host's cores on a bounded
+    sample of the same input.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
+FP32_MFMA_PEAK_TFLOPS = 157.3
+
+
+def _parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=21)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--all", action="store_true", help="one line per workload (1..5)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="target CPU time of the oracle baseline (0 disables it)")
+    ap.add_argument("--direct-max-n", type=int, default=None,
+                    help="override the direct/Gram distance engine threshold")
+    return ap.parse_args()
+
+
+class Step:
+    """One aggregation step of a workload with preallocated outputs."""
+
+    def __init__(self, gf, w, x):
+        import torch
+
+        self.gf, self.w, self.x = gf, w, x
+        self.lib = gf.load()
+        n, d = x.shape
+        dev = x.device
+        self.out = torch.empty(d, dtype=torch.float32, device=dev)
+        self.out2 = torch.empty(d, dtype=torch.float32, device=dev)
+        self.sel = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+        self.stream = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+        p = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+        self.px, self.pout, self.pout2, self.psel = p(x), p(self.out), p(self.out2), p(self.sel)
+
+    def __call__(self):
+        lib, w = self.lib, self.w
+        n, d = self.x.shape
+        f, s = w.f, self.stream
+        rules = w.rules
+        codes = []
+        if rules == ("krum", "median"):
+            codes.append(lib.garfield_krum(self.px, n, f, d, self.pout, self.psel, s))
+            codes.append(lib.garfield_median(self.px, n, f, d, None, n, self.pout2, s))
+        elif rules == ("multikrum",):
+            codes.append(lib.garfield_multikrum(self.px, n, f, d, w.m, self.pout, self.psel, s))
+        elif rules == ("bulyan",):
+            codes.append(lib.garfield_bulyan(self.px, n, f, d, self.pout, self.psel, s))
+        elif rules == ("mda",):
+            codes.append(lib.garfield_mda(self.px, n, f, d, self.pout, self.psel, s))
+        elif rules == ("multikrum-median",):
+            codes.append(lib.garfield_multikrum(self.px, n, f, d, w.m, None, self.psel, s))
+            codes.append(lib.garfield_median(self.px, n, f, d, self.psel, w.m, self.pout, s))
+        else:
+            raise ValueError(rules)
+        if any(codes):
+            raise RuntimeError(f"libgarfield returned {codes}")
+
+
+def algorithmic(kernel, w):
+    """(bound, algorithmic bytes or flops per launch, unit) of a kernel of workload w."""
+    n, f, d = w.n, w.f, w.d
+    if kernel in ("dist_direct", "dist_gram"):
+        return "hbm", 4.0 * n * d
+    if kernel == "mean_rows":
+        k = {"krum": 1, "multikrum": w.m, "mda": n - f}.get(w.rules[0], n)
+        return "hbm", 4.0 * (k + 1) * d
+    if kernel == "median":
+        k = w.m if w.rules == ("multikrum-median",) else n
+        return "hbm", 4.0 * (k + 1) * d
+    if kernel == "bulyan_agg":
+        return "hbm", 4.0 * (n - 2 * f + 1) * d
+    return None, None
+
+
+def cpu_baseline(w, x_host, seconds):
+    """Time the oracle on this host on a bounded sample of the input."""
+    import numpy as np
+
+    import oracle
+
+    n, d = x_host.shape
+    # the oracle is O(n^2 d) for distance rules: estimate from a small slice,
+    # then run on a slice sized for about `seconds` of CPU work
+    def run(xs):
+        t = time.perf_counter()
+        if w.rules == ("krum", "median"):
+            oracle.krum(xs, w.f)
+            oracle.median(xs, w.f)
+        elif w.rules == ("multikrum",):
+            oracle.multikrum(xs, w.f, w.m)
+        elif w.rules == ("bulyan",):
+            oracle.bulyan(xs, w.f)
+        elif w.rules == ("mda",):
+            oracle.mda(xs, w.f)
+        else:
+            _, sel = oracle.multikrum(xs, w.f, w.m)
+            oracle.median(xs, w.f, rows=sel)
+        return time.perf_counter() - t
+
+    probe_d = min(d, 1 << 16)
+    t_probe = run(np.ascontiguousarray(x_host[:, :probe_d]))
+    per_coord = max(t_probe / probe_d, 1e-12)
+    d_s = int(min(d, max(probe_d, seconds / per_coord)))
+    xs = np.ascontiguousarray(x_host[:, :d_s]) if d_s < d else x_host
+    reps, total = 0, 0.0
+    while reps == 0 or (total < seconds and reps < 50):
+        total += run(xs)
+        reps += 1
+    t = total / reps
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    sample = (f"first {d_s} of {d} coordinates" if d_s < d else "the full input") + \
+             f", {reps} run(s), mean time {t:.3f} s"
+    return {"value": round(n * d_s * 4 / t / 1e9, 4), "unit": "GB/s", "cores": threads,
+            "kind": "oracle", "sample": sample}
+
+
+def bench_workload(key, args):
+    import torch
+
+    import paper_2010_05888_amd as gf
+    from paper_2010_05888_amd import synth
+
+    w = synth.WORKLOADS[key]
+    dev = torch.device("cuda:0")
+    print(f"[bench] workload {key}: {w.name}: generating", file=sys.stderr, flush=True)
+    inp = synth.generate(w, dev)
+    x = inp.x
+    torch.cuda.synchronize()
+    step = Step(gf, w, x)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = start.elapsed_time(end) / args.steps
+    value = w.n * w.d * 4 / (ms * 1e-3) / 1e9
+    print(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step (wall {wall * 1e3 / args.steps:.4f})",
+          file=sys.stderr, flush=True)
+
+    # second pass of the same steps with per-kernel HIP events
+    gf.set_kernel_timing(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    kt = gf.kernel_timing()
+    gf.set_kernel_timing(False)
+    kernels = {k: {"launches": c, "avg_ms": round(t / c, 6)} for k, (c, t) in kt.items()}
+    dominant = max(kt, key=lambda k: kt[k][1])
+    bound, per_launch = algorithmic(dominant, w)
+    avg_ms = kt[dominant][1] / kt[dominant][0]
+    roofline = {"kernel": dominant, "bound": bound, "achieved": None, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": None, "traffic": None, "avg_ms": round(avg_ms, 6),
+                "bytes_per_launch": per_launch}
+    if per_launch:
+        achieved = per_launch / (avg_ms * 1e-3) / 1e9
+        roofline["achieved"] = round(achieved, 2)
+        roofline["frac"] = round(achieved / HBM_PEAK_GBS, 4)
+
+    base = None
+    if args.cpu_seconds > 0:
+        print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)
+        base = cpu_baseline(w, x.cpu().numpy(), args.cpu_seconds)
+
+    line = {
+        "metric": "GAR input GB/s (n*d*4B/time) and % of HBM peak",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "config": {"workload": w.name, "rules": list(w.rules), "n": w.n, "f": w.f, "d": w.d,
+                   "m": w.m, "seed": w.seed, "byzantine_rows": inp.byzantine,
+                   "distance_engine": gf.distance_engine(w.n, w.d)},
+        "kernels": kernels,
+        "roofline": roofline,
+        "cpu_baseline": base,
+    }
+    del x, inp, step
+    torch.cuda.empty_cache()
+    return line
+
+
+def main():
+    args = _parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the aggregation rules here are a single-GPU "
+              "build (no sharding or collectives); run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2010_05888_amd as gf
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    gf.load()  # fails loudly when the library is not built
+    if args.direct_max_n is not None:
+        gf.set_direct_max_n(args.direct_max_n)
+    keys = [1, 2, 3, 4, 5] if args.all else [args.workload]
+    for key in keys:
+        print(json.dumps(bench_workload(key, args)), flush=True)
+
+
+if __name__ == "__main__":
+    main()

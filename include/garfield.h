@@ -1,0 +1,153 @@
+/*
+ * garfield.h -- Byzantine-resilient gradient aggregation rules (GARs) on one
+ * MI355X (gfx950) GPU.
+ *
+ * The rules are those of Section 3.1 of "Garfield: System Support for
+ * Byzantine Machine Learning" (arXiv:2010.05888): coordinate-wise Median,
+ * Krum and Multi-Krum, MDA (minimum-diameter averaging) and Bulyan, plus the
+ * plain Average the paper benchmarks them against (Section 5.3).
+ *
+ * Common conventions for every entry point below:
+ *   - x is a DEVICE pointer to n input vectors of d fp32 values, row-major:
+ *     vector i occupies x[i*d .. i*d+d-1]. It is only read.
+ *   - out, sel, dist and rows are DEVICE pointers owned by the caller. The
+ *     library never frees caller memory and never writes outside the sizes
+ *     stated per function.
+ *   - stream is a hipStream_t passed as void* (NULL = the default stream). All
+ *     work is enqueued on it asynchronously; the call returns once enqueued.
+ *     No host<->device copy happens inside any call.
+ *   - Arguments are validated on the host before anything is enqueued. On an
+ *     error, nothing is enqueued and out/sel/dist are left untouched. No call
+ *     aborts or throws across this interface.
+ *   - Scratch memory (partial sums, the distance matrix, scores) lives in a
+ *     per-device workspace the library allocates on first use and grows when a
+ *     call needs more; growing it waits for the device to go idle. Calls on
+ *     one device share that workspace, so calls issued on different streams of
+ *     the same device must not overlap in time.
+ *   - Index outputs (sel) are sets written in ascending order. Ties in a
+ *     ranking are broken towards the lower index.
+ *   - Preconditions not checked: finite inputs with |x| < FLT_MAX/2, and x,
+ *     out, sel, rows, dist valid device allocations of the stated sizes.
+ *   - d == 0 is allowed (all distances are 0, so ties pick the lowest
+ *     indices; nothing is written to out).
+ *   - 1 <= n <= GARFIELD_NMAX.
+ */
+#ifndef GARFIELD_H
+#define GARFIELD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GARFIELD_NMAX 64
+/* Largest number of candidate subsets C(n, f) MDA will enumerate. */
+#define GARFIELD_MDA_MAX_SUBSETS 2147483647LL
+
+typedef enum garfield_status {
+  GARFIELD_OK = 0,
+  GARFIELD_EINVAL = 1,  /* null pointer, n < 1, f < 0, d < 0, m or k out of range */
+  GARFIELD_EREQ = 2,    /* n below the rule's requirement in f (Section 3.1) */
+  GARFIELD_ETOOBIG = 3, /* n > GARFIELD_NMAX, or C(n, f) > GARFIELD_MDA_MAX_SUBSETS */
+  GARFIELD_ENOMEM = 4,  /* the workspace could not be allocated */
+  GARFIELD_EHIP = 5     /* a HIP call or kernel launch failed */
+} garfield_status;
+
+/* Rule identifiers for garfield_workspace_bytes. */
+typedef enum garfield_rule {
+  GARFIELD_RULE_DIST = 0,
+  GARFIELD_RULE_KRUM = 1,
+  GARFIELD_RULE_MULTIKRUM = 2,
+  GARFIELD_RULE_MEDIAN = 3,
+  GARFIELD_RULE_BULYAN = 4,
+  GARFIELD_RULE_MDA = 5,
+  GARFIELD_RULE_AVERAGE = 6
+} garfield_rule;
+
+/*
+ * Pairwise squared Euclidean distances, the distance Krum, MDA and Bulyan
+ * score with (Section 3.1 items 2-4):
+ *   dist[i*n + j] = sum_c (x[i][c] - x[j][c])^2,  symmetric, zero diagonal.
+ * dist: device, n*n fp64. Per-tile partial sums are formed in fp32 and
+ * combined across tiles in fp64 in a fixed order, so the result is
+ * deterministic and identical input vectors give identical rows of dist.
+ */
+garfield_status garfield_pairwise_sqdist(const float* x, int n, int64_t d, double* dist,
+                                         void* stream);
+
+/*
+ * Multi-Krum (Section 3.1 item 2): score(i) = sum of the n-f-2 smallest
+ * dist[i][j], j != i; select the m vectors of lowest (score, index) and
+ * average them. Requires n >= 2f+3 (else GARFIELD_EREQ) and 1 <= m <= n-f;
+ * m <= 0 means the default m = n-f.
+ * out: device, d fp32 = mean of the selected vectors, or NULL to compute the
+ *      selection only (e.g. to feed garfield_median through `rows`).
+ * sel: device, m int32, the selected indices in ascending order.
+ */
+garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int m, float* out,
+                                   int32_t* sel, void* stream);
+
+/* Krum (Section 3.1 item 2): Multi-Krum with m = 1; out is a copy of vector
+ * sel[0]. out may be NULL. */
+garfield_status garfield_krum(const float* x, int n, int f, int64_t d, float* out, int32_t* sel,
+                              void* stream);
+
+/*
+ * Coordinate-wise median (Section 3.1 item 1) over the k vectors whose
+ * indices are listed in `rows` (device int32, each in [0, n)), or over all n
+ * vectors when rows is NULL (k is then ignored). Odd k: the middle value,
+ * which is one of the inputs bit for bit. Even k: the mean of the two middle
+ * values. Requires n >= 2f+1 (f is only checked against n). 1 <= k <= n.
+ * out: device, d fp32.
+ */
+garfield_status garfield_median(const float* x, int n, int f, int64_t d, const int32_t* rows,
+                                int k, float* out, void* stream);
+
+/*
+ * Bulyan (Section 3.1 item 4) with Krum as the inner rule. theta = n-2f
+ * rounds each select the vector of lowest (score, index) among those not yet
+ * selected, scoring against the not-yet-selected set with max(r-f-2, 0)
+ * neighbours (r = vectors left). Then per coordinate: the median of the theta
+ * selected values, and the mean of the beta = theta-2f values closest to it
+ * (closeness key (|v - median|, v)). Requires n >= 4f+3.
+ * out: device, d fp32.   sel: device, theta int32, ascending.
+ */
+garfield_status garfield_bulyan(const float* x, int n, int f, int64_t d, float* out,
+                                int32_t* sel, void* stream);
+
+/*
+ * MDA, minimum-diameter averaging (Section 3.1 item 3): among all subsets of
+ * n-f vectors, the first in lexicographic order whose diameter (largest
+ * squared distance inside it) is smallest; output its mean. Requires
+ * n >= 2f+1 and C(n, f) <= GARFIELD_MDA_MAX_SUBSETS (else GARFIELD_ETOOBIG).
+ * out: device, d fp32 (may be NULL).   sel: device, n-f int32, ascending.
+ */
+garfield_status garfield_mda(const float* x, int n, int f, int64_t d, float* out, int32_t* sel,
+                             void* stream);
+
+/* Average, the non-robust baseline rule of the paper's micro-benchmark
+ * (Section 5.3): out[c] = (1/n) sum_i x[i][c], summed in fp64. */
+garfield_status garfield_average(const float* x, int n, int64_t d, float* out, void* stream);
+
+/*
+ * Bytes of workspace one call of `rule` with these sizes uses (0 if the
+ * arguments are invalid). Informational: the library allocates it itself.
+ */
+size_t garfield_workspace_bytes(int rule, int n, int f, int64_t d, int m);
+
+/* Free the workspace of the current device (waits for the device first). */
+garfield_status garfield_release(void);
+
+/* Static, human-readable description of a status code. */
+const char* garfield_strerror(garfield_status s);
+
+/* Library version string, e.g. "garfield-mi355x 0.1". */
+const char* garfield_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GARFIELD_H */

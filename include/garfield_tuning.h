@@ -1,0 +1,56 @@
+/*
+ * garfield_tuning.h -- engine selection knobs of libgarfield, for tests and
+ * benchmarks. Results do not depend on them beyond floating-point rounding of
+ * the distance matrix; indices and aggregates keep the guarantees stated in
+ * garfield.h.
+ */
+#ifndef GARFIELD_TUNING_H
+#define GARFIELD_TUNING_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * Largest n for which pairwise distances use the direct-difference VALU
+ * engine; above it they use the MFMA Gram engine (Y = X - x_ref, fp32 MFMA).
+ * Valid range 1..GARFIELD_DIRECT_MAX_N_LIMIT (1 means: always MFMA for
+ * n >= 2). Returns the previous value, or -1 (and changes nothing) if the
+ * value is out of range. Process-wide; not synchronised with calls in flight.
+ */
+#define GARFIELD_DIRECT_MAX_N_LIMIT 20
+#define GARFIELD_DIRECT_MAX_N_DEFAULT 20
+int garfield_tuning_set_direct_max_n(int n);
+
+/* Engine the distance step would use for (n, d): 0 none (n < 2 or d == 0),
+ * 1 direct differences (VALU), 2 Gram (MFMA). */
+int garfield_tuning_distance_engine(int n, long long d);
+
+/* The reference row the Gram engine would shift the n x d device input x by
+ * (the row with the smallest sum of its ceil(n/2) nearest probe distances).
+ * Enqueues the probe on `stream`, waits for it and returns the index, or -1
+ * on error. Lets tests bound the Gram engine's cancellation error. */
+int garfield_tuning_gram_reference(const float* x, int n, long long d, void* stream);
+
+/*
+ * Per-kernel timing. While on, every call records a HIP event before and
+ * after each kernel it launches, on the call's stream. Turning it on or off
+ * (either way) waits for the device and drops the records collected so far.
+ * Returns the previous setting.
+ */
+int garfield_tuning_set_kernel_timing(int on);
+
+/*
+ * Waits for every recorded event and writes one line per kernel name,
+ * "name launches total_ms\n", in first-launch order, into buf (host memory,
+ * NUL-terminated, truncated to len-1 bytes). Returns the full length.
+ */
+size_t garfield_tuning_kernel_timing(char* buf, size_t len);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GARFIELD_TUNING_H */

@@ -1,0 +1,275 @@
+"""Garfield's robust gradient aggregation rules on MI355X (gfx950).
+
+Thin Python binding over ``libgarfield.so`` (C-ABI declared in
+``include/garfield.h``). It only marshals arguments: every step of every rule
+runs in the library's HIP kernels. PyTorch provides device memory (the input
+and output tensors) and the current stream; nothing here computes on the
+tensors. The interface mirrors the paper's ``init()`` / ``aggregate()`` pair
+(Section 3.3, Aggregation): ``gar(name, x, f)`` aggregates the n rows of an
+``n x d`` fp32 CUDA/HIP tensor.
+
+If the library has not been built, every call raises ``LibraryMissing``; there
+is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # first: libgarfield must bind to the HIP runtime torch has loaded
+
+__all__ = [
+    "GarfieldError", "LibraryMissing", "library_path", "load",
+    "pairwise_sqdist", "krum", "multikrum", "median", "bulyan", "mda", "average",
+    "multikrum_median", "gar", "workspace_bytes", "release", "set_direct_max_n",
+    "distance_engine", "gram_reference", "set_kernel_timing", "kernel_timing", "RULES",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libgarfield.so")
+
+OK, EINVAL, EREQ, ETOOBIG, ENOMEM, EHIP = range(6)
+RULE_IDS = {"dist": 0, "krum": 1, "multikrum": 2, "median": 3, "bulyan": 4, "mda": 5, "average": 6}
+NMAX = 64
+
+
+class LibraryMissing(RuntimeError):
+    pass
+
+
+class GarfieldError(RuntimeError):
+    def __init__(self, code: int, where: str, message: str):
+        super().__init__(f"{where}: {message} (status {code})")
+        self.code = code
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load():
+    """Load libgarfield.so (raises LibraryMissing if it is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise LibraryMissing(
+            f"{_LIB_PATH} is not built; run `python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+    st = ctypes.c_int
+    sig = {
+        "garfield_pairwise_sqdist": [vp, i32, i64, vp, vp],
+        "garfield_krum": [vp, i32, i32, i64, vp, vp, vp],
+        "garfield_multikrum": [vp, i32, i32, i64, i32, vp, vp, vp],
+        "garfield_median": [vp, i32, i32, i64, vp, i32, vp, vp],
+        "garfield_bulyan": [vp, i32, i32, i64, vp, vp, vp],
+        "garfield_mda": [vp, i32, i32, i64, vp, vp, vp],
+        "garfield_average": [vp, i32, i64, vp, vp],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = st
+    lib.garfield_workspace_bytes.argtypes = [i32, i32, i32, i64, i32]
+    lib.garfield_workspace_bytes.restype = ctypes.c_size_t
+    lib.garfield_release.argtypes = []
+    lib.garfield_release.restype = st
+    lib.garfield_strerror.argtypes = [st]
+    lib.garfield_strerror.restype = ctypes.c_char_p
+    lib.garfield_version.argtypes = []
+    lib.garfield_version.restype = ctypes.c_char_p
+    lib.garfield_tuning_set_direct_max_n.argtypes = [i32]
+    lib.garfield_tuning_set_direct_max_n.restype = i32
+    lib.garfield_tuning_distance_engine.argtypes = [i32, ctypes.c_longlong]
+    lib.garfield_tuning_distance_engine.restype = i32
+    lib.garfield_tuning_gram_reference.argtypes = [vp, i32, ctypes.c_longlong, vp]
+    lib.garfield_tuning_gram_reference.restype = i32
+    lib.garfield_tuning_set_kernel_timing.argtypes = [i32]
+    lib.garfield_tuning_set_kernel_timing.restype = i32
+    lib.garfield_tuning_kernel_timing.argtypes = [ctypes.c_char_p, ctypes.c_size_t]
+    lib.garfield_tuning_kernel_timing.restype = ctypes.c_size_t
+    _lib = lib
+    return lib
+
+
+def _check(code: int, where: str):
+    if code != OK:
+        msg = load().garfield_strerror(code).decode()
+        raise GarfieldError(code, where, msg)
+
+
+def _stream(x: torch.Tensor) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(x.device).cuda_stream)
+
+
+def _input(x: torch.Tensor) -> torch.Tensor:
+    if not isinstance(x, torch.Tensor) or x.dim() != 2:
+        raise ValueError("x must be a 2-D tensor (n vectors of d values)")
+    if x.device.type != "cuda":
+        raise ValueError("x must be on a GPU: this library has no CPU path")
+    if x.dtype != torch.float32:
+        raise ValueError("x must be float32")
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous (row-major n x d)")
+    return x
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def pairwise_sqdist(x: torch.Tensor) -> torch.Tensor:
+    """n x n fp64 squared Euclidean distances."""
+    x = _input(x)
+    n, d = x.shape
+    dist = torch.empty((n, n), dtype=torch.float64, device=x.device)
+    _check(load().garfield_pairwise_sqdist(_ptr(x), n, d, _ptr(dist), _stream(x)),
+           "garfield_pairwise_sqdist")
+    return dist
+
+
+def multikrum(x: torch.Tensor, f: int, m: int | None = None, aggregate: bool = True):
+    """(aggregate or None, sel) -- the m <= n-f vectors of lowest Krum score."""
+    x = _input(x)
+    n, d = x.shape
+    mm = (n - f) if (m is None or m <= 0) else m
+    sel = torch.empty(max(mm, 1), dtype=torch.int32, device=x.device)
+    out = torch.empty(d, dtype=torch.float32, device=x.device) if aggregate else None
+    _check(load().garfield_multikrum(_ptr(x), n, f, d, 0 if m is None else m, _ptr(out),
+                                     _ptr(sel), _stream(x)), "garfield_multikrum")
+    return out, sel[:mm]
+
+
+def krum(x: torch.Tensor, f: int):
+    """(aggregate, sel[1]) -- the vector of lowest Krum score."""
+    x = _input(x)
+    n, d = x.shape
+    sel = torch.empty(1, dtype=torch.int32, device=x.device)
+    out = torch.empty(d, dtype=torch.float32, device=x.device)
+    _check(load().garfield_krum(_ptr(x), n, f, d, _ptr(out), _ptr(sel), _stream(x)),
+           "garfield_krum")
+    return out, sel
+
+
+def median(x: torch.Tensor, f: int = 0, rows: torch.Tensor | None = None) -> torch.Tensor:
+    """Coordinate-wise median over all rows, or over `rows` (device int32)."""
+    x = _input(x)
+    n, d = x.shape
+    k = n
+    if rows is not None:
+        if rows.device != x.device or rows.dtype != torch.int32 or rows.dim() != 1:
+            raise ValueError("rows must be a 1-D int32 tensor on x's device")
+        rows = rows.contiguous()
+        k = rows.numel()
+    out = torch.empty(d, dtype=torch.float32, device=x.device)
+    _check(load().garfield_median(_ptr(x), n, f, d, _ptr(rows), k, _ptr(out), _stream(x)),
+           "garfield_median")
+    return out
+
+
+def bulyan(x: torch.Tensor, f: int):
+    """(aggregate, sel[n-2f])."""
+    x = _input(x)
+    n, d = x.shape
+    sel = torch.empty(max(n - 2 * f, 1), dtype=torch.int32, device=x.device)
+    out = torch.empty(d, dtype=torch.float32, device=x.device)
+    _check(load().garfield_bulyan(_ptr(x), n, f, d, _ptr(out), _ptr(sel), _stream(x)),
+           "garfield_bulyan")
+    return out, sel[: max(n - 2 * f, 0)]
+
+
+def mda(x: torch.Tensor, f: int, aggregate: bool = True):
+    """(aggregate or None, sel[n-f])."""
+    x = _input(x)
+    n, d = x.shape
+    sel = torch.empty(max(n - f, 1), dtype=torch.int32, device=x.device)
+    out = torch.empty(d, dtype=torch.float32, device=x.device) if aggregate else None
+    _check(load().garfield_mda(_ptr(x), n, f, d, _ptr(out), _ptr(sel), _stream(x)),
+           "garfield_mda")
+    return out, sel[: max(n - f, 0)]
+
+
+def average(x: torch.Tensor) -> torch.Tensor:
+    x = _input(x)
+    n, d = x.shape
+    out = torch.empty(d, dtype=torch.float32, device=x.device)
+    _check(load().garfield_average(_ptr(x), n, d, _ptr(out), _stream(x)), "garfield_average")
+    return out
+
+
+def multikrum_median(x: torch.Tensor, f: int, m: int | None = None):
+    """Multi-Krum selection, then the coordinate-wise median of the selected
+    rows (the selection stays on the device and feeds the median directly)."""
+    _, sel = multikrum(x, f, m, aggregate=False)
+    return median(x, f, rows=sel), sel
+
+
+RULES = {
+    "krum": lambda x, f, **kw: krum(x, f),
+    "multikrum": lambda x, f, m=None, **kw: multikrum(x, f, m),
+    "median": lambda x, f, rows=None, **kw: (median(x, f, rows), None),
+    "bulyan": lambda x, f, **kw: bulyan(x, f),
+    "mda": lambda x, f, **kw: mda(x, f),
+    "average": lambda x, f=0, **kw: (average(x), None),
+    "multikrum-median": lambda x, f, m=None, **kw: multikrum_median(x, f, m),
+}
+
+
+def gar(name: str, x: torch.Tensor, f: int, **kw):
+    """Aggregate the rows of x with rule `name`; returns (aggregate, selected indices or None)."""
+    try:
+        rule = RULES[name]
+    except KeyError:
+        raise ValueError(f"unknown rule {name!r}; known: {sorted(RULES)}") from None
+    return rule(x, f, **kw)
+
+
+def workspace_bytes(rule: str, n: int, f: int, d: int, m: int = 0) -> int:
+    return int(load().garfield_workspace_bytes(RULE_IDS[rule], n, f, d, m))
+
+
+def release():
+    _check(load().garfield_release(), "garfield_release")
+
+
+def set_direct_max_n(n: int) -> int:
+    old = load().garfield_tuning_set_direct_max_n(n)
+    if old < 0:
+        raise ValueError(f"direct_max_n out of range: {n}")
+    return old
+
+
+def gram_reference(x: torch.Tensor) -> int:
+    """Row the Gram engine shifts x by (synchronises the current stream)."""
+    x = _input(x)
+    n, d = x.shape
+    ref = load().garfield_tuning_gram_reference(_ptr(x), n, d, _stream(x))
+    if ref < 0:
+        raise GarfieldError(EHIP, "garfield_tuning_gram_reference", "probe failed")
+    return ref
+
+
+def set_kernel_timing(on: bool) -> bool:
+    """Record HIP events around every kernel launch (waits for the device)."""
+    return bool(load().garfield_tuning_set_kernel_timing(1 if on else 0))
+
+
+def kernel_timing() -> dict:
+    """{kernel name: (launches, total ms)} since timing was switched on."""
+    lib = load()
+    size = lib.garfield_tuning_kernel_timing(None, 0) + 1
+    buf = ctypes.create_string_buffer(size)
+    lib.garfield_tuning_kernel_timing(buf, size)
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, count, ms = line.split()
+        out[name] = (int(count), float(ms))
+    return out
+
+
+def distance_engine(n: int, d: int) -> str:
+    return {0: "none", 1: "direct", 2: "gram"}[load().garfield_tuning_distance_engine(n, d)]

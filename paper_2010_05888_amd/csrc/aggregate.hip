@@ -1,0 +1,279 @@
+// Streaming per-coordinate aggregation over HBM: one pass over the k rows an
+// aggregate needs, one write of d floats.
+//
+//  * mean of a row subset (Multi-Krum, MDA, Average; Krum is the 1-row case):
+//    fp64 sums in ascending row order, one rounding to fp32 at the end;
+//  * coordinate-wise median (Section 3.1 item 1): a branch-free selection
+//    network on k registers per coordinate (the paper's GPU median is built on
+//    a branchless 3-element sort, Section 4.3; on CDNA the min/max/med3
+//    instructions play that role and a pruned odd-even merge network replaces
+//    the selection loop);
+//  * Bulyan's aggregation (Section 3.1 item 4): a full sorting network on the
+//    theta selected values, the median, then the beta values closest to it
+//    under the key (|v - median|, v) -- in sorted order these form a window
+//    around the middle whose split is found by beta comparisons -- averaged.
+//
+// Row indices come from device memory (the selection kernels write them), so
+// no host round trip separates selection from aggregation.
+
+#include "device_common.h"
+#include "internal.h"
+#include "timing.h"
+
+namespace garfield {
+
+#include "networks.inc"
+
+namespace {
+
+__device__ __forceinline__ int64_t row_of(const int32_t* __restrict__ rows, int t, int n) {
+  if (!rows) return t;
+  const int r = rows[t];
+  return static_cast<int64_t>(r < 0 ? 0 : (r >= n ? n - 1 : r));
+}
+
+// ---------------------------------------------------------------------------
+template <int W>
+__global__ __launch_bounds__(kBlock) void k_mean_rows(const float* __restrict__ x, int n,
+                                                      int64_t d, const int32_t* __restrict__ rows,
+                                                      int k, float* __restrict__ out) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * W;
+  const double count = static_cast<double>(k);
+  for (int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W; c < d;
+       c += stride) {
+    double acc[W];
+#pragma unroll
+    for (int e = 0; e < W; ++e) acc[e] = 0.0;
+    const bool full = c + W <= d;
+    int t = 0;
+    for (; t + 8 <= k; t += 8) {
+      float v[8][W];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float* p = x + row_of(rows, t + u, n) * d + c;
+        if (full) load_w<W>(p, v[u]); else load_w_tail<W>(p, d - c, v[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int e = 0; e < W; ++e) acc[e] += static_cast<double>(v[u][e]);
+    }
+    for (; t < k; ++t) {
+      float v[W];
+      const float* p = x + row_of(rows, t, n) * d + c;
+      if (full) load_w<W>(p, v); else load_w_tail<W>(p, d - c, v);
+#pragma unroll
+      for (int e = 0; e < W; ++e) acc[e] += static_cast<double>(v[e]);
+    }
+    float o[W];
+#pragma unroll
+    for (int e = 0; e < W; ++e) o[e] = static_cast<float>(acc[e] / count);
+    if (full) {
+      store_w<W>(out + c, o);
+    } else {
+      for (int e = 0; e < W && c + e < d; ++e) out[c + e] = o[e];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+template <int K, int W>
+__global__ __launch_bounds__(kBlock) void k_median(const float* __restrict__ x, int n, int64_t d,
+                                                   const int32_t* __restrict__ rows,
+                                                   float* __restrict__ out) {
+  using Net = MedianNet<K>;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * W;
+  for (int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W; c < d;
+       c += stride) {
+    float v[K][W];
+    const bool full = c + W <= d;
+#pragma unroll
+    for (int t = 0; t < K; ++t) {
+      const float* p = x + row_of(rows, t, n) * d + c;
+      if (full) load_w<W>(p, v[t]); else load_w_tail<W>(p, d - c, v[t]);
+    }
+    float o[W];
+#pragma unroll
+    for (int e = 0; e < W; ++e) {
+      float a[K];
+#pragma unroll
+      for (int t = 0; t < K; ++t) a[t] = v[t][e];
+      Net::run(a);
+      if constexpr (K % 2 == 1) {
+        o[e] = a[Net::LO];
+      } else {  // mean of the two middle values, exact in fp64, rounded once
+        o[e] = static_cast<float>((static_cast<double>(a[Net::LO]) +
+                                   static_cast<double>(a[Net::HI])) * 0.5);
+      }
+    }
+    if (full) {
+      store_w<W>(out + c, o);
+    } else {
+      for (int e = 0; e < W && c + e < d; ++e) out[c + e] = o[e];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Bulyan aggregation for theta = T selected rows, beta = T - 2f closest.
+//
+// With s[0..T-1] sorted: odd T has the median s[c], c = (T-1)/2, always kept,
+// and K = beta-1 more to take; even T has med = (s[c-1]+s[c])/2, c = T/2, and
+// K = beta to take. Left candidates L_a = s[c-a] (a = 1, 2, ...) and right
+// candidates R_b (s[c+b] for odd T, s[c-1+b] for even T) are each ordered by
+// increasing key, so the K taken are the first K of their merge: L_a is taken
+// iff key(L_a) < key(R_{K+1-a}) (a missing R counts as +inf). The number of
+// left values taken is the count of such a.
+template <int T>
+__global__ __launch_bounds__(kBlock) void k_bulyan_agg(const float* __restrict__ x, int n,
+                                                       int64_t d, const int32_t* __restrict__ sel,
+                                                       int beta, float* __restrict__ out) {
+  using Net = SortNet<T>;
+  __shared__ float sorted[T * kBlock];
+  float* col = sorted + threadIdx.x;  // column of this thread: col[r * kBlock]
+  constexpr bool kOdd = (T % 2) == 1;
+  constexpr int c = kOdd ? (T - 1) / 2 : T / 2;
+  constexpr int n_left = c;                        // L_a exists for a <= n_left
+  constexpr int n_right = kOdd ? T - 1 - c : T - c;  // R_b exists for b <= n_right
+  const int K = kOdd ? beta - 1 : beta;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  for (int64_t cc = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; cc < d;
+       cc += stride) {
+    float v[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) v[t] = x[row_of(sel, t, n) * d + cc];
+    Net::run(v);
+#pragma unroll
+    for (int r = 0; r < T; ++r) col[r * kBlock] = v[Net::reg(r)];
+    const double med = kOdd ? static_cast<double>(col[c * kBlock])
+                            : (static_cast<double>(col[(c - 1) * kBlock]) +
+                               static_cast<double>(col[c * kBlock])) * 0.5;
+    int a_taken = 0;
+    for (int a = 1; a <= K; ++a) {
+      if (a > n_left) break;
+      const int b = K + 1 - a;
+      bool take = true;
+      if (b <= n_right) {
+        const float lv = col[(c - a) * kBlock];
+        const float rv = col[(kOdd ? c + b : c - 1 + b) * kBlock];
+        const double dl = med - static_cast<double>(lv);
+        const double dr = static_cast<double>(rv) - med;
+        take = (dl < dr) || (dl == dr && lv < rv);
+      }
+      if (!take) break;
+      a_taken = a;
+    }
+    const int lo = c - a_taken;
+    const int hi = lo + beta - 1;  // inclusive
+    double sum = 0.0;
+    for (int r = lo; r <= hi; ++r) sum += static_cast<double>(col[r * kBlock]);
+    out[cc] = static_cast<float>(sum / static_cast<double>(beta));
+  }
+}
+
+// ---------------------------------------------------------------------------
+int grid_for(int64_t items) {
+  int64_t blocks = (items + kBlock - 1) / kBlock;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < 1) blocks = 1;
+  return static_cast<int>(blocks);
+}
+
+template <int W>
+hipError_t launch_mean(const float* x, int n, int64_t d, const int32_t* rows, int k, float* out,
+                       hipStream_t s) {
+  {
+    TimedLaunch timed("mean_rows", s);
+    hipLaunchKernelGGL((k_mean_rows<W>), dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s, x, n,
+                       d, rows, k, out);
+  }
+  return hipGetLastError();
+}
+
+template <int K, int W>
+hipError_t launch_median_kw(const float* x, int n, int64_t d, const int32_t* rows, float* out,
+                            hipStream_t s) {
+  {
+    TimedLaunch timed("median", s);
+    hipLaunchKernelGGL((k_median<K, W>), dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s, x, n,
+                       d, rows, out);
+  }
+  return hipGetLastError();
+}
+
+template <int K>
+hipError_t launch_median_k(int width, const float* x, int n, int64_t d, const int32_t* rows,
+                           float* out, hipStream_t s) {
+  if constexpr (K <= 12) {
+    if (width == 4) return launch_median_kw<K, 4>(x, n, d, rows, out, s);
+  }
+  if constexpr (K <= 24) {
+    if (width >= 2) return launch_median_kw<K, 2>(x, n, d, rows, out, s);
+  }
+  return launch_median_kw<K, 1>(x, n, d, rows, out, s);
+}
+
+template <int K>
+hipError_t median_dispatch(int k, int width, const float* x, int n, int64_t d,
+                           const int32_t* rows, float* out, hipStream_t s) {
+  if constexpr (K > kNmax) {
+    return hipErrorInvalidValue;
+  } else {
+    if (k == K) return launch_median_k<K>(width, x, n, d, rows, out, s);
+    return median_dispatch<K + 1>(k, width, x, n, d, rows, out, s);
+  }
+}
+
+template <int T>
+hipError_t bulyan_dispatch(int theta, int beta, const float* x, int n, int64_t d,
+                           const int32_t* sel, float* out, hipStream_t s) {
+  if constexpr (T > kNmax) {
+    return hipErrorInvalidValue;
+  } else {
+    if (theta == T) {
+      {
+        TimedLaunch timed("bulyan_agg", s);
+        hipLaunchKernelGGL((k_bulyan_agg<T>), dim3(grid_for(d)), dim3(kBlock), 0, s, x, n, d, sel,
+                           beta, out);
+      }
+      return hipGetLastError();
+    }
+    return bulyan_dispatch<T + 1>(theta, beta, x, n, d, sel, out, s);
+  }
+}
+
+}  // namespace
+
+// Widest load both x (every row) and out support.
+int stream_width(const float* x, int64_t d, const float* out) {
+  int w = load_width(x, d);
+  const uintptr_t o = reinterpret_cast<uintptr_t>(out);
+  if (w == 4 && o % 16 != 0) w = 2;
+  if (w == 2 && o % 8 != 0) w = 1;
+  return w;
+}
+
+hipError_t enqueue_mean_rows(const float* x, int n, int64_t d, const int32_t* rows, int k,
+                             float* out, hipStream_t s) {
+  if (d == 0) return hipSuccess;
+  const int w = stream_width(x, d, out);
+  if (w == 4) return launch_mean<4>(x, n, d, rows, k, out, s);
+  if (w == 2) return launch_mean<2>(x, n, d, rows, k, out, s);
+  return launch_mean<1>(x, n, d, rows, k, out, s);
+}
+
+hipError_t enqueue_median(const float* x, int n, int64_t d, const int32_t* rows, int k,
+                          float* out, hipStream_t s) {
+  if (d == 0) return hipSuccess;
+  return median_dispatch<1>(k, stream_width(x, d, out), x, n, d, rows, out, s);
+}
+
+hipError_t enqueue_bulyan_aggregate(const float* x, int n, int f, int64_t d, const int32_t* sel,
+                                    float* out, hipStream_t s) {
+  if (d == 0) return hipSuccess;
+  const int theta = n - 2 * f;
+  const int beta = theta - 2 * f;
+  return bulyan_dispatch<1>(theta, beta, x, n, d, sel, out, s);
+}
+
+}  // namespace garfield

@@ -1,0 +1,54 @@
+// Device-side helpers shared by the libgarfield kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace garfield {
+
+typedef float f2 __attribute__((ext_vector_type(2)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+// min / max on finite values (inputs are finite by contract).
+__device__ __forceinline__ float fmin_(float a, float b) { return __builtin_fminf(a, b); }
+__device__ __forceinline__ float fmax_(float a, float b) { return __builtin_fmaxf(a, b); }
+
+// Load W consecutive floats (W in {1, 2, 4}); p must be W*4-byte aligned.
+template <int W>
+__device__ __forceinline__ void load_w(const float* __restrict__ p, float* v) {
+  if constexpr (W == 4) {
+    const f4 t = *reinterpret_cast<const f4*>(p);
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  } else if constexpr (W == 2) {
+    const f2 t = *reinterpret_cast<const f2*>(p);
+    v[0] = t.x; v[1] = t.y;
+  } else {
+    v[0] = *p;
+  }
+}
+
+template <int W>
+__device__ __forceinline__ void store_w(float* __restrict__ p, const float* v) {
+  if constexpr (W == 4) {
+    f4 t;
+    t.x = v[0]; t.y = v[1]; t.z = v[2]; t.w = v[3];
+    __builtin_nontemporal_store(t, reinterpret_cast<f4*>(p));
+  } else if constexpr (W == 2) {
+    f2 t;
+    t.x = v[0]; t.y = v[1];
+    __builtin_nontemporal_store(t, reinterpret_cast<f2*>(p));
+  } else {
+    __builtin_nontemporal_store(v[0], p);
+  }
+}
+
+// Guarded load of W consecutive floats: elements at or beyond `limit`
+// (relative to p) read as 0.
+template <int W>
+__device__ __forceinline__ void load_w_tail(const float* __restrict__ p, int64_t limit, float* v) {
+#pragma unroll
+  for (int e = 0; e < W; ++e) v[e] = (e < limit) ? p[e] : 0.0f;
+}
+
+}  // namespace garfield

@@ -1,0 +1,268 @@
+// C-ABI of libgarfield: argument validation (the requirements of Section 3.1
+// of the paper), the per-device workspace, and the launch sequence of each
+// aggregation rule on the caller's stream. See include/garfield.h.
+
+#include <hip/hip_runtime.h>
+
+#include <map>
+#include <mutex>
+
+#include "../../include/garfield.h"
+#include "../../include/garfield_tuning.h"
+#include "internal.h"
+#include "timing.h"
+
+namespace garfield {
+namespace {
+
+struct DeviceWorkspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+
+std::mutex g_mutex;
+std::map<int, DeviceWorkspace> g_workspaces;
+
+garfield_status to_status(hipError_t e) {
+  if (e == hipSuccess) return GARFIELD_OK;
+  (void)hipGetLastError();  // clear the sticky launch error for the next call
+  return GARFIELD_EHIP;
+}
+
+// Workspace of the current device with at least `need` bytes. Growing it
+// waits for the device to go idle before the old buffer is freed.
+garfield_status workspace(size_t need, void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return to_status(hipErrorInvalidDevice);
+  std::lock_guard<std::mutex> lock(g_mutex);
+  DeviceWorkspace& w = g_workspaces[dev];
+  if (w.bytes < need) {
+    if (w.ptr) {
+      if (hipDeviceSynchronize() != hipSuccess) return to_status(hipErrorUnknown);
+      (void)hipFree(w.ptr);
+      w.ptr = nullptr;
+      w.bytes = 0;
+    }
+    size_t alloc = need < (size_t{1} << 20) ? (size_t{1} << 20) : need;
+    alloc = (alloc + 0xFFFFF) & ~size_t{0xFFFFF};
+    if (hipMalloc(&w.ptr, alloc) != hipSuccess) {
+      (void)hipGetLastError();
+      w.ptr = nullptr;
+      return GARFIELD_ENOMEM;
+    }
+    w.bytes = alloc;
+  }
+  *out = w.ptr;
+  return GARFIELD_OK;
+}
+
+size_t align256(size_t b) { return (b + 255) & ~size_t{255}; }
+
+// Checks shared by every rule.
+garfield_status check_common(const float* x, int n, int f, int64_t d) {
+  if (n < 1 || f < 0 || d < 0) return GARFIELD_EINVAL;
+  if (d > 0 && !x) return GARFIELD_EINVAL;
+  if (n > GARFIELD_NMAX) return GARFIELD_ETOOBIG;
+  return GARFIELD_OK;
+}
+
+// Distance step. D goes to `dist` when given (n x n fp64, device), else into
+// the workspace; *dist_used receives where it went. `extra` bytes of scratch
+// follow the distance workspace and are returned in *extra_ptr.
+garfield_status run_distances(const float* x, int n, int64_t d, double* dist, size_t extra,
+                              double** dist_used, void** extra_ptr, hipStream_t s) {
+  const DistPlan plan = plan_distances(n, d, x);
+  const size_t dist_bytes = dist_workspace_bytes(plan);
+  void* base = nullptr;
+  garfield_status st = workspace(dist_bytes + align256(extra), &base);
+  if (st != GARFIELD_OK) return st;
+  DistWorkspace ws = carve_dist_workspace(plan, base);
+  if (dist) ws.dist = dist;
+  if (dist_used) *dist_used = ws.dist;
+  if (extra_ptr) *extra_ptr = static_cast<char*>(base) + dist_bytes;
+  return to_status(enqueue_distances(x, plan, ws, s));
+}
+
+static_assert(GARFIELD_NMAX == kNmax, "kernel limit and public limit differ");
+static_assert(GARFIELD_DIRECT_MAX_N_LIMIT == kDirectMaxNLimit, "direct engine limit differs");
+
+}  // namespace
+}  // namespace garfield
+
+using namespace garfield;
+
+extern "C" {
+
+garfield_status garfield_pairwise_sqdist(const float* x, int n, int64_t d, double* dist,
+                                         void* stream) {
+  garfield_status st = check_common(x, n, 0, d);
+  if (st != GARFIELD_OK) return st;
+  if (!dist) return GARFIELD_EINVAL;
+  return run_distances(x, n, d, dist, 0, nullptr, nullptr, static_cast<hipStream_t>(stream));
+}
+
+garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int m, float* out,
+                                   int32_t* sel, void* stream) {
+  garfield_status st = check_common(x, n, f, d);
+  if (st != GARFIELD_OK) return st;
+  if (!sel) return GARFIELD_EINVAL;
+  if (n < 2 * f + 3) return GARFIELD_EREQ;
+  if (m <= 0) m = n - f;
+  if (m > n - f) return GARFIELD_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  double* D = nullptr;
+  st = run_distances(x, n, d, nullptr, 0, &D, nullptr, s);
+  if (st != GARFIELD_OK) return st;
+  st = to_status(enqueue_krum_select(D, n, f, m, sel, s));
+  if (st != GARFIELD_OK || !out) return st;
+  return to_status(enqueue_mean_rows(x, n, d, sel, m, out, s));
+}
+
+garfield_status garfield_krum(const float* x, int n, int f, int64_t d, float* out, int32_t* sel,
+                              void* stream) {
+  return garfield_multikrum(x, n, f, d, 1, out, sel, stream);
+}
+
+garfield_status garfield_median(const float* x, int n, int f, int64_t d, const int32_t* rows,
+                                int k, float* out, void* stream) {
+  garfield_status st = check_common(x, n, f, d);
+  if (st != GARFIELD_OK) return st;
+  if (d > 0 && !out) return GARFIELD_EINVAL;
+  if (n < 2 * f + 1) return GARFIELD_EREQ;
+  if (rows) {
+    if (k < 1 || k > n) return GARFIELD_EINVAL;
+  } else {
+    k = n;
+  }
+  return to_status(enqueue_median(x, n, d, rows, k, out, static_cast<hipStream_t>(stream)));
+}
+
+garfield_status garfield_bulyan(const float* x, int n, int f, int64_t d, float* out,
+                                int32_t* sel, void* stream) {
+  garfield_status st = check_common(x, n, f, d);
+  if (st != GARFIELD_OK) return st;
+  if (!sel || (d > 0 && !out)) return GARFIELD_EINVAL;
+  if (n < 4 * f + 3) return GARFIELD_EREQ;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  double* D = nullptr;
+  st = run_distances(x, n, d, nullptr, 0, &D, nullptr, s);
+  if (st != GARFIELD_OK) return st;
+  st = to_status(enqueue_bulyan_select(D, n, f, sel, s));
+  if (st != GARFIELD_OK) return st;
+  return to_status(enqueue_bulyan_aggregate(x, n, f, d, sel, out, s));
+}
+
+garfield_status garfield_mda(const float* x, int n, int f, int64_t d, float* out, int32_t* sel,
+                             void* stream) {
+  garfield_status st = check_common(x, n, f, d);
+  if (st != GARFIELD_OK) return st;
+  if (!sel) return GARFIELD_EINVAL;
+  if (n < 2 * f + 1) return GARFIELD_EREQ;
+  const int64_t subsets = binomial(n, f);
+  if (subsets < 0 || subsets > GARFIELD_MDA_MAX_SUBSETS) return GARFIELD_ETOOBIG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  void* scratch = nullptr;
+  double* D = nullptr;
+  st = run_distances(x, n, d, nullptr, mda_scratch_bytes(n, f), &D, &scratch, s);
+  if (st != GARFIELD_OK) return st;
+  st = to_status(enqueue_mda_select(D, n, f, scratch, sel, s));
+  if (st != GARFIELD_OK || !out) return st;
+  return to_status(enqueue_mean_rows(x, n, d, sel, n - f, out, s));
+}
+
+garfield_status garfield_average(const float* x, int n, int64_t d, float* out, void* stream) {
+  garfield_status st = check_common(x, n, 0, d);
+  if (st != GARFIELD_OK) return st;
+  if (d > 0 && !out) return GARFIELD_EINVAL;
+  return to_status(enqueue_mean_rows(x, n, d, nullptr, n, out, static_cast<hipStream_t>(stream)));
+}
+
+size_t garfield_workspace_bytes(int rule, int n, int f, int64_t d, int m) {
+  (void)m;
+  if (n < 1 || n > GARFIELD_NMAX || f < 0 || d < 0) return 0;
+  // Plan for 4-byte-aligned rows: the narrowest loads give the most tiles, so
+  // this bounds every alignment of x.
+  const float* narrow = reinterpret_cast<const float*>(uintptr_t{4});
+  switch (rule) {
+    case GARFIELD_RULE_DIST:
+    case GARFIELD_RULE_KRUM:
+    case GARFIELD_RULE_MULTIKRUM:
+    case GARFIELD_RULE_BULYAN:
+      return dist_workspace_bytes(plan_distances(n, d, narrow));
+    case GARFIELD_RULE_MDA: {
+      const int64_t subsets = binomial(n, f);
+      if (n < 2 * f + 1 || subsets < 0 || subsets > GARFIELD_MDA_MAX_SUBSETS) return 0;
+      return dist_workspace_bytes(plan_distances(n, d, narrow)) +
+             align256(mda_scratch_bytes(n, f));
+    }
+    case GARFIELD_RULE_MEDIAN:
+    case GARFIELD_RULE_AVERAGE:
+      return 0;
+    default:
+      return 0;
+  }
+}
+
+garfield_status garfield_release(void) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return to_status(hipErrorInvalidDevice);
+  std::lock_guard<std::mutex> lock(g_mutex);
+  auto it = g_workspaces.find(dev);
+  if (it == g_workspaces.end() || !it->second.ptr) return GARFIELD_OK;
+  if (hipDeviceSynchronize() != hipSuccess) return to_status(hipErrorUnknown);
+  (void)hipFree(it->second.ptr);
+  g_workspaces.erase(it);
+  return GARFIELD_OK;
+}
+
+const char* garfield_strerror(garfield_status s) {
+  switch (s) {
+    case GARFIELD_OK: return "success";
+    case GARFIELD_EINVAL: return "invalid argument (null pointer, n < 1, f < 0, d < 0, m or k out of range)";
+    case GARFIELD_EREQ: return "n is below the rule's requirement in f";
+    case GARFIELD_ETOOBIG: return "problem too large (n > GARFIELD_NMAX or too many MDA subsets)";
+    case GARFIELD_ENOMEM: return "device workspace allocation failed";
+    case GARFIELD_EHIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* garfield_version(void) { return "garfield-mi355x 0.1"; }
+
+int garfield_tuning_set_direct_max_n(int n) {
+  if (n < 1 || n > GARFIELD_DIRECT_MAX_N_LIMIT) return -1;
+  const int old = direct_max_n();
+  set_direct_max_n(n);
+  return old;
+}
+
+int garfield_tuning_gram_reference(const float* x, int n, long long d, void* stream) {
+  if (check_common(x, n, 0, d) != GARFIELD_OK || n < 2 || d < 1) return -1;
+  DistPlan plan = plan_distances(n, d, x);
+  plan.engine = kEngineGram;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  void* base = nullptr;
+  if (workspace(dist_workspace_bytes(plan), &base) != GARFIELD_OK) return -1;
+  const DistWorkspace ws = carve_dist_workspace(plan, base);
+  if (enqueue_reference(x, plan, ws, s) != hipSuccess) return -1;
+  int32_t ref = -1;
+  if (hipMemcpyAsync(&ref, ws.ref, sizeof(ref), hipMemcpyDeviceToHost, s) != hipSuccess) return -1;
+  if (hipStreamSynchronize(s) != hipSuccess) return -1;
+  return ref;
+}
+
+int garfield_tuning_set_kernel_timing(int on) {
+  const int old = timing_enabled() ? 1 : 0;
+  timing_set(on != 0);
+  return old;
+}
+
+size_t garfield_tuning_kernel_timing(char* buf, size_t len) { return timing_summary(buf, len); }
+
+int garfield_tuning_distance_engine(int n, long long d) {
+  if (n < 1 || n > GARFIELD_NMAX || d < 0) return -1;
+  const float* aligned = reinterpret_cast<const float*>(uintptr_t{256});
+  return plan_distances(n, d, aligned).engine;
+}
+
+}  // extern "C"

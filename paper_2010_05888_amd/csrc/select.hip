@@ -1,0 +1,297 @@
+// Selection on the distance matrix D (n x n fp64, n <= 64): Krum / Multi-Krum
+// scores and top-m, Bulyan's iterated Krum, and MDA's subset search
+// (Section 3.1 items 2-4). All of it runs on the device so the selected
+// indices never round-trip through the host; every ranking breaks ties
+// towards the lower index and every sum is added in a fixed order.
+
+#include "device_common.h"
+#include "internal.h"
+#include "timing.h"
+
+namespace garfield {
+
+namespace {
+
+// order[i*n + r] = the j != i whose (D[i][j], j) has rank r in row i.
+// Scores then walk a row in ascending distance order, which is the order the
+// distances are added in (so identical rows get bit-identical scores).
+__device__ void load_and_rank(const double* __restrict__ dist, int n, double* D,
+                              unsigned char* order) {
+  for (int idx = threadIdx.x; idx < n * n; idx += blockDim.x) D[idx] = dist[idx];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < n * n; idx += blockDim.x) {
+    const int i = idx / n, j = idx % n;
+    if (i == j) continue;
+    const double v = D[idx];
+    int rank = 0;
+    for (int j2 = 0; j2 < n; ++j2) {
+      if (j2 == i) continue;
+      const double w = D[i * n + j2];
+      rank += (w < v) || (w == v && j2 < j);
+    }
+    order[i * n + rank] = static_cast<unsigned char>(j);
+  }
+  __syncthreads();
+}
+
+// Write the indices i < n with flag[i] set, ascending.
+__device__ void write_flagged(const int* flag, int n, int32_t* __restrict__ sel) {
+  const int i = threadIdx.x;
+  if (i < n && flag[i]) {
+    int pos = 0;
+    for (int j = 0; j < i; ++j) pos += flag[j];
+    sel[pos] = i;
+  }
+}
+
+// Multi-Krum: score(i) = sum of the k = n-f-2 smallest D[i][j], j != i; the
+// m lowest (score, i) are selected.
+__global__ __launch_bounds__(kBlock) void k_krum_select(const double* __restrict__ dist, int n,
+                                                        int f, int m, int32_t* __restrict__ sel) {
+  __shared__ double D[kNmax * kNmax];
+  __shared__ unsigned char order[kNmax * kNmax];
+  __shared__ double score[kNmax];
+  __shared__ int flag[kNmax];
+  load_and_rank(dist, n, D, order);
+  const int i = threadIdx.x;
+  const int k = n - f - 2;
+  if (i < n) {
+    double s = 0.0;
+    for (int r = 0; r < k; ++r) s += D[i * n + order[i * n + r]];
+    score[i] = s;
+  }
+  __syncthreads();
+  if (i < n) {
+    const double si = score[i];
+    int rank = 0;
+    for (int j = 0; j < n; ++j) rank += (score[j] < si) || (score[j] == si && j < i);
+    flag[i] = rank < m;
+  }
+  __syncthreads();
+  write_flagged(flag, n, sel);
+}
+
+// Bulyan's selection: theta = n-2f rounds; each round scores every remaining
+// vector against the other remaining ones with max(r-f-2, 0) neighbours
+// (r = vectors remaining) and moves the lowest (score, index) to the
+// selection. The ranking of each row is computed once; a round walks it and
+// skips vectors already selected.
+__global__ __launch_bounds__(kBlock) void k_bulyan_select(const double* __restrict__ dist, int n,
+                                                          int f, int32_t* __restrict__ sel) {
+  __shared__ double D[kNmax * kNmax];
+  __shared__ unsigned char order[kNmax * kNmax];
+  __shared__ double score[kNmax];
+  __shared__ int active[kNmax];
+  __shared__ int picked[kNmax];
+  load_and_rank(dist, n, D, order);
+  const int i = threadIdx.x;
+  if (i < n) {
+    active[i] = 1;
+    picked[i] = 0;
+  }
+  __syncthreads();
+  const int theta = n - 2 * f;
+  for (int round = 0; round < theta; ++round) {
+    const int remaining = n - round;
+    const int k = remaining - f - 2 > 0 ? remaining - f - 2 : 0;
+    if (i < n && active[i]) {
+      double s = 0.0;
+      int taken = 0;
+      for (int r = 0; r < n - 1 && taken < k; ++r) {
+        const int j = order[i * n + r];
+        if (active[j]) {
+          s += D[i * n + j];
+          ++taken;
+        }
+      }
+      score[i] = s;
+    }
+    __syncthreads();
+    if (i == 0) {
+      int best = -1;
+      for (int j = 0; j < n; ++j)
+        if (active[j] && (best < 0 || score[j] < score[best])) best = j;
+      active[best] = 0;
+      picked[best] = 1;
+    }
+    __syncthreads();
+  }
+  write_flagged(picked, n, sel);
+}
+
+// ---------------------------------------------------------------------------
+// MDA. Subsets of size s = n-f are ranked in lexicographic order; thread g
+// scans ranks [g*per, (g+1)*per) with a successor step, keeping the first
+// strictly smaller diameter; blocks then take the minimum (diameter, rank).
+
+__device__ int64_t binom_dev(int a, int b) {
+  if (b < 0 || b > a) return 0;
+  if (b > a - b) b = a - b;
+  int64_t c = 1;
+  for (int t = 1; t <= b; ++t) c = c * (a - b + t) / t;
+  return c;
+}
+
+// The rank-th s-subset of {0..n-1} in lexicographic order (rank < C(n, s)).
+// Every loop is bounded by n, so an out-of-range rank cannot hang a thread;
+// it yields the last subset instead.
+__device__ void unrank_subset(int64_t rank, int n, int s, unsigned char* idx) {
+  int e = 0;
+  for (int t = 0; t < s; ++t) {
+    const int last = n - s + t;  // largest element position t can hold
+    while (e < last) {
+      const int64_t cnt = binom_dev(n - e - 1, s - t - 1);
+      if (rank < cnt) break;
+      rank -= cnt;
+      ++e;
+    }
+    idx[t] = static_cast<unsigned char>(e);
+    ++e;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_mda_search(const double* __restrict__ dist, int n,
+                                                       int s, int64_t total, int64_t per,
+                                                       double* __restrict__ bdiam,
+                                                       int64_t* __restrict__ brank) {
+  __shared__ double D[kNmax * kNmax];
+  __shared__ unsigned char idx_all[kBlock * kNmax];
+  __shared__ double rd[kBlock];
+  __shared__ int64_t rr[kBlock];
+  for (int t = threadIdx.x; t < n * n; t += kBlock) D[t] = dist[t];
+  __syncthreads();
+  unsigned char* idx = idx_all + threadIdx.x * kNmax;
+  const int64_t g = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int64_t r0 = g * per;
+  const int64_t r1 = (r0 + per < total) ? r0 + per : total;
+  double best = __builtin_inf();
+  int64_t best_r = INT64_MAX;
+  if (r0 < total) {
+    unrank_subset(r0, n, s, idx);
+    for (int64_t r = r0; r < r1; ++r) {
+      double diam = 0.0;
+      for (int a = 0; a < s; ++a) {
+        const double* row = D + idx[a] * n;
+        for (int b = a + 1; b < s; ++b) {
+          const double v = row[idx[b]];
+          diam = v > diam ? v : diam;
+        }
+      }
+      if (diam < best) {
+        best = diam;
+        best_r = r;
+      }
+      // lexicographic successor
+      int t = s - 1;
+      while (t >= 0 && idx[t] == n - s + t) --t;
+      if (t < 0) break;
+      idx[t] = static_cast<unsigned char>(idx[t] + 1);
+      for (int u = t + 1; u < s; ++u) idx[u] = static_cast<unsigned char>(idx[u - 1] + 1);
+    }
+  }
+  rd[threadIdx.x] = best;
+  rr[threadIdx.x] = best_r;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double bd = rd[0];
+    int64_t br = rr[0];
+    for (int t = 1; t < kBlock; ++t)
+      if (rd[t] < bd || (rd[t] == bd && rr[t] < br)) {
+        bd = rd[t];
+        br = rr[t];
+      }
+    bdiam[blockIdx.x] = bd;
+    brank[blockIdx.x] = br;
+  }
+}
+
+__global__ __launch_bounds__(64) void k_mda_pick(const double* __restrict__ bdiam,
+                                                 const int64_t* __restrict__ brank, int blocks,
+                                                 int n, int s, int32_t* __restrict__ sel) {
+  __shared__ unsigned char idx[kNmax];
+  if (threadIdx.x == 0) {
+    double bd = bdiam[0];
+    int64_t br = brank[0];
+    for (int b = 1; b < blocks; ++b)
+      if (bdiam[b] < bd || (bdiam[b] == bd && brank[b] < br)) {
+        bd = bdiam[b];
+        br = brank[b];
+      }
+    unrank_subset(br, n, s, idx);
+  }
+  __syncthreads();
+  if (threadIdx.x < s) sel[threadIdx.x] = idx[threadIdx.x];
+}
+
+constexpr int64_t kMdaMaxBlocks = 1024;
+
+void mda_split(int n, int f, int64_t* total, int64_t* per, int* blocks) {
+  *total = binomial(n, f);
+  *per = (*total + kMdaMaxBlocks * kBlock - 1) / (kMdaMaxBlocks * kBlock);
+  if (*per < 1) *per = 1;
+  *blocks = static_cast<int>((*total + *per * kBlock - 1) / (*per * kBlock));
+}
+
+}  // namespace
+
+int64_t binomial(int a, int b) {
+  if (b < 0 || b > a) return 0;
+  if (b > a - b) b = a - b;
+  unsigned __int128 c = 1;
+  for (int t = 1; t <= b; ++t) {
+    c = c * static_cast<unsigned>(a - b + t) / static_cast<unsigned>(t);
+    if (c > (static_cast<unsigned __int128>(1) << 62)) return -1;
+  }
+  return static_cast<int64_t>(c);
+}
+
+int mda_blocks(int n, int f) {
+  int64_t total, per;
+  int blocks;
+  mda_split(n, f, &total, &per, &blocks);
+  return blocks;
+}
+
+size_t mda_scratch_bytes(int n, int f) {
+  return static_cast<size_t>(mda_blocks(n, f)) * (sizeof(double) + sizeof(int64_t));
+}
+
+hipError_t enqueue_krum_select(const double* dist, int n, int f, int m, int32_t* sel,
+                               hipStream_t s) {
+  {
+    TimedLaunch timed("krum_select", s);
+    hipLaunchKernelGGL(k_krum_select, dim3(1), dim3(kBlock), 0, s, dist, n, f, m, sel);
+  }
+  return hipGetLastError();
+}
+
+hipError_t enqueue_bulyan_select(const double* dist, int n, int f, int32_t* sel, hipStream_t s) {
+  {
+    TimedLaunch timed("bulyan_select", s);
+    hipLaunchKernelGGL(k_bulyan_select, dim3(1), dim3(kBlock), 0, s, dist, n, f, sel);
+  }
+  return hipGetLastError();
+}
+
+hipError_t enqueue_mda_select(const double* dist, int n, int f, void* scratch, int32_t* sel,
+                              hipStream_t s) {
+  int64_t total, per;
+  int blocks;
+  mda_split(n, f, &total, &per, &blocks);
+  double* bdiam = static_cast<double*>(scratch);
+  int64_t* brank = reinterpret_cast<int64_t*>(bdiam + blocks);
+  {
+    TimedLaunch timed("mda_search", s);
+    hipLaunchKernelGGL(k_mda_search, dim3(blocks), dim3(kBlock), 0, s, dist, n, n - f, total, per,
+                       bdiam, brank);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  {
+    TimedLaunch timed("mda_pick", s);
+    hipLaunchKernelGGL(k_mda_pick, dim3(1), dim3(64), 0, s, bdiam, brank, blocks, n, n - f, sel);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace garfield

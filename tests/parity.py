@@ -1,0 +1,136 @@
+"""Tolerances and decision-gap checks for GPU-vs-oracle parity.
+
+Distances. The library's D differs from the oracle's fp64 D only by fp32
+rounding inside a tile (everything across tiles is fp64). Per entry:
+
+* direct engine: each lane adds at most 16 squares (kDirectLaneCoords) into
+  an fp32 accumulator with one fused multiply-add each, after one rounded
+  fp32 subtraction; for positive terms that is a relative error of at most
+  (16 + 2) u, u = 2^-24.
+* Gram engine: Y = X - x_ref is rounded once (relative u on every y), and each
+  fp32 accumulator sums at most 4 MFMA k-slices of 4 products (16 products,
+  counted as up to 16 roundings, each at most u times the running sum of
+  absolute products) before it is added in fp64. With N_i = ||x_i - x_ref||^2
+  and sum |y_i y_j| <= (N_i + N_j)/2: |dG_ij| <= 8u (N_i + N_j) + u (N_i + N_j)
+  and |dN_i| <= 16u N_i + 2u N_i, so |dD_ij| <= (8*4 + 4) u (N_i + N_j).
+
+Decisions. A selection is "pinned" when every decision it makes is separated
+by more than the summed error bounds of the two quantities compared, so any
+D within those bounds makes the same decision; identical input rows are
+exact ties on both sides (broken by the lower index), and are not gaps.
+"""
+from __future__ import annotations
+
+from itertools import combinations
+
+import numpy as np
+
+U = 2.0 ** -24
+DIRECT_LANE_COORDS = 16
+EPS_DIRECT = (DIRECT_LANE_COORDS + 2) * U
+EPS_GRAM = (8 * 4 + 4) * U
+
+
+def agg_close(got, want):
+    """North-star aggregate tolerance: max(1e-5 |want|, 1e-6) per coordinate."""
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    tol = np.maximum(1e-5 * np.abs(want), 1e-6)
+    err = np.abs(got - want)
+    bad = np.nonzero(err > tol)[0]
+    return bad.size == 0, (int(bad[0]) if bad.size else -1), float(err.max(initial=0.0))
+
+
+def dist_bounds(D, engine, ref=None):
+    """n x n absolute error bounds on the library's D entries, from the oracle's
+    D (for the Gram engine N_i = ||x_i - x_ref||^2 is the oracle's D[i][ref])."""
+    n = D.shape[0]
+    if engine == "direct":
+        B = EPS_DIRECT * D
+    elif engine == "gram":
+        N = D[:, ref]
+        B = EPS_GRAM * (N[:, None] + N[None, :])
+    else:  # no distance kernel ran: D is exactly 0
+        B = np.zeros_like(D)
+    B = B + 1e-300
+    B[np.arange(n), np.arange(n)] = 0.0
+    return B
+
+
+def identical_rows(D):
+    """Rows i, j are identical iff the oracle's exact-difference D[i][j] is 0."""
+    return D == 0.0
+
+
+def _score_bounds(B, cand, k):
+    """Bound on |score error| of each candidate: sum of its k largest B."""
+    out = {}
+    for i in cand:
+        row = sorted((B[i, j] for j in cand if j != i), reverse=True)
+        out[i] = float(sum(row[:k]))
+    return out
+
+
+def krum_pinned(scores, B, f, m, same):
+    """Multi-Krum's selected set is decided beyond the error bounds."""
+    n = len(scores)
+    order = sorted(range(n), key=lambda i: (scores[i], i))
+    chosen, rest = order[:m], order[m:]
+    sb = _score_bounds(B, range(n), n - f - 2)
+    margin = np.inf
+    for a in chosen:
+        for b in rest:
+            if same[a, b]:
+                continue
+            margin = min(margin, (scores[b] - scores[a]) - (sb[a] + sb[b]))
+    return margin > 0, margin
+
+
+def bulyan_pinned(picks, round_scores, B, n, f, same):
+    remaining = list(range(n))
+    margin = np.inf
+    for r, w in enumerate(picks):
+        k = max(len(remaining) - f - 2, 0)
+        s = round_scores[r]
+        sb = _score_bounds(B, remaining, k)
+        for j in remaining:
+            if j == w or same[j, w]:
+                continue
+            margin = min(margin, (s[j] - s[w]) - (sb[j] + sb[w]))
+        remaining.remove(w)
+    return margin > 0, margin
+
+
+def mda_pinned(D, B, n, f, best_set):
+    """The lexicographically first minimum-diameter subset is decided beyond the bounds."""
+    s = n - f
+    best_set = tuple(int(i) for i in best_set)
+
+    def interval(S):
+        pairs = list(combinations(S, 2))
+        if not pairs:
+            return 0.0, 0.0, None
+        lo = max(D[i, j] - B[i, j] for i, j in pairs)
+        hi = max(D[i, j] + B[i, j] for i, j in pairs)
+        top = max(pairs, key=lambda p: D[p])
+        return lo, hi, top
+
+    _, best_hi, best_top = interval(best_set)
+    best = max((D[i, j] for i, j in combinations(best_set, 2)), default=0.0)
+    margin = np.inf
+    for S in combinations(range(n), s):
+        if S == best_set:
+            continue
+        diam = max((D[i, j] for i, j in combinations(S, 2)), default=0.0)
+        lo, hi, top = interval(S)
+        if diam > best:
+            margin = min(margin, lo - best_hi)
+        elif diam == best and S < best_set:
+            return False, -np.inf  # oracle would not have picked best_set
+        elif diam == best:
+            # an exact tie: both must have the same, clearly largest, pair
+            for T, t in ((S, top), (best_set, best_top)):
+                rest = [D[i, j] + B[i, j] for i, j in combinations(T, 2) if (i, j) != t]
+                if t != best_top or (rest and max(rest) >= D[t] - B[t]):
+                    return False, -np.inf
+    return margin > 0, margin

@@ -1,0 +1,115 @@
+"""The C-ABI library loads and exports every declared symbol (no GPU needed).
+
+Only calls that the library rejects during host-side validation are made
+here: they return before any HIP call, so nothing touches a device.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2010_05888_amd as gf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("garfield.h", "garfield_tuning.h")]
+
+
+def _declared():
+    names = set()
+    for h in HEADERS:
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names.update(re.findall(r"\b(garfield_\w+)\s*\(", text))
+    return sorted(names)
+
+
+def test_headers_declare_the_boundary():
+    names = _declared()
+    for required in ["garfield_pairwise_sqdist", "garfield_krum", "garfield_multikrum",
+                     "garfield_median", "garfield_bulyan", "garfield_mda"]:
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    assert os.path.exists(gf.library_path()), "libgarfield.so is not built"
+    lib = ctypes.CDLL(gf.library_path())
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return gf.load()
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation
+NULL = ctypes.c_void_p(0)
+
+
+def test_validation_codes(lib):
+    # garfield_krum(x, n, f, d, out, sel, stream)
+    assert lib.garfield_krum(FAKE, 0, 0, 10, FAKE, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_krum(FAKE, 6, 2, 10, FAKE, FAKE, NULL) == gf.EREQ   # n < 2f+3
+    assert lib.garfield_krum(FAKE, 65, 2, 10, FAKE, FAKE, NULL) == gf.ETOOBIG
+    assert lib.garfield_krum(NULL, 7, 1, 10, FAKE, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_krum(FAKE, 7, -1, 10, FAKE, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_krum(FAKE, 7, 1, -1, FAKE, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_krum(FAKE, 7, 1, 10, FAKE, NULL, NULL) == gf.EINVAL
+    # multikrum: m > n - f
+    assert lib.garfield_multikrum(FAKE, 7, 1, 10, 7, FAKE, FAKE, NULL) == gf.EINVAL
+    # median: n < 2f+1, k out of range with a row list, null out
+    assert lib.garfield_median(FAKE, 6, 3, 10, NULL, 0, FAKE, NULL) == gf.EREQ
+    assert lib.garfield_median(FAKE, 6, 1, 10, FAKE, 7, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_median(FAKE, 6, 1, 10, FAKE, 0, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_median(FAKE, 6, 1, 10, NULL, 0, NULL, NULL) == gf.EINVAL
+    # bulyan: n < 4f+3
+    assert lib.garfield_bulyan(FAKE, 10, 2, 10, FAKE, FAKE, NULL) == gf.EREQ
+    # mda: n < 2f+1, and C(n, f) above the cap
+    assert lib.garfield_mda(FAKE, 6, 3, 10, FAKE, FAKE, NULL) == gf.EREQ
+    assert lib.garfield_mda(FAKE, 64, 31, 10, FAKE, FAKE, NULL) == gf.ETOOBIG
+    # distances / average
+    assert lib.garfield_pairwise_sqdist(FAKE, 5, 10, NULL, NULL) == gf.EINVAL
+    assert lib.garfield_average(FAKE, 0, 10, FAKE, NULL) == gf.EINVAL
+
+
+def test_strerror_and_version(lib):
+    for code in range(6):
+        assert lib.garfield_strerror(code)
+    assert b"unknown" in lib.garfield_strerror(99)
+    assert lib.garfield_version().startswith(b"garfield")
+
+
+def test_workspace_bytes(lib):
+    assert gf.workspace_bytes("median", 64, 15, 10 ** 8) == 0
+    assert gf.workspace_bytes("krum", 0, 0, 10) == 0
+    small = gf.workspace_bytes("multikrum", 11, 2, 11_173_962)
+    big = gf.workspace_bytes("multikrum", 64, 15, 138_357_544)
+    assert 0 < small < 64 << 20 and 0 < big < 256 << 20
+    assert gf.workspace_bytes("mda", 10, 3, 25_557_032) > 0
+    assert gf.workspace_bytes("mda", 64, 31, 10) == 0
+
+
+def test_engine_selection(lib):
+    old = gf.set_direct_max_n(20)
+    try:
+        assert gf.distance_engine(1, 100) == "none"
+        assert gf.distance_engine(7, 0) == "none"
+        assert gf.distance_engine(19, 100) == "direct"
+        assert gf.distance_engine(21, 100) == "gram"
+        assert gf.set_direct_max_n(1) == 20
+        assert gf.distance_engine(2, 100) == "gram"
+        with pytest.raises(ValueError):
+            gf.set_direct_max_n(0)
+        with pytest.raises(ValueError):
+            gf.set_direct_max_n(21)
+    finally:
+        gf.set_direct_max_n(old)
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        gf.krum(torch.zeros((7, 10)), 1)
+    with pytest.raises(ValueError):
+        gf.median(torch.zeros((7, 10), dtype=torch.float64))
