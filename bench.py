@@ -99,13 +99,18 @@ def algorithmic(kernel, w):
     return None, None
 
 
-def cpu_baseline(w, x_host, seconds):
-    """Time the oracle on this host on a bounded sample of the input."""
+def cpu_baseline(w, x_dev, seconds):
+    """Time the oracle on this host on a bounded sample of the input (only the
+    sampled coordinates are copied to the host)."""
     import numpy as np
 
     import oracle
 
-    n, d = x_host.shape
+    n, d = x_dev.shape
+
+    def host_slice(width):
+        return np.ascontiguousarray(x_dev[:, :width].cpu().numpy())
+
     # the oracle is O(n^2 d) for distance rules: estimate from a small slice,
     # then run on a slice sized for about `seconds` of CPU work
     def run(xs):
@@ -125,10 +130,10 @@ def cpu_baseline(w, x_host, seconds):
         return time.perf_counter() - t
 
     probe_d = min(d, 1 << 16)
-    t_probe = run(np.ascontiguousarray(x_host[:, :probe_d]))
+    t_probe = run(host_slice(probe_d))
     per_coord = max(t_probe / probe_d, 1e-12)
     d_s = int(min(d, max(probe_d, seconds / per_coord)))
-    xs = np.ascontiguousarray(x_host[:, :d_s]) if d_s < d else x_host
+    xs = host_slice(d_s)
     reps, total = 0, 0.0
     while reps == 0 or (total < seconds and reps < 50):
         total += run(xs)
@@ -192,7 +197,7 @@ def bench_workload(key, args):
     base = None
     if args.cpu_seconds > 0:
         print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)
-        base = cpu_baseline(w, x.cpu().numpy(), args.cpu_seconds)
+        base = cpu_baseline(w, x, args.cpu_seconds)
 
     line = {
         "metric": "GAR input GB/s (n*d*4B/time) and % of HBM peak",

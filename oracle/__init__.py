@@ -50,10 +50,10 @@ def _load():
         c_int, c_i64 = ctypes.c_int, ctypes.c_int64
         lib.oracle_pairwise_sqdist.argtypes = [f32p, c_int, c_i64, f64p]
         lib.oracle_krum_scores.argtypes = [f32p, c_int, c_int, c_i64, f64p]
-        lib.oracle_multikrum.argtypes = [f32p, c_int, c_int, c_i64, c_int, f32p, i32p, f64p]
+        lib.oracle_multikrum.argtypes = [f32p, c_int, c_int, c_i64, c_int, f32p, i32p, f64p, f64p]
         lib.oracle_median.argtypes = [f32p, c_int, c_int, c_i64, i32p, c_int, f32p]
-        lib.oracle_bulyan.argtypes = [f32p, c_int, c_int, c_i64, f32p, i32p, i32p, f64p]
-        lib.oracle_mda.argtypes = [f32p, c_int, c_int, c_i64, f32p, i32p, f64p, f64p, i64p]
+        lib.oracle_bulyan.argtypes = [f32p, c_int, c_int, c_i64, f32p, i32p, i32p, f64p, f64p]
+        lib.oracle_mda.argtypes = [f32p, c_int, c_int, c_i64, f32p, i32p, f64p, f64p, i64p, f64p]
         for fn in (lib.oracle_pairwise_sqdist, lib.oracle_krum_scores, lib.oracle_multikrum,
                    lib.oracle_median, lib.oracle_bulyan, lib.oracle_mda):
             fn.restype = ctypes.c_int
@@ -104,19 +104,26 @@ def krum_scores(x, f: int) -> np.ndarray:
     return s
 
 
-def multikrum(x, f: int, m: int | None = None, return_scores: bool = False):
-    """(aggregate fp32 [d], sel int32 [m] ascending[, scores fp64 [n]])."""
+def multikrum(x, f: int, m: int | None = None, return_scores: bool = False,
+              return_distances: bool = False):
+    """(aggregate fp32 [d], sel int32 [m] ascending[, scores fp64 [n]][, D fp64 [n, n]])."""
     x = _rows(x)
     n, d = x.shape
     mm = (n - f) if (m is None or m <= 0) else m
     out = np.zeros(d, dtype=np.float32)
     sel = np.zeros(max(mm, 1), dtype=np.int32)
     scores = np.zeros(n, dtype=np.float64)
+    D = np.zeros((n, n), dtype=np.float64)
     _check(_load().oracle_multikrum(_ptr(x, ctypes.c_float), n, f, d, 0 if m is None else m,
                                     _ptr(out, ctypes.c_float), _ptr(sel, ctypes.c_int32),
-                                    _ptr(scores, ctypes.c_double)), "multikrum")
-    sel = sel[:mm]
-    return (out, sel, scores) if return_scores else (out, sel)
+                                    _ptr(scores, ctypes.c_double), _ptr(D, ctypes.c_double)),
+           "multikrum")
+    res = (out, sel[:mm])
+    if return_scores:
+        res += (scores,)
+    if return_distances:
+        res += (D,)
+    return res
 
 
 def krum(x, f: int, return_scores: bool = False):
@@ -138,8 +145,8 @@ def median(x, f: int = 0, rows=None) -> np.ndarray:
     return out
 
 
-def bulyan(x, f: int, return_rounds: bool = False):
-    """(aggregate, sel ascending[, picks in order, round scores theta x n])."""
+def bulyan(x, f: int, return_rounds: bool = False, return_distances: bool = False):
+    """(aggregate, sel ascending[, picks in order, round scores theta x n][, D])."""
     x = _rows(x)
     n, d = x.shape
     theta = n - 2 * f
@@ -147,16 +154,20 @@ def bulyan(x, f: int, return_rounds: bool = False):
     sel = np.zeros(max(theta, 1), dtype=np.int32)
     picks = np.zeros(max(theta, 1), dtype=np.int32)
     rs = np.zeros((max(theta, 1), n), dtype=np.float64)
+    D = np.zeros((n, n), dtype=np.float64)
     _check(_load().oracle_bulyan(_ptr(x, ctypes.c_float), n, f, d, _ptr(out, ctypes.c_float),
                                  _ptr(sel, ctypes.c_int32), _ptr(picks, ctypes.c_int32),
-                                 _ptr(rs, ctypes.c_double)), "bulyan")
+                                 _ptr(rs, ctypes.c_double), _ptr(D, ctypes.c_double)), "bulyan")
+    res = (out, sel[:theta])
     if return_rounds:
-        return out, sel[:theta], picks[:theta], rs[:theta]
-    return out, sel[:theta]
+        res += (picks[:theta], rs[:theta])
+    if return_distances:
+        res += (D,)
+    return res
 
 
-def mda(x, f: int, return_diameters: bool = False):
-    """(aggregate, sel ascending[, best diameter, next larger diameter, #subsets at best])."""
+def mda(x, f: int, return_diameters: bool = False, return_distances: bool = False):
+    """(aggregate, sel ascending[, best diameter, next larger diameter, #subsets at best][, D])."""
     x = _rows(x)
     n, d = x.shape
     out = np.zeros(d, dtype=np.float32)
@@ -164,9 +175,14 @@ def mda(x, f: int, return_diameters: bool = False):
     best = np.zeros(1, dtype=np.float64)
     second = np.zeros(1, dtype=np.float64)
     nbest = np.zeros(1, dtype=np.int64)
+    D = np.zeros((n, n), dtype=np.float64)
     _check(_load().oracle_mda(_ptr(x, ctypes.c_float), n, f, d, _ptr(out, ctypes.c_float),
                               _ptr(sel, ctypes.c_int32), _ptr(best, ctypes.c_double),
-                              _ptr(second, ctypes.c_double), _ptr(nbest, ctypes.c_int64)), "mda")
+                              _ptr(second, ctypes.c_double), _ptr(nbest, ctypes.c_int64),
+                              _ptr(D, ctypes.c_double)), "mda")
+    res = (out, sel[:n - f])
     if return_diameters:
-        return out, sel[:n - f], float(best[0]), float(second[0]), int(nbest[0])
-    return out, sel[:n - f]
+        res += (float(best[0]), float(second[0]), int(nbest[0]))
+    if return_distances:
+        res += (D,)
+    return res

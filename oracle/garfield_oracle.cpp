@@ -135,15 +135,16 @@ int oracle_krum_scores(const float* x, int n, int f, int64_t d, double* scores) 
 
 // Multi-Krum (Section 3.1 item 2): the m rows with the lowest (score, index),
 // then their mean. m <= 0 selects the default n - f. Krum is m = 1.
-// `scores` (n fp64) is optional.
+// `scores` (n fp64) and `D_out` (n*n fp64, the distance matrix) are optional.
 int oracle_multikrum(const float* x, int n, int f, int64_t d, int m, float* out,
-                     int32_t* sel, double* scores) {
+                     int32_t* sel, double* scores, double* D_out) {
   if (n < 1 || f < 0 || d < 0 || !sel || (d > 0 && (!x || !out))) return kInval;
   if (n < 2 * f + 3) return kReq;
   if (m <= 0) m = n - f;
   if (m > n - f) return kInval;
   std::vector<double> D(static_cast<size_t>(n) * n);
   distance_matrix(x, n, d, D.data());
+  if (D_out) std::copy(D.begin(), D.end(), D_out);
   std::vector<int> all(n);
   for (int i = 0; i < n; ++i) all[i] = i;
   std::vector<std::pair<double, int>> ranked;
@@ -194,15 +195,17 @@ int oracle_median(const float* x, int n, int f, int64_t d, const int32_t* rows, 
 // Bulyan (Section 3.1 item 4, reading R6). `sel` receives the theta selected
 // rows in ascending order; `picks` (optional, theta entries) the same rows in
 // the order they were picked; `round_scores` (optional, theta*n fp64) the
-// Krum score of every row in each round, +inf for rows already picked.
+// Krum score of every row in each round, +inf for rows already picked;
+// `D_out` (optional, n*n fp64) the distance matrix.
 int oracle_bulyan(const float* x, int n, int f, int64_t d, float* out, int32_t* sel,
-                  int32_t* picks, double* round_scores) {
+                  int32_t* picks, double* round_scores, double* D_out) {
   if (n < 1 || f < 0 || d < 0 || !sel || (d > 0 && (!x || !out))) return kInval;
   if (n < 4 * f + 3) return kReq;
   const int theta = n - 2 * f;
   const int beta = theta - 2 * f;
   std::vector<double> D(static_cast<size_t>(n) * n);
   distance_matrix(x, n, d, D.data());
+  if (D_out) std::copy(D.begin(), D.end(), D_out);
   std::vector<int> remaining(n);
   for (int i = 0; i < n; ++i) remaining[i] = i;
   std::vector<int> chosen;
@@ -251,14 +254,16 @@ int oracle_bulyan(const float* x, int n, int f, int64_t d, float* out, int32_t* 
 // Minimum-diameter averaging (Section 3.1 item 3, reading R7). `best_diam`
 // and `second_diam` (optional) receive the smallest diameter and the smallest
 // diameter strictly larger than it (+inf if none). `n_best` (optional)
-// receives how many subsets reach the smallest diameter.
+// receives how many subsets reach the smallest diameter; `D_out` (optional,
+// n*n fp64) the distance matrix.
 int oracle_mda(const float* x, int n, int f, int64_t d, float* out, int32_t* sel,
-               double* best_diam, double* second_diam, int64_t* n_best) {
+               double* best_diam, double* second_diam, int64_t* n_best, double* D_out) {
   if (n < 1 || f < 0 || d < 0 || !sel || (d > 0 && (!x || !out))) return kInval;
   if (n < 2 * f + 1) return kReq;
   const int s = n - f;
   std::vector<double> D(static_cast<size_t>(n) * n);
   distance_matrix(x, n, d, D.data());
+  if (D_out) std::copy(D.begin(), D.end(), D_out);
   // Lexicographic enumeration of s-subsets of {0..n-1}.
   std::vector<int> idx(s);
   for (int t = 0; t < s; ++t) idx[t] = t;

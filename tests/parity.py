@@ -62,41 +62,70 @@ def identical_rows(D):
     return D == 0.0
 
 
-def _score_bounds(B, cand, k):
-    """Bound on |score error| of each candidate: sum of its k largest B."""
+def _score_intervals(D, B, cand, k):
+    """Interval [lo, hi] holding the library's Krum score of each candidate.
+
+    With N_i the oracle's k nearest of i among cand, the library sums its own
+    k smallest perturbed distances, which is at most sum_{j in N_i} (D+B) and
+    at least the sum of the k smallest (D-B).
+    """
     out = {}
     for i in cand:
-        row = sorted((B[i, j] for j in cand if j != i), reverse=True)
-        out[i] = float(sum(row[:k]))
+        others = [j for j in cand if j != i]
+        near = sorted(others, key=lambda j: (D[i, j], j))[:k]
+        hi = float(sum(D[i, j] + B[i, j] for j in near))
+        lo = float(sum(sorted(D[i, j] - B[i, j] for j in others)[:k]))
+        out[i] = (lo, hi, near)
     return out
 
 
-def krum_pinned(scores, B, f, m, same):
+def _structural_tie(D, B, a, b, k, cand, same):
+    """Oracle scores of a and b are equal, and so are the library's."""
+    if same[a, b] or k == 0:
+        return True
+    if k != 1:
+        return False
+    # mutual nearest neighbours: both scores are the one entry D[a][b], which
+    # the library stores symmetrically; it must be clearly the nearest of each
+    for i, j in ((a, b), (b, a)):
+        rest = [D[i, t] - B[i, t] for t in cand if t not in (i, j)]
+        if rest and D[i, j] + B[i, j] >= min(rest):
+            return False
+    return True
+
+
+def _pair_margin(sc, iv, a, b, D, B, k, cand, same):
+    """Margin by which a (ranked first) is decided before b."""
+    if sc[a] == sc[b]:
+        return np.inf if _structural_tie(D, B, a, b, k, cand, same) else -np.inf
+    return iv[b][0] - iv[a][1]
+
+
+def krum_pinned(scores, D, B, f, m, same):
     """Multi-Krum's selected set is decided beyond the error bounds."""
     n = len(scores)
+    k = n - f - 2
     order = sorted(range(n), key=lambda i: (scores[i], i))
     chosen, rest = order[:m], order[m:]
-    sb = _score_bounds(B, range(n), n - f - 2)
+    iv = _score_intervals(D, B, range(n), k)
     margin = np.inf
     for a in chosen:
         for b in rest:
-            if same[a, b]:
-                continue
-            margin = min(margin, (scores[b] - scores[a]) - (sb[a] + sb[b]))
+            margin = min(margin, _pair_margin(scores, iv, a, b, D, B, k, range(n), same))
     return margin > 0, margin
 
 
-def bulyan_pinned(picks, round_scores, B, n, f, same):
+def bulyan_pinned(picks, round_scores, D, B, n, f, same):
     remaining = list(range(n))
     margin = np.inf
     for r, w in enumerate(picks):
         k = max(len(remaining) - f - 2, 0)
         s = round_scores[r]
-        sb = _score_bounds(B, remaining, k)
+        iv = _score_intervals(D, B, remaining, k)
         for j in remaining:
-            if j == w or same[j, w]:
+            if j == w:
                 continue
-            margin = min(margin, (s[j] - s[w]) - (sb[j] + sb[w]))
+            margin = min(margin, _pair_margin(s, iv, w, j, D, B, k, remaining, same))
         remaining.remove(w)
     return margin > 0, margin
 

@@ -115,10 +115,10 @@ def _pinned_inputs(key, d, max_tries=25):
             if rule in ("krum", "multikrum", "multikrum-median"):
                 m = 1 if rule == "krum" else (w.m or w.n - w.f)
                 _, _, sc = oracle.multikrum(x, w.f, m, return_scores=True)
-                ok &= parity.krum_pinned(sc, B, w.f, m, same)[0]
+                ok &= parity.krum_pinned(sc, Do, B, w.f, m, same)[0]
             elif rule == "bulyan":
                 _, _, picks, rs = oracle.bulyan(x, w.f, return_rounds=True)
-                ok &= parity.bulyan_pinned(picks, rs, B, w.n, w.f, same)[0]
+                ok &= parity.bulyan_pinned(picks, rs, Do, B, w.n, w.f, same)[0]
             elif rule == "mda":
                 _, sel = oracle.mda(x, w.f)
                 ok &= parity.mda_pinned(Do, B, w.n, w.f, sel)[0]
@@ -240,7 +240,7 @@ def test_bulyan_shapes(n, f):
     Do = oracle.pairwise_sqdist(x)
     B, _ = _bounds(x, xt, Do)
     oo, so, picks, rs = oracle.bulyan(x, f, return_rounds=True)
-    if not parity.bulyan_pinned(picks, rs, B, n, f, parity.identical_rows(Do))[0]:
+    if not parity.bulyan_pinned(picks, rs, Do, B, n, f, parity.identical_rows(Do))[0]:
         pytest.skip("selection not pinned at this seed")
     out, sel = gf.bulyan(xt, f)
     assert sel.cpu().numpy().tolist() == so.tolist()
@@ -287,7 +287,7 @@ def test_multikrum_m_range(m):
     _, _, sc = oracle.multikrum(x, w.f, m, return_scores=True)
     Do = oracle.pairwise_sqdist(x)
     B, _ = _bounds(x, xt, Do)
-    if not parity.krum_pinned(sc, B, w.f, m, parity.identical_rows(Do))[0]:
+    if not parity.krum_pinned(sc, Do, B, w.f, m, parity.identical_rows(Do))[0]:
         pytest.skip("not pinned for this m")
     out, sel = gf.multikrum(xt, w.f, m)
     oo, so = oracle.multikrum(x, w.f, m)
