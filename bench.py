@@ -39,7 +39,33 @@ def _parse():
                     help="target CPU time of the oracle baseline (0 disables it)")
     ap.add_argument("--direct-max-n", type=int, default=None,
                     help="override the direct/Gram distance engine threshold")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="time a plain 1 GiB device-to-device copy instead (HBM calibration "
+                         "and the reference for the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
+
+
+def calibrate_copy(args):
+    """A plain device copy of a known size: achieved HBM rate, and the bytes the
+    memory counters should report for it (1 GiB read + 1 GiB written)."""
+    import torch
+
+    nbytes = 1 << 30
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda:0").uniform_()
+    dst = torch.empty_like(src)
+    for _ in range(args.warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        dst.copy_(src)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    return {"calibration": "device copy", "bytes_read": nbytes, "bytes_written": nbytes,
+            "ms": round(ms, 6), "GBps_read_plus_write": round(2 * nbytes / (ms * 1e-3) / 1e9, 2),
+            "steps": args.steps}
 
 
 class Step:
@@ -97,6 +123,24 @@ def algorithmic(kernel, w):
     if kernel == "bulyan_agg":
         return "hbm", 4.0 * (n - 2 * f + 1) * d
     return None, None
+
+
+def measured_traffic(kernel, key):
+    """HBM bytes per launch from the committed counter profile, or None when
+    there is none for this kernel and workload or its source changed since."""
+    import hashlib
+
+    root = os.path.dirname(os.path.abspath(__file__))
+    try:
+        with open(os.path.join(root, "profiles", "traffic.json")) as fh:
+            entry = json.load(fh).get(kernel)
+        if not entry or entry["workload"] != key:
+            return None
+        with open(os.path.join(root, entry["source"]), "rb") as fh:
+            digest = hashlib.sha256(fh.read()).hexdigest()[:16]
+        return entry["bytes_per_launch"] if digest == entry["source_sha256"] else None
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(w, x_dev, seconds):
@@ -187,8 +231,8 @@ def bench_workload(key, args):
     bound, per_launch = algorithmic(dominant, w)
     avg_ms = kt[dominant][1] / kt[dominant][0]
     roofline = {"kernel": dominant, "bound": bound, "achieved": None, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": None, "traffic": None, "avg_ms": round(avg_ms, 6),
-                "bytes_per_launch": per_launch}
+                "unit": "GB/s", "frac": None, "traffic": measured_traffic(dominant, key),
+                "avg_ms": round(avg_ms, 6), "bytes_per_launch": per_launch}
     if per_launch:
         achieved = per_launch / (avg_ms * 1e-3) / 1e9
         roofline["achieved"] = round(achieved, 2)
@@ -238,6 +282,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.calibrate_copy:
+        print(json.dumps(calibrate_copy(args)), flush=True)
+        return
     gf.load()  # fails loudly when the library is not built
     if args.direct_max_n is not None:
         gf.set_direct_max_n(args.direct_max_n)
