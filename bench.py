@@ -25,6 +25,7 @@ import sys
 import time
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
+INPUT_RING_BYTES = 4 << 30   # inputs smaller than this are alternated between two copies
 FP32_MFMA_PEAK_TFLOPS = 157.3
 
 
@@ -201,16 +202,25 @@ def bench_workload(key, args):
     print(f"[bench] workload {key}: {w.name}: generating", file=sys.stderr, flush=True)
     inp = synth.generate(w, dev)
     x = inp.x
+    # Consecutive steps alternate between two copies of the input when it is
+    # small enough for a step to find the previous step's data still in the
+    # 256 MB Infinity Cache: every step then starts from HBM, as a step on
+    # fresh gradients would. (Reuse within a step is kept.)
+    copies = [x] if x.numel() * 4 >= INPUT_RING_BYTES else [x, x.clone()]
     torch.cuda.synchronize()
-    step = Step(gf, w, x)
-    for _ in range(args.warmup):
-        step()
+    steps = [Step(gf, w, xi) for xi in copies]
+
+    def step_k(k):
+        steps[k % len(steps)]()
+
+    for k in range(args.warmup):
+        step_k(k)
     torch.cuda.synchronize()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     start.record()
-    for _ in range(args.steps):
-        step()
+    for k in range(args.steps):
+        step_k(args.warmup + k)
     end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -221,8 +231,8 @@ def bench_workload(key, args):
 
     # second pass of the same steps with per-kernel HIP events
     gf.set_kernel_timing(True)
-    for _ in range(args.steps):
-        step()
+    for k in range(args.steps):
+        step_k(args.warmup + args.steps + k)
     torch.cuda.synchronize()
     kt = gf.kernel_timing()
     gf.set_kernel_timing(False)
@@ -259,12 +269,13 @@ def bench_workload(key, args):
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "config": {"workload": w.name, "rules": list(w.rules), "n": w.n, "f": w.f, "d": w.d,
                    "m": w.m, "seed": w.seed, "byzantine_rows": inp.byzantine,
-                   "distance_engine": gf.distance_engine(w.n, w.d)},
+                   "distance_engine": gf.distance_engine(w.n, w.d),
+                   "input_copies": len(copies)},
         "kernels": kernels,
         "roofline": roofline,
         "cpu_baseline": base,
     }
-    del x, inp, step
+    del x, inp, steps, copies
     torch.cuda.empty_cache()
     return line
 

@@ -124,7 +124,7 @@ __global__ __launch_bounds__(kBlock) void k_median(const float* __restrict__ x, 
 // increasing key, so the K taken are the first K of their merge: L_a is taken
 // iff key(L_a) < key(R_{K+1-a}) (a missing R counts as +inf). The number of
 // left values taken is the count of such a.
-template <int T>
+template <int T, int W>
 __global__ __launch_bounds__(kBlock) void k_bulyan_agg(const float* __restrict__ x, int n,
                                                        int64_t d, const int32_t* __restrict__ sel,
                                                        int beta, float* __restrict__ out) {
@@ -133,48 +133,64 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_agg(const float* __restrict__
   float* col = sorted + threadIdx.x;  // column of this thread: col[r * kBlock]
   constexpr bool kOdd = (T % 2) == 1;
   constexpr int c = kOdd ? (T - 1) / 2 : T / 2;
-  constexpr int n_left = c;                        // L_a exists for a <= n_left
+  constexpr int n_left = c;                          // L_a exists for a <= n_left
   constexpr int n_right = kOdd ? T - 1 - c : T - c;  // R_b exists for b <= n_right
   const int K = kOdd ? beta - 1 : beta;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-  for (int64_t cc = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; cc < d;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * W;
+  for (int64_t cc = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W; cc < d;
        cc += stride) {
-    float v[T];
+    float v[T][W];
+    const bool full = cc + W <= d;
 #pragma unroll
-    for (int t = 0; t < T; ++t) v[t] = x[row_of(sel, t, n) * d + cc];
-    Net::run(v);
-#pragma unroll
-    for (int r = 0; r < T; ++r) col[r * kBlock] = v[Net::reg(r)];
-    const double med = kOdd ? static_cast<double>(col[c * kBlock])
-                            : (static_cast<double>(col[(c - 1) * kBlock]) +
-                               static_cast<double>(col[c * kBlock])) * 0.5;
-    int a_taken = 0;
-    for (int a = 1; a <= K; ++a) {
-      if (a > n_left) break;
-      const int b = K + 1 - a;
-      bool take = true;
-      if (b <= n_right) {
-        const float lv = col[(c - a) * kBlock];
-        const float rv = col[(kOdd ? c + b : c - 1 + b) * kBlock];
-        const double dl = med - static_cast<double>(lv);
-        const double dr = static_cast<double>(rv) - med;
-        take = (dl < dr) || (dl == dr && lv < rv);
-      }
-      if (!take) break;
-      a_taken = a;
+    for (int t = 0; t < T; ++t) {
+      const float* p = x + row_of(sel, t, n) * d + cc;
+      if (full) load_w<W>(p, v[t]); else load_w_tail<W>(p, d - cc, v[t]);
     }
-    const int lo = c - a_taken;
-    const int hi = lo + beta - 1;  // inclusive
-    double sum = 0.0;
-    for (int r = lo; r <= hi; ++r) sum += static_cast<double>(col[r * kBlock]);
-    out[cc] = static_cast<float>(sum / static_cast<double>(beta));
+    float o[W];
+#pragma unroll
+    for (int e = 0; e < W; ++e) {
+      float a[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) a[t] = v[t][e];
+      Net::run(a);
+#pragma unroll
+      for (int r = 0; r < T; ++r) col[r * kBlock] = a[Net::reg(r)];
+      const double med = kOdd ? static_cast<double>(col[c * kBlock])
+                              : (static_cast<double>(col[(c - 1) * kBlock]) +
+                                 static_cast<double>(col[c * kBlock])) * 0.5;
+      int a_taken = 0;
+      for (int i = 1; i <= K; ++i) {
+        if (i > n_left) break;
+        const int b = K + 1 - i;
+        bool take = true;
+        if (b <= n_right) {
+          const float lv = col[(c - i) * kBlock];
+          const float rv = col[(kOdd ? c + b : c - 1 + b) * kBlock];
+          const double dl = med - static_cast<double>(lv);
+          const double dr = static_cast<double>(rv) - med;
+          take = (dl < dr) || (dl == dr && lv < rv);
+        }
+        if (!take) break;
+        a_taken = i;
+      }
+      const int lo = c - a_taken;
+      const int hi = lo + beta - 1;  // inclusive
+      double sum = 0.0;
+      for (int r = lo; r <= hi; ++r) sum += static_cast<double>(col[r * kBlock]);
+      o[e] = static_cast<float>(sum / static_cast<double>(beta));
+    }
+    if (full) {
+      store_w<W>(out + cc, o);
+    } else {
+      for (int e = 0; e < W && cc + e < d; ++e) out[cc + e] = o[e];
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
 int grid_for(int64_t items) {
   int64_t blocks = (items + kBlock - 1) / kBlock;
-  if (blocks > 8192) blocks = 8192;
+  if (blocks > 32768) blocks = 32768;
   if (blocks < 1) blocks = 1;
   return static_cast<int>(blocks);
 }
@@ -204,12 +220,10 @@ hipError_t launch_median_kw(const float* x, int n, int64_t d, const int32_t* row
 template <int K>
 hipError_t launch_median_k(int width, const float* x, int n, int64_t d, const int32_t* rows,
                            float* out, hipStream_t s) {
-  if constexpr (K <= 12) {
+  if constexpr (K <= 32) {
     if (width == 4) return launch_median_kw<K, 4>(x, n, d, rows, out, s);
   }
-  if constexpr (K <= 24) {
-    if (width >= 2) return launch_median_kw<K, 2>(x, n, d, rows, out, s);
-  }
+  if (width >= 2) return launch_median_kw<K, 2>(x, n, d, rows, out, s);
   return launch_median_kw<K, 1>(x, n, d, rows, out, s);
 }
 
@@ -224,21 +238,33 @@ hipError_t median_dispatch(int k, int width, const float* x, int n, int64_t d,
   }
 }
 
+template <int T, int W>
+hipError_t launch_bulyan_tw(int beta, const float* x, int n, int64_t d, const int32_t* sel,
+                            float* out, hipStream_t s) {
+  {
+    TimedLaunch timed("bulyan_agg", s);
+    hipLaunchKernelGGL((k_bulyan_agg<T, W>), dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s,
+                       x, n, d, sel, beta, out);
+  }
+  return hipGetLastError();
+}
+
 template <int T>
-hipError_t bulyan_dispatch(int theta, int beta, const float* x, int n, int64_t d,
+hipError_t bulyan_dispatch(int theta, int beta, int width, const float* x, int n, int64_t d,
                            const int32_t* sel, float* out, hipStream_t s) {
   if constexpr (T > kNmax) {
     return hipErrorInvalidValue;
   } else {
     if (theta == T) {
-      {
-        TimedLaunch timed("bulyan_agg", s);
-        hipLaunchKernelGGL((k_bulyan_agg<T>), dim3(grid_for(d)), dim3(kBlock), 0, s, x, n, d, sel,
-                           beta, out);
+      if constexpr (T <= 24) {
+        if (width == 4) return launch_bulyan_tw<T, 4>(beta, x, n, d, sel, out, s);
       }
-      return hipGetLastError();
+      if constexpr (T <= 48) {
+        if (width >= 2) return launch_bulyan_tw<T, 2>(beta, x, n, d, sel, out, s);
+      }
+      return launch_bulyan_tw<T, 1>(beta, x, n, d, sel, out, s);
     }
-    return bulyan_dispatch<T + 1>(theta, beta, x, n, d, sel, out, s);
+    return bulyan_dispatch<T + 1>(theta, beta, width, x, n, d, sel, out, s);
   }
 }
 
@@ -273,7 +299,7 @@ hipError_t enqueue_bulyan_aggregate(const float* x, int n, int f, int64_t d, con
   if (d == 0) return hipSuccess;
   const int theta = n - 2 * f;
   const int beta = theta - 2 * f;
-  return bulyan_dispatch<1>(theta, beta, x, n, d, sel, out, s);
+  return bulyan_dispatch<1>(theta, beta, stream_width(x, d, out), x, n, d, sel, out, s);
 }
 
 }  // namespace garfield

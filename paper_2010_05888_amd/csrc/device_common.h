@@ -15,16 +15,19 @@ __device__ __forceinline__ float fmin_(float a, float b) { return __builtin_fmin
 __device__ __forceinline__ float fmax_(float a, float b) { return __builtin_fmaxf(a, b); }
 
 // Load W consecutive floats (W in {1, 2, 4}); p must be W*4-byte aligned.
-template <int W>
+// NT: a streaming (nontemporal) load, for data read exactly once.
+template <int W, bool NT = true>
 __device__ __forceinline__ void load_w(const float* __restrict__ p, float* v) {
   if constexpr (W == 4) {
-    const f4 t = *reinterpret_cast<const f4*>(p);
+    const f4* q = reinterpret_cast<const f4*>(p);
+    const f4 t = NT ? __builtin_nontemporal_load(q) : *q;
     v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
   } else if constexpr (W == 2) {
-    const f2 t = *reinterpret_cast<const f2*>(p);
+    const f2* q = reinterpret_cast<const f2*>(p);
+    const f2 t = NT ? __builtin_nontemporal_load(q) : *q;
     v[0] = t.x; v[1] = t.y;
   } else {
-    v[0] = *p;
+    v[0] = NT ? __builtin_nontemporal_load(p) : *p;
   }
 }
 

@@ -1,0 +1,53 @@
+// How the distance step's per-entry sums map to D[i][j]. Shared by the
+// kernels that consume distances (selection, MDA search, the D writer).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "internal.h"
+
+namespace garfield {
+
+// The result of the distance step: one fp64 sum per entry.
+//  * direct engine: entry p = pair (i < j), row-major over i, holds D[i][j];
+//  * Gram engine: entry q*256 + r*16 + c holds G[16*b1 + r][16*b2 + c] for the
+//    q-th block pair (b1 <= b2) of the upper block triangle, G = Y Y^T;
+//  * no engine (n < 2 or d == 0): D is all zeros.
+struct DistSums {
+  const double* sums;
+  int engine;
+  int n;
+};
+
+__device__ __forceinline__ int direct_entry(int n, int i, int j) {  // i < j
+  return i * (2 * n - i - 1) / 2 + (j - i - 1);
+}
+
+__device__ __forceinline__ int gram_entry(int nb, int i, int j) {  // i <= j
+  const int b1 = i >> 4, b2 = j >> 4;
+  const int q = b1 * nb - b1 * (b1 - 1) / 2 + (b2 - b1);
+  return q * 256 + (i & 15) * 16 + (j & 15);
+}
+
+// D[i][j] (symmetric, zero diagonal). The Gram form is evaluated in fp64 and
+// clamped at 0; identical rows give exactly 0 because their G entries agree.
+__device__ __forceinline__ double dist_entry(const DistSums& ds, int i, int j) {
+  if (i == j || ds.engine == kEngineNone) return 0.0;
+  const int a = i < j ? i : j, b = i < j ? j : i;
+  if (ds.engine == kEngineDirect) return ds.sums[direct_entry(ds.n, a, b)];
+  const int nb = (ds.n + 15) / 16;
+  const double v = (ds.sums[gram_entry(nb, a, a)] + ds.sums[gram_entry(nb, b, b)]) -
+                   2.0 * ds.sums[gram_entry(nb, a, b)];
+  return v > 0.0 ? v : 0.0;
+}
+
+// D into a block-shared n x n array (all threads of the block take part).
+__device__ __forceinline__ void load_dist(const DistSums& ds, double* D) {
+  const int n = ds.n;
+  for (int idx = threadIdx.x; idx < n * n; idx += blockDim.x) D[idx] = dist_entry(ds, idx / n, idx % n);
+  __syncthreads();
+}
+
+}  // namespace garfield

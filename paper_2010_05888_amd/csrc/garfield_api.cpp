@@ -7,8 +7,9 @@
 #include <map>
 #include <mutex>
 
-#include "../../include/garfield.h"
-#include "../../include/garfield_tuning.h"
+#include "garfield.h"
+#include "garfield_tuning.h"
+#include "dist_layout.h"
 #include "internal.h"
 #include "timing.h"
 
@@ -66,19 +67,18 @@ garfield_status check_common(const float* x, int n, int f, int64_t d) {
   return GARFIELD_OK;
 }
 
-// Distance step. D goes to `dist` when given (n x n fp64, device), else into
-// the workspace; *dist_used receives where it went. `extra` bytes of scratch
-// follow the distance workspace and are returned in *extra_ptr.
-garfield_status run_distances(const float* x, int n, int64_t d, double* dist, size_t extra,
-                              double** dist_used, void** extra_ptr, hipStream_t s) {
+// Distance step into the workspace. *ds receives the entry sums (valid once
+// the stream reaches the end of the step). `extra` bytes of scratch follow
+// the distance workspace and are returned in *extra_ptr.
+garfield_status run_distances(const float* x, int n, int64_t d, size_t extra, DistSums* ds,
+                              void** extra_ptr, hipStream_t s) {
   const DistPlan plan = plan_distances(n, d, x);
   const size_t dist_bytes = dist_workspace_bytes(plan);
   void* base = nullptr;
   garfield_status st = workspace(dist_bytes + align256(extra), &base);
   if (st != GARFIELD_OK) return st;
-  DistWorkspace ws = carve_dist_workspace(plan, base);
-  if (dist) ws.dist = dist;
-  if (dist_used) *dist_used = ws.dist;
+  const DistWorkspace ws = carve_dist_workspace(plan, base);
+  *ds = dist_sums(plan, ws);
   if (extra_ptr) *extra_ptr = static_cast<char*>(base) + dist_bytes;
   return to_status(enqueue_distances(x, plan, ws, s));
 }
@@ -98,7 +98,11 @@ garfield_status garfield_pairwise_sqdist(const float* x, int n, int64_t d, doubl
   garfield_status st = check_common(x, n, 0, d);
   if (st != GARFIELD_OK) return st;
   if (!dist) return GARFIELD_EINVAL;
-  return run_distances(x, n, d, dist, 0, nullptr, nullptr, static_cast<hipStream_t>(stream));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  DistSums ds;
+  st = run_distances(x, n, d, 0, &ds, nullptr, s);
+  if (st != GARFIELD_OK) return st;
+  return to_status(enqueue_write_dist(ds, dist, s));
 }
 
 garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int m, float* out,
@@ -110,10 +114,10 @@ garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int 
   if (m <= 0) m = n - f;
   if (m > n - f) return GARFIELD_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  double* D = nullptr;
-  st = run_distances(x, n, d, nullptr, 0, &D, nullptr, s);
+  DistSums ds;
+  st = run_distances(x, n, d, 0, &ds, nullptr, s);
   if (st != GARFIELD_OK) return st;
-  st = to_status(enqueue_krum_select(D, n, f, m, sel, s));
+  st = to_status(enqueue_krum_select(ds, f, m, sel, s));
   if (st != GARFIELD_OK || !out) return st;
   return to_status(enqueue_mean_rows(x, n, d, sel, m, out, s));
 }
@@ -144,10 +148,10 @@ garfield_status garfield_bulyan(const float* x, int n, int f, int64_t d, float* 
   if (!sel || (d > 0 && !out)) return GARFIELD_EINVAL;
   if (n < 4 * f + 3) return GARFIELD_EREQ;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  double* D = nullptr;
-  st = run_distances(x, n, d, nullptr, 0, &D, nullptr, s);
+  DistSums ds;
+  st = run_distances(x, n, d, 0, &ds, nullptr, s);
   if (st != GARFIELD_OK) return st;
-  st = to_status(enqueue_bulyan_select(D, n, f, sel, s));
+  st = to_status(enqueue_bulyan_select(ds, f, sel, s));
   if (st != GARFIELD_OK) return st;
   return to_status(enqueue_bulyan_aggregate(x, n, f, d, sel, out, s));
 }
@@ -162,10 +166,10 @@ garfield_status garfield_mda(const float* x, int n, int f, int64_t d, float* out
   if (subsets < 0 || subsets > GARFIELD_MDA_MAX_SUBSETS) return GARFIELD_ETOOBIG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   void* scratch = nullptr;
-  double* D = nullptr;
-  st = run_distances(x, n, d, nullptr, mda_scratch_bytes(n, f), &D, &scratch, s);
+  DistSums ds;
+  st = run_distances(x, n, d, mda_scratch_bytes(n, f), &ds, &scratch, s);
   if (st != GARFIELD_OK) return st;
-  st = to_status(enqueue_mda_select(D, n, f, scratch, sel, s));
+  st = to_status(enqueue_mda_select(ds, f, scratch, sel, s));
   if (st != GARFIELD_OK || !out) return st;
   return to_status(enqueue_mean_rows(x, n, d, sel, n - f, out, s));
 }

@@ -12,8 +12,7 @@ constexpr int kBlock = 256;       // threads per workgroup (4 wave64s)
 constexpr int kNmax = 64;         // largest n any kernel is built for
 constexpr int kDirectMaxNLimit = 20;   // direct-difference kernels are built for n <= this
 constexpr int kGramBlocks = 4;    // Gram engine: at most 4 blocks of 16 rows (n <= 64)
-constexpr int kProbeRuns = 16;    // reference-row probe: runs of kBlock coordinates
-constexpr int kMaxSegs = 64;      // cross-tile reduction: at most this many segments
+constexpr int kProbeRuns = 4;     // reference-row probe: runs of kBlock coordinates
 constexpr int kDirectLaneCoords = 16;  // direct engine: coordinates per lane per tile
 
 enum Engine { kEngineNone = 0, kEngineDirect = 1, kEngineGram = 2 };
@@ -27,8 +26,6 @@ struct DistPlan {
   int64_t chunk = 0;       // coordinates per workgroup (tile)
   int64_t tiles = 0;       // workgroups of the distance kernel
   int entries = 0;         // partial sums each tile writes
-  int64_t tiles_per_seg = 0;
-  int segs = 0;            // segments after the first reduction
 };
 
 // n <= direct_max_n(): distances by direct differences on VALU; else MFMA Gram.
@@ -37,15 +34,14 @@ void set_direct_max_n(int n);
 
 DistPlan plan_distances(int n, int64_t d, const float* x);
 
-// Bytes of device workspace the distance step needs (partials, segments, D,
-// probe buffers), 256-byte aligned sections.
+// Device workspace of the distance step (256-byte aligned sections).
 struct DistWorkspace {
-  double* partial = nullptr;  // tiles x entries
-  double* seg = nullptr;      // segs x entries
-  double* dist = nullptr;     // n x n
-  float* probe = nullptr;     // n x n (Gram engine only)
+  double* partial = nullptr;  // entries x tiles (entry-major)
+  double* sums = nullptr;     // entries
+  double* probe = nullptr;    // kNmax x kNmax (Gram engine only)
   int32_t* ref = nullptr;     // 1 (Gram engine only)
 };
+struct DistSums;
 size_t dist_workspace_bytes(const DistPlan& p);
 DistWorkspace carve_dist_workspace(const DistPlan& p, void* base);
 
@@ -53,21 +49,23 @@ DistWorkspace carve_dist_workspace(const DistPlan& p, void* base);
 hipError_t enqueue_reference(const float* x, const DistPlan& p, const DistWorkspace& ws,
                              hipStream_t s);
 
-// Enqueue the distance step; on return ws.dist holds D (n x n fp64) once the
-// stream reaches that point.
+// Enqueue the distance step; when the stream reaches its end, ws.sums holds
+// one fp64 sum per entry (see dist_layout.h for how they map to D).
 hipError_t enqueue_distances(const float* x, const DistPlan& p, const DistWorkspace& ws,
                              hipStream_t s);
+DistSums dist_sums(const DistPlan& p, const DistWorkspace& ws);
+// Write D (n x n fp64, device) from the entry sums.
+hipError_t enqueue_write_dist(const DistSums& ds, double* dist, hipStream_t s);
 
-// Selection on D (one workgroup). mode: 0 Multi-Krum (m), 1 Bulyan.
-hipError_t enqueue_krum_select(const double* dist, int n, int f, int m, int32_t* sel,
-                               hipStream_t s);
-hipError_t enqueue_bulyan_select(const double* dist, int n, int f, int32_t* sel, hipStream_t s);
+// Selection on D (one workgroup each).
+hipError_t enqueue_krum_select(const DistSums& ds, int f, int m, int32_t* sel, hipStream_t s);
+hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStream_t s);
 
 // MDA subset search. Scratch: mda_blocks(n, f) x 16 bytes.
 int64_t binomial(int a, int b);  // exact, or -1 if above 2^62
 int mda_blocks(int n, int f);
 size_t mda_scratch_bytes(int n, int f);
-hipError_t enqueue_mda_select(const double* dist, int n, int f, void* scratch, int32_t* sel,
+hipError_t enqueue_mda_select(const DistSums& ds, int f, void* scratch, int32_t* sel,
                               hipStream_t s);
 
 // Streaming aggregation kernels over the coordinates.

@@ -1,10 +1,12 @@
-// Selection on the distance matrix D (n x n fp64, n <= 64): Krum / Multi-Krum
+// Selection on the distance matrix D (n x n fp64, n <= 64, built in LDS from
+// the distance step's entry sums): Krum / Multi-Krum
 // scores and top-m, Bulyan's iterated Krum, and MDA's subset search
 // (Section 3.1 items 2-4). All of it runs on the device so the selected
 // indices never round-trip through the host; every ranking breaks ties
 // towards the lower index and every sum is added in a fixed order.
 
 #include "device_common.h"
+#include "dist_layout.h"
 #include "internal.h"
 #include "timing.h"
 
@@ -15,10 +17,9 @@ namespace {
 // order[i*n + r] = the j != i whose (D[i][j], j) has rank r in row i.
 // Scores then walk a row in ascending distance order, which is the order the
 // distances are added in (so identical rows get bit-identical scores).
-__device__ void load_and_rank(const double* __restrict__ dist, int n, double* D,
-                              unsigned char* order) {
-  for (int idx = threadIdx.x; idx < n * n; idx += blockDim.x) D[idx] = dist[idx];
-  __syncthreads();
+__device__ void load_and_rank(const DistSums& ds, double* D, unsigned char* order) {
+  const int n = ds.n;
+  load_dist(ds, D);
   for (int idx = threadIdx.x; idx < n * n; idx += blockDim.x) {
     const int i = idx / n, j = idx % n;
     if (i == j) continue;
@@ -46,13 +47,14 @@ __device__ void write_flagged(const int* flag, int n, int32_t* __restrict__ sel)
 
 // Multi-Krum: score(i) = sum of the k = n-f-2 smallest D[i][j], j != i; the
 // m lowest (score, i) are selected.
-__global__ __launch_bounds__(kBlock) void k_krum_select(const double* __restrict__ dist, int n,
-                                                        int f, int m, int32_t* __restrict__ sel) {
+__global__ __launch_bounds__(kBlock) void k_krum_select(DistSums ds, int f, int m,
+                                                        int32_t* __restrict__ sel) {
+  const int n = ds.n;
   __shared__ double D[kNmax * kNmax];
   __shared__ unsigned char order[kNmax * kNmax];
   __shared__ double score[kNmax];
   __shared__ int flag[kNmax];
-  load_and_rank(dist, n, D, order);
+  load_and_rank(ds, D, order);
   const int i = threadIdx.x;
   const int k = n - f - 2;
   if (i < n) {
@@ -76,14 +78,15 @@ __global__ __launch_bounds__(kBlock) void k_krum_select(const double* __restrict
 // (r = vectors remaining) and moves the lowest (score, index) to the
 // selection. The ranking of each row is computed once; a round walks it and
 // skips vectors already selected.
-__global__ __launch_bounds__(kBlock) void k_bulyan_select(const double* __restrict__ dist, int n,
-                                                          int f, int32_t* __restrict__ sel) {
+__global__ __launch_bounds__(kBlock) void k_bulyan_select(DistSums ds, int f,
+                                                          int32_t* __restrict__ sel) {
+  const int n = ds.n;
   __shared__ double D[kNmax * kNmax];
   __shared__ unsigned char order[kNmax * kNmax];
   __shared__ double score[kNmax];
   __shared__ int active[kNmax];
   __shared__ int picked[kNmax];
-  load_and_rank(dist, n, D, order);
+  load_and_rank(ds, D, order);
   const int i = threadIdx.x;
   if (i < n) {
     active[i] = 1;
@@ -150,16 +153,15 @@ __device__ void unrank_subset(int64_t rank, int n, int s, unsigned char* idx) {
   }
 }
 
-__global__ __launch_bounds__(kBlock) void k_mda_search(const double* __restrict__ dist, int n,
-                                                       int s, int64_t total, int64_t per,
-                                                       double* __restrict__ bdiam,
+__global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64_t total,
+                                                       int64_t per, double* __restrict__ bdiam,
                                                        int64_t* __restrict__ brank) {
   __shared__ double D[kNmax * kNmax];
   __shared__ unsigned char idx_all[kBlock * kNmax];
   __shared__ double rd[kBlock];
   __shared__ int64_t rr[kBlock];
-  for (int t = threadIdx.x; t < n * n; t += kBlock) D[t] = dist[t];
-  __syncthreads();
+  const int n = ds.n;
+  load_dist(ds, D);
   unsigned char* idx = idx_all + threadIdx.x * kNmax;
   const int64_t g = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   const int64_t r0 = g * per;
@@ -256,25 +258,25 @@ size_t mda_scratch_bytes(int n, int f) {
   return static_cast<size_t>(mda_blocks(n, f)) * (sizeof(double) + sizeof(int64_t));
 }
 
-hipError_t enqueue_krum_select(const double* dist, int n, int f, int m, int32_t* sel,
-                               hipStream_t s) {
+hipError_t enqueue_krum_select(const DistSums& ds, int f, int m, int32_t* sel, hipStream_t s) {
   {
     TimedLaunch timed("krum_select", s);
-    hipLaunchKernelGGL(k_krum_select, dim3(1), dim3(kBlock), 0, s, dist, n, f, m, sel);
+    hipLaunchKernelGGL(k_krum_select, dim3(1), dim3(kBlock), 0, s, ds, f, m, sel);
   }
   return hipGetLastError();
 }
 
-hipError_t enqueue_bulyan_select(const double* dist, int n, int f, int32_t* sel, hipStream_t s) {
+hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStream_t s) {
   {
     TimedLaunch timed("bulyan_select", s);
-    hipLaunchKernelGGL(k_bulyan_select, dim3(1), dim3(kBlock), 0, s, dist, n, f, sel);
+    hipLaunchKernelGGL(k_bulyan_select, dim3(1), dim3(kBlock), 0, s, ds, f, sel);
   }
   return hipGetLastError();
 }
 
-hipError_t enqueue_mda_select(const double* dist, int n, int f, void* scratch, int32_t* sel,
+hipError_t enqueue_mda_select(const DistSums& ds, int f, void* scratch, int32_t* sel,
                               hipStream_t s) {
+  const int n = ds.n;
   int64_t total, per;
   int blocks;
   mda_split(n, f, &total, &per, &blocks);
@@ -282,7 +284,7 @@ hipError_t enqueue_mda_select(const double* dist, int n, int f, void* scratch, i
   int64_t* brank = reinterpret_cast<int64_t*>(bdiam + blocks);
   {
     TimedLaunch timed("mda_search", s);
-    hipLaunchKernelGGL(k_mda_search, dim3(blocks), dim3(kBlock), 0, s, dist, n, n - f, total, per,
+    hipLaunchKernelGGL(k_mda_search, dim3(blocks), dim3(kBlock), 0, s, ds, n - f, total, per,
                        bdiam, brank);
   }
   hipError_t e = hipGetLastError();
