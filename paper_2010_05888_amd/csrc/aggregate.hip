@@ -33,6 +33,34 @@ __device__ __forceinline__ int64_t row_of(const int32_t* __restrict__ rows, int 
 }
 
 // ---------------------------------------------------------------------------
+// fp64 sum of the k rows at coordinates c .. c+W-1, eight loads in flight at a
+// time; FULL: all W coordinates exist (else the guarded tail loads).
+template <int W, bool FULL>
+__device__ __forceinline__ void sum_rows_at(const float* __restrict__ x, int n, int64_t d,
+                                            const int32_t* __restrict__ rows, int k, int64_t c,
+                                            double* acc) {
+  int t = 0;
+  for (; t + 8 <= k; t += 8) {
+    float v[8][W];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float* p = x + row_of(rows, t + u, n) * d + c;
+      if constexpr (FULL) load_w<W>(p, v[u]); else load_w_tail<W>(p, d - c, v[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int e = 0; e < W; ++e) acc[e] += static_cast<double>(v[u][e]);
+  }
+  for (; t < k; ++t) {
+    float v[W];
+    const float* p = x + row_of(rows, t, n) * d + c;
+    if constexpr (FULL) load_w<W>(p, v); else load_w_tail<W>(p, d - c, v);
+#pragma unroll
+    for (int e = 0; e < W; ++e) acc[e] += static_cast<double>(v[e]);
+  }
+}
+
 template <int W>
 __global__ __launch_bounds__(kBlock) void k_mean_rows(const float* __restrict__ x, int n,
                                                       int64_t d, const int32_t* __restrict__ rows,
@@ -45,26 +73,8 @@ __global__ __launch_bounds__(kBlock) void k_mean_rows(const float* __restrict__ 
 #pragma unroll
     for (int e = 0; e < W; ++e) acc[e] = 0.0;
     const bool full = c + W <= d;
-    int t = 0;
-    for (; t + 8 <= k; t += 8) {
-      float v[8][W];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float* p = x + row_of(rows, t + u, n) * d + c;
-        if (full) load_w<W>(p, v[u]); else load_w_tail<W>(p, d - c, v[u]);
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-#pragma unroll
-        for (int e = 0; e < W; ++e) acc[e] += static_cast<double>(v[u][e]);
-    }
-    for (; t < k; ++t) {
-      float v[W];
-      const float* p = x + row_of(rows, t, n) * d + c;
-      if (full) load_w<W>(p, v); else load_w_tail<W>(p, d - c, v);
-#pragma unroll
-      for (int e = 0; e < W; ++e) acc[e] += static_cast<double>(v[e]);
-    }
+    if (full) sum_rows_at<W, true>(x, n, d, rows, k, c, acc);
+    else sum_rows_at<W, false>(x, n, d, rows, k, c, acc);
     float o[W];
 #pragma unroll
     for (int e = 0; e < W; ++e) o[e] = static_cast<float>(acc[e] / count);
@@ -77,6 +87,12 @@ __global__ __launch_bounds__(kBlock) void k_mean_rows(const float* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
+// Every lane loads W consecutive coordinates of each of the K rows: 16-byte
+// loads (W = 4) stream a K-row gather far faster than 8- or 4-byte ones, so
+// W = 4 is kept up to K = kMedianX4MaxK, where the K x 4 values still fit the
+// registers of two waves per SIMD.
+constexpr int kMedianX4MaxK = 52;
+
 template <int K, int W>
 __global__ __launch_bounds__(kBlock) void k_median(const float* __restrict__ x, int n, int64_t d,
                                                    const int32_t* __restrict__ rows,
@@ -87,10 +103,12 @@ __global__ __launch_bounds__(kBlock) void k_median(const float* __restrict__ x, 
        c += stride) {
     float v[K][W];
     const bool full = c + W <= d;
+    if (full) {  // all K loads back to back, then the network
 #pragma unroll
-    for (int t = 0; t < K; ++t) {
-      const float* p = x + row_of(rows, t, n) * d + c;
-      if (full) load_w<W>(p, v[t]); else load_w_tail<W>(p, d - c, v[t]);
+      for (int t = 0; t < K; ++t) load_w<W>(x + row_of(rows, t, n) * d + c, v[t]);
+    } else {
+#pragma unroll
+      for (int t = 0; t < K; ++t) load_w_tail<W>(x + row_of(rows, t, n) * d + c, d - c, v[t]);
     }
     float o[W];
 #pragma unroll
@@ -141,10 +159,12 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_agg(const float* __restrict__
        cc += stride) {
     float v[T][W];
     const bool full = cc + W <= d;
+    if (full) {
 #pragma unroll
-    for (int t = 0; t < T; ++t) {
-      const float* p = x + row_of(sel, t, n) * d + cc;
-      if (full) load_w<W>(p, v[t]); else load_w_tail<W>(p, d - cc, v[t]);
+      for (int t = 0; t < T; ++t) load_w<W>(x + row_of(sel, t, n) * d + cc, v[t]);
+    } else {
+#pragma unroll
+      for (int t = 0; t < T; ++t) load_w_tail<W>(x + row_of(sel, t, n) * d + cc, d - cc, v[t]);
     }
     float o[W];
 #pragma unroll
@@ -188,9 +208,12 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_agg(const float* __restrict__
 }
 
 // ---------------------------------------------------------------------------
+// One pass: a workgroup per kBlock items, so every lane handles one item (the
+// grid-stride loops in the kernels only matter beyond 2^31 - 1 workgroups).
+// A single pass streams measurably faster than a capped grid looping over d.
 int grid_for(int64_t items) {
   int64_t blocks = (items + kBlock - 1) / kBlock;
-  if (blocks > 32768) blocks = 32768;
+  if (blocks > 0x7fffffff) blocks = 0x7fffffff;
   if (blocks < 1) blocks = 1;
   return static_cast<int>(blocks);
 }
@@ -198,29 +221,23 @@ int grid_for(int64_t items) {
 template <int W>
 hipError_t launch_mean(const float* x, int n, int64_t d, const int32_t* rows, int k, float* out,
                        hipStream_t s) {
-  {
-    TimedLaunch timed("mean_rows", s);
-    hipLaunchKernelGGL((k_mean_rows<W>), dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s, x, n,
-                       d, rows, k, out);
-  }
+  launch("mean_rows", k_mean_rows<W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s, x, n,
+    d, rows, k, out);
   return hipGetLastError();
 }
 
 template <int K, int W>
 hipError_t launch_median_kw(const float* x, int n, int64_t d, const int32_t* rows, float* out,
                             hipStream_t s) {
-  {
-    TimedLaunch timed("median", s);
-    hipLaunchKernelGGL((k_median<K, W>), dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s, x, n,
-                       d, rows, out);
-  }
+  launch("median", k_median<K, W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s, x, n,
+    d, rows, out);
   return hipGetLastError();
 }
 
 template <int K>
 hipError_t launch_median_k(int width, const float* x, int n, int64_t d, const int32_t* rows,
                            float* out, hipStream_t s) {
-  if constexpr (K <= 32) {
+  if constexpr (K <= kMedianX4MaxK) {
     if (width == 4) return launch_median_kw<K, 4>(x, n, d, rows, out, s);
   }
   if (width >= 2) return launch_median_kw<K, 2>(x, n, d, rows, out, s);
@@ -241,11 +258,8 @@ hipError_t median_dispatch(int k, int width, const float* x, int n, int64_t d,
 template <int T, int W>
 hipError_t launch_bulyan_tw(int beta, const float* x, int n, int64_t d, const int32_t* sel,
                             float* out, hipStream_t s) {
-  {
-    TimedLaunch timed("bulyan_agg", s);
-    hipLaunchKernelGGL((k_bulyan_agg<T, W>), dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s,
-                       x, n, d, sel, beta, out);
-  }
+  launch("bulyan_agg", k_bulyan_agg<T, W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s,
+    x, n, d, sel, beta, out);
   return hipGetLastError();
 }
 
@@ -270,19 +284,16 @@ hipError_t bulyan_dispatch(int theta, int beta, int width, const float* x, int n
 
 }  // namespace
 
-// Widest load both x (every row) and out support.
-int stream_width(const float* x, int64_t d, const float* out) {
-  int w = load_width(x, d);
-  const uintptr_t o = reinterpret_cast<uintptr_t>(out);
-  if (w == 4 && o % 16 != 0) w = 2;
-  if (w == 2 && o % 8 != 0) w = 1;
-  return w;
+// Load/store width of the streaming kernels: 16-byte accesses whenever x and
+// out are float-aligned, whatever d (see f4u).
+int stream_width(const float* x, const float* out) {
+  return (vector_width(x) == 4 && vector_width(out) == 4) ? 4 : 1;
 }
 
 hipError_t enqueue_mean_rows(const float* x, int n, int64_t d, const int32_t* rows, int k,
                              float* out, hipStream_t s) {
   if (d == 0) return hipSuccess;
-  const int w = stream_width(x, d, out);
+  const int w = stream_width(x, out);
   if (w == 4) return launch_mean<4>(x, n, d, rows, k, out, s);
   if (w == 2) return launch_mean<2>(x, n, d, rows, k, out, s);
   return launch_mean<1>(x, n, d, rows, k, out, s);
@@ -291,7 +302,7 @@ hipError_t enqueue_mean_rows(const float* x, int n, int64_t d, const int32_t* ro
 hipError_t enqueue_median(const float* x, int n, int64_t d, const int32_t* rows, int k,
                           float* out, hipStream_t s) {
   if (d == 0) return hipSuccess;
-  return median_dispatch<1>(k, stream_width(x, d, out), x, n, d, rows, out, s);
+  return median_dispatch<1>(k, stream_width(x, out), x, n, d, rows, out, s);
 }
 
 hipError_t enqueue_bulyan_aggregate(const float* x, int n, int f, int64_t d, const int32_t* sel,
@@ -299,7 +310,7 @@ hipError_t enqueue_bulyan_aggregate(const float* x, int n, int f, int64_t d, con
   if (d == 0) return hipSuccess;
   const int theta = n - 2 * f;
   const int beta = theta - 2 * f;
-  return bulyan_dispatch<1>(theta, beta, stream_width(x, d, out), x, n, d, sel, out, s);
+  return bulyan_dispatch<1>(theta, beta, stream_width(x, out), x, n, d, sel, out, s);
 }
 
 }  // namespace garfield

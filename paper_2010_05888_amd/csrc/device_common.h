@@ -9,22 +9,28 @@ namespace garfield {
 
 typedef float f2 __attribute__((ext_vector_type(2)));
 typedef float f4 __attribute__((ext_vector_type(4)));
+// The same vectors at the alignment of a float: global memory on CDNA serves
+// 8- and 16-byte accesses at any dword-aligned address, so rows of any length
+// d stream with 16-byte loads (row i starts at i * d floats, which is 16-byte
+// aligned only when d % 4 == 0).
+typedef float f2u __attribute__((ext_vector_type(2), aligned(4)));
+typedef float f4u __attribute__((ext_vector_type(4), aligned(4)));
 
 // min / max on finite values (inputs are finite by contract).
 __device__ __forceinline__ float fmin_(float a, float b) { return __builtin_fminf(a, b); }
 __device__ __forceinline__ float fmax_(float a, float b) { return __builtin_fmaxf(a, b); }
 
-// Load W consecutive floats (W in {1, 2, 4}); p must be W*4-byte aligned.
+// Load W consecutive floats (W in {1, 2, 4}); p must be 4-byte aligned.
 // NT: a streaming (nontemporal) load, for data read exactly once.
 template <int W, bool NT = true>
 __device__ __forceinline__ void load_w(const float* __restrict__ p, float* v) {
   if constexpr (W == 4) {
-    const f4* q = reinterpret_cast<const f4*>(p);
-    const f4 t = NT ? __builtin_nontemporal_load(q) : *q;
+    const f4u* q = reinterpret_cast<const f4u*>(p);
+    const f4u t = NT ? __builtin_nontemporal_load(q) : *q;
     v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
   } else if constexpr (W == 2) {
-    const f2* q = reinterpret_cast<const f2*>(p);
-    const f2 t = NT ? __builtin_nontemporal_load(q) : *q;
+    const f2u* q = reinterpret_cast<const f2u*>(p);
+    const f2u t = NT ? __builtin_nontemporal_load(q) : *q;
     v[0] = t.x; v[1] = t.y;
   } else {
     v[0] = NT ? __builtin_nontemporal_load(p) : *p;
@@ -34,13 +40,13 @@ __device__ __forceinline__ void load_w(const float* __restrict__ p, float* v) {
 template <int W>
 __device__ __forceinline__ void store_w(float* __restrict__ p, const float* v) {
   if constexpr (W == 4) {
-    f4 t;
+    f4u t;
     t.x = v[0]; t.y = v[1]; t.z = v[2]; t.w = v[3];
-    __builtin_nontemporal_store(t, reinterpret_cast<f4*>(p));
+    __builtin_nontemporal_store(t, reinterpret_cast<f4u*>(p));
   } else if constexpr (W == 2) {
-    f2 t;
+    f2u t;
     t.x = v[0]; t.y = v[1];
-    __builtin_nontemporal_store(t, reinterpret_cast<f2*>(p));
+    __builtin_nontemporal_store(t, reinterpret_cast<f2u*>(p));
   } else {
     __builtin_nontemporal_store(v[0], p);
   }

@@ -685,20 +685,19 @@ __global__ __launch_bounds__(kBlock) void k_write_dist(DistSums ds, double* __re
 // ---------------------------------------------------------------------------
 template <int N, int W>
 hipError_t launch_direct_nw(const float* x, const DistPlan& p, double* partial, hipStream_t s) {
-  {
-    TimedLaunch timed("dist_direct", s);
-    hipLaunchKernelGGL((k_dist_direct<N, W>), dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock), 0,
-                       s, x, p.d, p.chunk, partial);
-  }
+  launch("dist_direct", k_dist_direct<N, W>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock), 0,
+    s, x, p.d, p.chunk, partial);
   return hipGetLastError();
 }
 
-// Vector width the direct engine uses for n rows (register budget).
-int direct_width_cap(int n) { return n <= 8 ? 4 : (n <= 16 ? 2 : 1); }
+// Widest per-lane load that keeps the n(n-1)/2 accumulators and the n x W
+// loaded values within the registers of four waves per SIMD (16-byte loads
+// stream an n-row read fastest).
+int direct_width_cap(int n) { return n <= 12 ? 4 : (n <= 16 ? 2 : 1); }
 
 template <int N>
 hipError_t launch_direct_n(const float* x, const DistPlan& p, double* partial, hipStream_t s) {
-  if constexpr (N <= 8) {
+  if constexpr (N <= 12) {
     if (p.width == 4) return launch_direct_nw<N, 4>(x, p, partial, s);
   }
   if constexpr (N <= 16) {
@@ -721,15 +720,12 @@ hipError_t launch_direct_dispatch(int n, const float* x, const DistPlan& p, doub
 template <int NB, int W>
 hipError_t launch_gram_nw(const float* x, const DistPlan& p, const int32_t* ref, double* partial,
                           hipStream_t s) {
-  {
-    TimedLaunch timed("dist_gram", s);
-    if constexpr (W == 4) {
-      hipLaunchKernelGGL((k_dist_gram_lds<NB>), dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock),
-                         0, s, x, p.n, p.d, p.chunk, ref, partial);
-    } else {
-      hipLaunchKernelGGL((k_dist_gram2<NB, W>), dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock),
-                         0, s, x, p.n, p.d, p.chunk, ref, partial);
-    }
+  if constexpr (W == 4) {
+    launch("dist_gram", k_dist_gram_lds<NB>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock), 0,
+           s, x, p.n, p.d, p.chunk, ref, partial);
+  } else {
+    launch("dist_gram", k_dist_gram2<NB, W>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock), 0,
+           s, x, p.n, p.d, p.chunk, ref, partial);
   }
   return hipGetLastError();
 }
@@ -813,14 +809,16 @@ int load_width(const float* x, int64_t d) {
   return 1;
 }
 
+int vector_width(const float* p) { return reinterpret_cast<uintptr_t>(p) % 4 == 0 ? 4 : 1; }
+
 DistPlan plan_distances(int n, int64_t d, const float* x) {
   DistPlan p;
   p.n = n;
   p.d = d;
   if (n < 2 || d == 0) return p;  // D is all zeros
-  p.width = load_width(x, d);
   if (n <= direct_max_n()) {
     p.engine = kEngineDirect;
+    p.width = vector_width(x);
     if (p.width > direct_width_cap(n)) p.width = direct_width_cap(n);
     // kDirectLaneCoords coordinates per lane per tile: each fp32 accumulator
     // sums at most that many squares before the tile is reduced in fp64.
@@ -828,6 +826,7 @@ DistPlan plan_distances(int n, int64_t d, const float* x) {
     p.entries = n * (n - 1) / 2;
   } else {
     p.engine = kEngineGram;
+    p.width = load_width(x, d);
     // As many workgroups as the device holds resident (at most one per
     // 64-coordinate stage); workgroup b takes stages b, b + tiles, ...
     const int nb = (n + 15) / 16;
@@ -882,16 +881,10 @@ DistSums dist_sums(const DistPlan& p, const DistWorkspace& ws) {
 
 hipError_t enqueue_reference(const float* x, const DistPlan& p, const DistWorkspace& ws,
                              hipStream_t s) {
-  {
-    TimedLaunch timed("probe", s);
-    hipLaunchKernelGGL(k_probe, dim3(p.n), dim3(kBlock), 0, s, x, p.n, p.d, ws.probe);
-  }
+  launch("probe", k_probe, dim3(p.n), dim3(kBlock), 0, s, x, p.n, p.d, ws.probe);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  {
-    TimedLaunch timed("pick_ref", s);
-    hipLaunchKernelGGL(k_pick_ref, dim3(1), dim3(kBlock), 0, s, ws.probe, p.n, ws.ref);
-  }
+  launch("pick_ref", k_pick_ref, dim3(1), dim3(kBlock), 0, s, ws.probe, p.n, ws.ref);
   return hipGetLastError();
 }
 
@@ -913,19 +906,13 @@ hipError_t enqueue_distances(const float* x, const DistPlan& p, const DistWorksp
     }
   }
   if (e != hipSuccess) return e;
-  {
-    TimedLaunch timed("sum_tiles", s);
-    hipLaunchKernelGGL(k_sum_tiles, dim3(p.entries), dim3(kBlock), 0, s, ws.partial, p.tiles,
-                       ws.sums);
-  }
+  launch("sum_tiles", k_sum_tiles, dim3(p.entries), dim3(kBlock), 0, s, ws.partial, p.tiles,
+    ws.sums);
   return hipGetLastError();
 }
 
 hipError_t enqueue_write_dist(const DistSums& ds, double* dist, hipStream_t s) {
-  {
-    TimedLaunch timed("write_dist", s);
-    hipLaunchKernelGGL(k_write_dist, dim3(1), dim3(kBlock), 0, s, ds, dist);
-  }
+  launch("write_dist", k_write_dist, dim3(1), dim3(kBlock), 0, s, ds, dist);
   return hipGetLastError();
 }
 

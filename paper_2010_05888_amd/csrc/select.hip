@@ -259,18 +259,12 @@ size_t mda_scratch_bytes(int n, int f) {
 }
 
 hipError_t enqueue_krum_select(const DistSums& ds, int f, int m, int32_t* sel, hipStream_t s) {
-  {
-    TimedLaunch timed("krum_select", s);
-    hipLaunchKernelGGL(k_krum_select, dim3(1), dim3(kBlock), 0, s, ds, f, m, sel);
-  }
+  launch("krum_select", k_krum_select, dim3(1), dim3(kBlock), 0, s, ds, f, m, sel);
   return hipGetLastError();
 }
 
 hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStream_t s) {
-  {
-    TimedLaunch timed("bulyan_select", s);
-    hipLaunchKernelGGL(k_bulyan_select, dim3(1), dim3(kBlock), 0, s, ds, f, sel);
-  }
+  launch("bulyan_select", k_bulyan_select, dim3(1), dim3(kBlock), 0, s, ds, f, sel);
   return hipGetLastError();
 }
 
@@ -282,17 +276,11 @@ hipError_t enqueue_mda_select(const DistSums& ds, int f, void* scratch, int32_t*
   mda_split(n, f, &total, &per, &blocks);
   double* bdiam = static_cast<double*>(scratch);
   int64_t* brank = reinterpret_cast<int64_t*>(bdiam + blocks);
-  {
-    TimedLaunch timed("mda_search", s);
-    hipLaunchKernelGGL(k_mda_search, dim3(blocks), dim3(kBlock), 0, s, ds, n - f, total, per,
-                       bdiam, brank);
-  }
+  launch("mda_search", k_mda_search, dim3(blocks), dim3(kBlock), 0, s, ds, n - f, total, per,
+    bdiam, brank);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  {
-    TimedLaunch timed("mda_pick", s);
-    hipLaunchKernelGGL(k_mda_pick, dim3(1), dim3(64), 0, s, bdiam, brank, blocks, n, n - f, sel);
-  }
+  launch("mda_pick", k_mda_pick, dim3(1), dim3(64), 0, s, bdiam, brank, blocks, n, n - f, sel);
   return hipGetLastError();
 }
 

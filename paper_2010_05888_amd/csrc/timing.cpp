@@ -19,7 +19,6 @@ std::mutex g_mu;
 int g_on = 0;
 std::vector<Record> g_records;
 std::vector<hipEvent_t> g_free;  // events ready for reuse
-thread_local int t_open = -1;    // index of this thread's open record
 
 hipEvent_t take_event() {
   if (!g_free.empty()) {
@@ -54,21 +53,17 @@ void timing_set(bool on) {
   __atomic_store_n(&g_on, on ? 1 : 0, __ATOMIC_RELAXED);
 }
 
-void timing_begin(const char* name, hipStream_t s) {
+LaunchEvents timing_record(const char* name) {
   std::lock_guard<std::mutex> lock(g_mu);
-  Record r{name, take_event(), nullptr};
-  if (r.start) (void)hipEventRecord(r.start, s);
-  g_records.push_back(r);
-  t_open = static_cast<int>(g_records.size()) - 1;
-}
-
-void timing_end(hipStream_t s) {
-  std::lock_guard<std::mutex> lock(g_mu);
-  if (t_open < 0 || t_open >= static_cast<int>(g_records.size())) return;
-  Record& r = g_records[t_open];
-  r.stop = take_event();
-  if (r.stop) (void)hipEventRecord(r.stop, s);
-  t_open = -1;
+  LaunchEvents ev;
+  ev.start = take_event();
+  ev.stop = ev.start ? take_event() : nullptr;
+  if (!ev.stop) {
+    if (ev.start) g_free.push_back(ev.start);
+    return LaunchEvents{};
+  }
+  g_records.push_back(Record{name, ev.start, ev.stop});
+  return ev;
 }
 
 size_t timing_summary(char* buf, size_t len) {

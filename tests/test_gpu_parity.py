@@ -53,8 +53,9 @@ def _bounds(x, xt, Do):
 
 # --- distances -------------------------------------------------------------------
 
-@pytest.mark.parametrize("n,d", [(2, 1), (3, 7), (7, 1000), (11, 4097), (19, 65537),
-                                 (20, 5000), (21, 3000), (33, 4097), (64, 20000), (64, 1)])
+@pytest.mark.parametrize("n,d", [(2, 1), (3, 7), (7, 1000), (11, 4097), (12, 4099), (13, 2051),
+                                 (19, 65537), (20, 5000), (21, 3000), (33, 4097), (64, 20000),
+                                 (64, 1)])
 def test_distances_within_bound(engine, n, d):
     rng = np.random.default_rng(n * 1000 + d)
     x = rng.standard_normal((n, d)).astype(np.float32)
@@ -308,7 +309,19 @@ def test_misaligned_and_odd_dimensions():
                                       x.astype(np.float64).sum(0).__truediv__(11).astype(np.float32))
         D = gf.pairwise_sqdist(xt).cpu().numpy()
         Do = oracle.pairwise_sqdist(x)
-        assert np.all(np.abs(D - Do) <= parity.dist_bounds(Do, "direct"))
+        B = parity.dist_bounds(Do, "direct")
+        assert np.all(np.abs(D - Do) <= B)
+        same = parity.identical_rows(Do)
+        oo, so, sc = oracle.multikrum(x, 2, 9, return_scores=True)
+        if parity.krum_pinned(sc, Do, B, 2, 9, same)[0]:
+            out, sel = gf.multikrum(xt, 2, 9)
+            assert sel.cpu().numpy().tolist() == so.tolist(), d
+            assert parity.agg_close(out.cpu().numpy(), oo)[0], d
+        oo, so, picks, rs = oracle.bulyan(x, 2, return_rounds=True)
+        if parity.bulyan_pinned(picks, rs, Do, B, 11, 2, same)[0]:
+            out, sel = gf.bulyan(xt, 2)
+            assert sel.cpu().numpy().tolist() == so.tolist(), d
+            assert parity.agg_close(out.cpu().numpy(), oo)[0], d
 
 
 def test_average_matches_fp64_mean():
