@@ -176,32 +176,45 @@ __global__ __launch_bounds__(kBlock) void k_pick_ref(const double* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
-// Gram engine, step 3: G partial sums per tile on MFMA (v_mfma_f32_16x16x4_f32).
+// Gram engine, step 3: partial sums of G = Y Y^T, Y = X - x_ref, on fp32 MFMA
+// (v_mfma_f32_16x16x4_f32), upper block triangle only.
 //
-// The workgroup streams its tile in stages of 64 coordinates. For each stage
-// every thread loads 4 consecutive coordinates of up to 4 rows (and of the
-// reference row), subtracts the reference, and stores them into one of two
-// LDS buffers (row-major, 68-float pitch); while the waves multiply from one
-// buffer the next stage's loads are in flight.
+// Streaming. A stage is the 16*NB rows (rows at or beyond n alias the
+// reference row, so their Y rows are exactly 0) times kGramStage = 256
+// consecutive coordinates: 1 KB of every row, the shortest run that streams
+// well from rows whose starts are not cache-line aligned (row i starts at
+// i * d floats). Wave w loads rows w*4NB .. w*4NB + 4NB - 1 with one 16-byte
+// load per lane per row (lane l: coordinates 4l .. 4l+3, so one instruction
+// reads 1 KB of one row), writes them to the stage buffer in LDS, and issues
+// the next stage's loads into the same registers before the stage is
+// multiplied: a stage is in flight while the previous one is computed.
 //
-// The work of a stage is NBP block pairs (b1 <= b2) x 16 k-slices. It is cut
-// into UNITS = NBP * H units (pair q, k-part h) with UNITS a multiple of 4,
-// and wave w takes units u = w, w + 4, ...: the four waves issue the same
-// number of MFMAs. Within a 16-coordinate group lane (g = l / 16, r = l % 16)
-// reads row 16b + r, coordinates 4g .. 4g + 3, as one 16-byte LDS read: these
-// are the A (or B) operands of 4 consecutive MFMA k-slices. Each fp32
-// accumulator takes 4 MFMAs (16 products) before it is added into fp64.
+// Multiplying. The stage buffer holds Y (the reference row is subtracted as
+// the stage is written). Wave w takes half h = w % 2 of the stage's
+// coordinates (128) for the block pairs (b1 <= b2) of parity w / 2 (pairs q
+// with q % 2 == w / 2; five each when NB = 4, so every wave issues the same
+// number of MFMAs): per 16-coordinate group, lane (g = l/16, r = l%16) reads
+// the 16-byte fragment of row 16b + r at coordinates 4g .. 4g+3 of each block
+// b once (the A and B operands of four consecutive MFMA k-steps). Each pair's
+// MFMAs over two groups start from zero and their fp32 result (32 products)
+// is added into fp64, so every fp32 accumulation spans 32 products whatever d
+// is. (The conversions and fp64 additions do not overlap the MFMAs on this
+// hardware: one addition per 32 products instead of per 16 saves about a
+// fifth of the multiply time.)
+//
+// Partials. The two halves' fp64 sums of each pair are added (half 0 first)
+// and written as this workgroup's partials; workgroup b takes stages b, b + G, ... (G = grid
+// size), so at any time the grid streams one compact window of every row.
+constexpr int kGramStage = 256;               // coordinates per stage
+constexpr int kGramPitch = kGramStage + 4;    // floats per LDS row (bank spread)
+
 template <int NB>
 struct GramShape {
-  static constexpr int NBP = NB * (NB + 1) / 2;
-  static constexpr int H = (NBP % 4 == 0) ? 1 : ((NBP % 2 == 0) ? 2 : 4);
-  static constexpr int UNITS = NBP * H;
-  static constexpr int UPW = UNITS / 4;       // units per wave
-  static constexpr int GROUPS = 4 / H;        // 16-coordinate groups per unit per stage
+  static constexpr int ROWS = 16 * NB;
+  static constexpr int NBP = NB * (NB + 1) / 2;   // block pairs b1 <= b2
+  static constexpr int RPW = ROWS / 4;            // rows loaded per wave
+  static constexpr int PPW = (NBP + 1) / 2;       // pairs per wave (one parity)
 };
-
-constexpr int kGramStage = 64;                // coordinates per stage
-constexpr int kGramPitch = kGramStage + 4;    // floats per LDS row
 
 __host__ __device__ constexpr int pair_b1(int nb, int q) {
   int b1 = 0;
@@ -220,437 +233,162 @@ __host__ __device__ constexpr int pair_b2(int nb, int q) {
   return b1 + q;
 }
 
-// Multiply-accumulate this wave's units over one 16-coordinate group.
-template <int NB, int WV, int GRP>
-__device__ __forceinline__ void gram_group(const float* __restrict__ buf, f4* acc, int g, int r) {
-  using S = GramShape<NB>;
-#pragma unroll
-  for (int i = 0; i < S::UPW; ++i) {
-    const int u = WV + 4 * i;
-    const int q = u / S::H;
-    const int h = u % S::H;
-    if (GRP / S::GROUPS != h) continue;  // this group belongs to another k-part
-    const int b1 = pair_b1(NB, q), b2 = pair_b2(NB, q);
-    const f4 a = *reinterpret_cast<const f4*>(buf + (16 * b1 + r) * kGramPitch + 16 * GRP + 4 * g);
-    const f4 b = (b1 == b2) ? a
-                            : *reinterpret_cast<const f4*>(buf + (16 * b2 + r) * kGramPitch +
-                                                           16 * GRP + 4 * g);
-    acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, acc[i], 0, 0, 0);
-    acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, acc[i], 0, 0, 0);
-    acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, acc[i], 0, 0, 0);
-    acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, acc[i], 0, 0, 0);
-  }
+// LDS-only barrier: waits for this wave's LDS operations, then for every
+// wave, and leaves vector-memory loads in flight (a __syncthreads() would also
+// wait for those).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt unconstrained
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
-template <int NB, int WV>
-__device__ __forceinline__ void gram_stage(const float* __restrict__ buf, f4* acc,
-                                           double (*acc64)[4], int g, int r) {
+// Issue the loads of the stage at c0: this wave's rows into v, the reference
+// row into vr (coordinates at or beyond d read as 0 when the stage is the
+// partial last one).
+template <int NB, bool FULL>
+__device__ __forceinline__ void gram_issue(const float* __restrict__ x, int n, int64_t d,
+                                           int ref, int wave, int lane, int64_t c0, f4* v,
+                                           f4& vr) {
   using S = GramShape<NB>;
-#pragma unroll
-  for (int grp = 0; grp < 4; ++grp) {
-    switch (grp) {
-      case 0: gram_group<NB, WV, 0>(buf, acc, g, r); break;
-      case 1: gram_group<NB, WV, 1>(buf, acc, g, r); break;
-      case 2: gram_group<NB, WV, 2>(buf, acc, g, r); break;
-      default: gram_group<NB, WV, 3>(buf, acc, g, r); break;
-    }
-    // flush the units that just took this group's 4 MFMAs
-#pragma unroll
-    for (int i = 0; i < S::UPW; ++i) {
-      const int u = WV + 4 * i;
-      if (grp / S::GROUPS != u % S::H) continue;
-      acc64[i][0] += static_cast<double>(acc[i].x);
-      acc64[i][1] += static_cast<double>(acc[i].y);
-      acc64[i][2] += static_cast<double>(acc[i].z);
-      acc64[i][3] += static_cast<double>(acc[i].w);
-      acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    }
-  }
-}
-
-// Load (registers) the shifted stage starting at c0: rows lr + 16i, 4
-// coordinates at c0 + 4*col. Coordinates at or beyond `end` read as 0.
-template <int NB, int W>
-__device__ __forceinline__ void gram_load(const float* __restrict__ x, const float* __restrict__ xref,
-                                          int n, int64_t d, int64_t c0, int64_t end, int lr,
-                                          int col, float (*pv)[4], float* pr) {
-  const int64_t c = c0 + 4 * col;
-  const bool full = c + 4 <= end;
-  if (full) {
-#pragma unroll
-    for (int u = 0; u < 4; u += W) load_w<W, false>(xref + c + u, pr + u);
-  } else {
-    load_w_tail<4>(xref + c, end - c, pr);
-  }
-#pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    const int row = lr + 16 * i;
-    if (row < n) {
-      const float* p = x + static_cast<int64_t>(row) * d + c;
-      if (full) {
-#pragma unroll
-        for (int u = 0; u < 4; u += W) load_w<W>(p + u, pv[i] + u);
-      } else {
-        load_w_tail<4>(p, end - c, pv[i]);
-      }
+  const int64_t c = c0 + 4 * lane;
+  auto load = [&](int row, f4& out) {
+    const float* p = x + static_cast<int64_t>(row) * d + c;
+    float t[4];
+    if constexpr (FULL) {
+      load_w<4>(p, t);
     } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) pv[i][e] = 0.0f;
+      if (c + 4 <= d) load_w<4>(p, t); else load_w_tail<4>(p, d - c, t);
     }
+    out = f4{t[0], t[1], t[2], t[3]};
+  };
+#pragma unroll
+  for (int i = 0; i < S::RPW; ++i) {
+    const int row = wave * S::RPW + i;
+    load(row < n ? row : ref, v[i]);
   }
+  load(ref, vr);
 }
 
+// Y = X - x_ref for this wave's rows into the stage buffer (rows at or beyond
+// n hold the reference row, so theirs are exactly 0).
 template <int NB>
-__device__ __forceinline__ void gram_store(float* __restrict__ buf, int n, int lr, int col,
-                                           float (*pv)[4], const float* pr) {
-#pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    const int row = lr + 16 * i;
-    f4 y;
-    if (row < n) {
-      y = f4{pv[i][0] - pr[0], pv[i][1] - pr[1], pv[i][2] - pr[2], pv[i][3] - pr[3]};
-    } else {
-      y = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    }
-    *reinterpret_cast<f4*>(buf + row * kGramPitch + 4 * col) = y;
-  }
-}
-
-// This workgroup's stages are global stages blockIdx.x, + gridDim.x, ...;
-// the last global stage may be partial (zero-filled by gram_load).
-template <int NB, int W, int WV>
-__device__ __forceinline__ void gram_tile(const float* __restrict__ x, int n, int64_t d,
-                                          const float* __restrict__ xref,
-                                          float* __restrict__ bufs, double (*acc64)[4]) {
+__device__ __forceinline__ void gram_put(float* __restrict__ buf, int wave, int lane, const f4* v,
+                                         const f4& vr) {
   using S = GramShape<NB>;
-  const int t = threadIdx.x;
-  const int lane = t & 63;
-  const int g = lane >> 4, r = lane & 15;
-  const int lr = t >> 4, col = t & 15;  // loading role: row lr + 16i, coordinates 4*col..
-  f4 acc[S::UPW];
 #pragma unroll
-  for (int i = 0; i < S::UPW; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-  float pv[NB][4];
-  float pr[4];
-  const int64_t total = (d + kGramStage - 1) / kGramStage;
-  const int64_t b = blockIdx.x, G = gridDim.x;
-  const int64_t mine = (total > b) ? (total - b + G - 1) / G : 0;
-  if (mine <= 0) return;
-  auto stage_end = [d](int64_t c0) { return (c0 + kGramStage < d) ? c0 + kGramStage : d; };
-  int64_t c0 = b * kGramStage;
-  gram_load<NB, W>(x, xref, n, d, c0, stage_end(c0), lr, col, pv, pr);
-  gram_store<NB>(bufs, n, lr, col, pv, pr);
-  __syncthreads();
-  for (int64_t k = 0; k < mine; ++k) {
-    float* cur = bufs + (k & 1) * (64 * kGramPitch);
-    float* nxt = bufs + ((k + 1) & 1) * (64 * kGramPitch);
-    const bool more = k + 1 < mine;
-    if (more) {
-      c0 = (b + (k + 1) * G) * kGramStage;
-      gram_load<NB, W>(x, xref, n, d, c0, stage_end(c0), lr, col, pv, pr);
-    }
-    gram_stage<NB, WV>(cur, acc, acc64, g, r);
-    if (more) gram_store<NB>(nxt, n, lr, col, pv, pr);
-    __syncthreads();
-  }
+  for (int i = 0; i < S::RPW; ++i)
+    *reinterpret_cast<f4*>(buf + (wave * S::RPW + i) * kGramPitch + 4 * lane) = v[i] - vr;
 }
 
-template <int NB, int W>
-__global__ __launch_bounds__(kBlock) void k_dist_gram2(const float* __restrict__ x, int n,
-                                                        int64_t d, int64_t chunk,
-                                                        const int32_t* __restrict__ ref_idx,
-                                                        double* __restrict__ partial) {
+// Pairs I, I + 1, ... of this wave (pair q = 2I + PH) over two consecutive
+// 16-coordinate groups (fragments y0, y1): a chain of eight MFMAs (32
+// products) from zero, then one addition into fp64. A template recursion, so
+// that every pair's blocks are compile-time constants (the fragments stay in
+// fixed registers).
+template <int NB, int PH, int I>
+__device__ __forceinline__ void gram_pairs(const f4* y0, const f4* y1, double (*acc64)[4]) {
   using S = GramShape<NB>;
-  __shared__ __attribute__((aligned(16))) float bufs[2 * 64 * kGramPitch];
-  const int wave = threadIdx.x >> 6;
-  const int lane = threadIdx.x & 63;
-  const int g = lane >> 4, r = lane & 15;
-  const float* __restrict__ xref = x + static_cast<int64_t>(*ref_idx) * d;
-  (void)chunk;
-  double acc64[S::UPW][4];
-#pragma unroll
-  for (int i = 0; i < S::UPW; ++i)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) acc64[i][e] = 0.0;
-  switch (wave) {
-    case 0: gram_tile<NB, W, 0>(x, n, d, xref, bufs, acc64); break;
-    case 1: gram_tile<NB, W, 1>(x, n, d, xref, bufs, acc64); break;
-    case 2: gram_tile<NB, W, 2>(x, n, d, xref, bufs, acc64); break;
-    default: gram_tile<NB, W, 3>(x, n, d, xref, bufs, acc64); break;
-  }
-  // Combine the k-parts of each pair in ascending h (fixed order) and write the
-  // tile's partials: entry q*256 + row*16 + col holds G[16*b1 + row][16*b2 + col].
-  double* red = reinterpret_cast<double*>(bufs);  // H x 256 doubles
-  double* __restrict__ out = partial + blockIdx.x;
-  const int64_t stride = gridDim.x;
-#pragma unroll
-  for (int q = 0; q < S::NBP; ++q) {
-#pragma unroll
-    for (int h = 0; h < S::H; ++h) {
-      const int u = q * S::H + h;
-      if (wave == u % 4) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) red[h * 256 + (4 * g + e) * 16 + r] = acc64[u / 4][e];
-      }
-    }
-    __syncthreads();
-    const int t = threadIdx.x;
-    double v = red[t];
-#pragma unroll
-    for (int h = 1; h < S::H; ++h) v += red[h * 256 + t];
-    out[(q * 256 + t) * stride] = v;
-    __syncthreads();
+  constexpr int q = 2 * I + PH;
+  if constexpr (I < S::PPW && q < S::NBP) {
+    constexpr int b1 = pair_b1(NB, q), b2 = pair_b2(NB, q);
+    const f4 zero = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    f4 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[b1].x, y0[b2].x, zero, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[b1].y, y0[b2].y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[b1].z, y0[b2].z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[b1].w, y0[b2].w, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[b1].x, y1[b2].x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[b1].y, y1[b2].y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[b1].z, y1[b2].z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[b1].w, y1[b2].w, acc, 0, 0, 0);
+    acc64[I][0] += static_cast<double>(acc.x);
+    acc64[I][1] += static_cast<double>(acc.y);
+    acc64[I][2] += static_cast<double>(acc.z);
+    acc64[I][3] += static_cast<double>(acc.w);
+    gram_pairs<NB, PH, I + 1>(y0, y1, acc64);
   }
 }
 
-// ---------------------------------------------------------------------------
-// Gram engine, step 3 for 16-byte-aligned rows: the same contraction with the
-// stages brought into LDS by direct global-to-LDS loads (global_load_lds_dwordx4),
-// through a ring of three stage buffers, so two stages are in flight while the
-// waves multiply the third, with no staging registers.
-//
-// A stage is 16*NB rows x 16 chunks of 4 coordinates. Chunk c of row `row`
-// sits in LDS slot row*17 + c (16 bytes per slot; slot 16 of each row is
-// padding), so the 16 rows a fragment read touches fall in distinct bank
-// groups, and every fragment address is one per-lane base plus a constant. A
-// direct load writes 64 consecutive slots per instruction (lane l -> slot
-// base + l); lanes whose slot is padding, or whose row is at or beyond n, load
-// row 0 instead (always in bounds) and those rows are masked at use, so every
-// lane issues every load and each wave's count of loads in flight is a
-// compile-time constant. The shift by the reference row (one of the staged
-// rows) is applied when a fragment is read. A final stage that runs past the
-// tile end is staged through registers with zero fill.
-typedef __attribute__((address_space(3))) void* lds_ptr;
-
-// global_load_lds_dwordx4: 16 bytes per lane from `src` into LDS at
-// lds_base + 16 * lane. Written as inline assembly so that the compiler does
-// not add a wait for these loads before every later LDS read (it cannot tell
-// the ring buffers apart); the ring code waits for them explicitly.
-__device__ __forceinline__ void load_lds_16(const float* src, float* lds_base) {
-  const lds_ptr lds = (lds_ptr)lds_base;
-  const uint32_t m0 = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>((uintptr_t)lds));
-  asm volatile(
-      "s_mov_b32 m0, %0\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off"
-      :
-      : "s"(m0), "v"(src)
-      : "memory", "m0");
-}
-
-template <int NB>
-struct Ring {
-  static constexpr int SLOTS = 16 * NB * 17;            // 16-byte slots per stage
-  static constexpr int LOADS = (SLOTS + 63) / 64;       // load instructions per stage
-  static constexpr int FLOATS = LOADS * 64 * 4;         // floats per ring buffer
-  // loads per stage issued by wave w (instructions j = w, w + 4, ...)
-  __host__ __device__ static constexpr int loads_of(int w) { return (LOADS - w + 3) / 4; }
-};
-
-__device__ __forceinline__ int ring_slot(int row, int chunk) { return row * 17 + chunk; }
-
-// Wait until at most N vector-memory operations of this wave are outstanding
-// and all of its LDS operations are done (s_waitcnt vmcnt(N) lgkmcnt(0)).
-template <int N>
-__device__ __forceinline__ void wait_vmem_lds() {
-  static_assert(N >= 0 && N < 16, "vmcnt immediate");
-  __builtin_amdgcn_s_waitcnt(N | (0x7 << 4) | (0x0 << 8));
-}
-
-// Issue the loads of the full stage starting at c0 into `slot` (one buffer).
-template <int NB, int WV>
-__device__ __forceinline__ void ring_issue(const float* __restrict__ x, int n, int64_t d,
-                                           int64_t c0, float* slot) {
-  const int l = threadIdx.x & 63;
+// This wave's half h of the stage in `buf`, block pairs of parity PH.
+template <int NB, int PH>
+__device__ __forceinline__ void gram_multiply(const float* __restrict__ buf, int h, int g, int r,
+                                              double (*acc64)[4]) {
 #pragma unroll
-  for (int j = WV; j < Ring<NB>::LOADS; j += 4) {
-    const int s = 64 * j + l;
-    const int row = s / 17, chunk = s % 17;
-    const bool real = chunk < 16 && row < n && row < 16 * NB;
-    const float* src = real ? x + static_cast<int64_t>(row) * d + c0 + 4 * chunk : x + c0;
-    load_lds_16(src, slot + j * 256);
-  }
-}
-
-// The last, partial stage [c0, t1) through registers, zero-filled beyond t1
-// and for rows at or beyond n.
-template <int NB>
-__device__ __noinline__ void ring_fill_tail(const float* __restrict__ x, int n, int64_t d,
-                                            int64_t c0, int64_t t1, float* slot) {
-  for (int s = threadIdx.x; s < Ring<NB>::SLOTS; s += kBlock) {
-    const int row = s / 17, chunk = s % 17;
-    f4 v = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    if (chunk < 16 && row < n) {
-      const int64_t c = c0 + 4 * chunk;
-      const float* src = x + static_cast<int64_t>(row) * d + c;
-      v.x = (c + 0 < t1) ? src[0] : 0.0f;
-      v.y = (c + 1 < t1) ? src[1] : 0.0f;
-      v.z = (c + 2 < t1) ? src[2] : 0.0f;
-      v.w = (c + 3 < t1) ? src[3] : 0.0f;
-    }
-    *reinterpret_cast<f4*>(slot + 4 * s) = v;
-  }
-}
-
-// Blocks (16-row groups) that wave WV's units touch in 16-coordinate group GRP.
-template <int NB, int WV, int GRP>
-__host__ __device__ constexpr unsigned ring_blocks_used() {
-  using S = GramShape<NB>;
-  unsigned mask = 0;
-  for (int i = 0; i < S::UPW; ++i) {
-    const int u = WV + 4 * i;
-    if (GRP / S::GROUPS != u % S::H) continue;
-    mask |= 1u << pair_b1(NB, u / S::H);
-    mask |= 1u << pair_b2(NB, u / S::H);
-  }
-  return mask;
-}
-
-// Multiply-accumulate this wave's units over 16-coordinate group GRP: each
-// block's shifted fragment is read once and shared by the units using it; the
-// first of a unit's 4 MFMAs starts from zero, and the 4 are then added into
-// fp64 (16 products per fp32 accumulation).
-template <int NB, int WV, int GRP>
-__device__ __forceinline__ void ring_group(const float* __restrict__ slot, int n, int ref,
-                                           double (*acc64)[4], int g, int r) {
-  using S = GramShape<NB>;
-  constexpr unsigned used = ring_blocks_used<NB, WV, GRP>();
-  if constexpr (used != 0) {
-    const int c = 4 * GRP + g;
-    const f4 rf = *reinterpret_cast<const f4*>(slot + 4 * ring_slot(ref, c));
-    f4 fr[NB];
+  for (int grp = 0; grp < 8; grp += 2) {
+    const int col = 128 * h + 16 * grp + 4 * g;
+    f4 y0[NB], y1[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      if (!((used >> b) & 1u)) continue;
-      const int row = 16 * b + r;
-      fr[b] = *reinterpret_cast<const f4*>(slot + 4 * ring_slot(row, c)) - rf;
-      if (row >= n) fr[b] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+      y0[b] = *reinterpret_cast<const f4*>(buf + (16 * b + r) * kGramPitch + col);
+      y1[b] = *reinterpret_cast<const f4*>(buf + (16 * b + r) * kGramPitch + col + 16);
     }
-    const f4 zero = f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int i = 0; i < S::UPW; ++i) {
-      const int u = WV + 4 * i;
-      if (GRP / S::GROUPS != u % S::H) continue;
-      const int b1 = pair_b1(NB, u / S::H), b2 = pair_b2(NB, u / S::H);
-      f4 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fr[b1].x, fr[b2].x, zero, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fr[b1].y, fr[b2].y, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fr[b1].z, fr[b2].z, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fr[b1].w, fr[b2].w, acc, 0, 0, 0);
-      acc64[i][0] += static_cast<double>(acc.x);
-      acc64[i][1] += static_cast<double>(acc.y);
-      acc64[i][2] += static_cast<double>(acc.z);
-      acc64[i][3] += static_cast<double>(acc.w);
-    }
+    gram_pairs<NB, PH, 0>(y0, y1, acc64);
   }
 }
 
-template <int NB, int WV>
-__device__ __forceinline__ void ring_compute(const float* __restrict__ slot, int n, int ref,
-                                             double (*acc64)[4], int g, int r) {
-  // sched_barrier: keep each group's LDS reads next to their MFMAs
-  ring_group<NB, WV, 0>(slot, n, ref, acc64, g, r);
-  __builtin_amdgcn_sched_barrier(0);
-  ring_group<NB, WV, 1>(slot, n, ref, acc64, g, r);
-  __builtin_amdgcn_sched_barrier(0);
-  ring_group<NB, WV, 2>(slot, n, ref, acc64, g, r);
-  __builtin_amdgcn_sched_barrier(0);
-  ring_group<NB, WV, 3>(slot, n, ref, acc64, g, r);
-}
-
-// One ring step: wait for stage st (held by `cur`), then refill the buffer
-// freed by stage st - 1 (`next`) with stage st + 2, then multiply stage st.
-// The barrier is a bare s_barrier: each wave first waits for its own loads of
-// stage st (its loads of stage st + 1 may stay in flight) and its LDS
-// operations, so after the barrier every wave's part of stage st is in LDS,
-// and every wave has finished reading stage st - 1. (A full __syncthreads()
-// would also drain the loads of stage st + 1.)
-template <int NB, int WV>
-__device__ __forceinline__ void ring_step(const float* __restrict__ x, int n, int64_t d,
-                                          int64_t k, int64_t mine, int64_t b, int64_t G,
-                                          const float* cur, float* next, int ref,
-                                          double (*acc64)[4], int g, int r) {
-  if (k >= mine) return;
-  if (k + 1 < mine) wait_vmem_lds<Ring<NB>::loads_of(WV)>(); else wait_vmem_lds<0>();
-  __builtin_amdgcn_s_barrier();
-  if (k + 2 < mine) ring_issue<NB, WV>(x, n, d, (b + (k + 2) * G) * kGramStage, next);
-  ring_compute<NB, WV>(cur, n, ref, acc64, g, r);
-}
-
-// This workgroup's stages: global stages blockIdx.x, + gridDim.x, ... (all
-// workgroups stream one compact window of every row at a time, which keeps
-// the pages in flight few). The final partial stage (when 64 does not divide
-// d) belongs to workgroup (d / 64) % gridDim.x and is taken after the ring.
-template <int NB, int WV>
-__device__ __forceinline__ void ring_tile(const float* __restrict__ x, int n, int64_t d, int ref,
-                                          float* s0, float* s1, float* s2, double (*acc64)[4]) {
+// The stages of this workgroup (b, b + G, ...): load, stage in LDS, multiply.
+template <int NB, int PH>
+__device__ __forceinline__ void gram_tile(const float* __restrict__ x, int n, int64_t d, int ref,
+                                          int wave, float* __restrict__ buf, double (*acc64)[4]) {
+  using S = GramShape<NB>;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, r = lane & 15;
-  const int64_t full = d / kGramStage;
+  const int64_t full = d / kGramStage;                      // full stages
+  const int64_t total = full + (full * kGramStage < d ? 1 : 0);
   const int64_t b = blockIdx.x, G = gridDim.x;
-  const int64_t mine = (full > b) ? (full - b + G - 1) / G : 0;  // full stages of this group
-  if (mine > 0) ring_issue<NB, WV>(x, n, d, (b + 0 * G) * kGramStage, s0);
-  if (mine > 1) ring_issue<NB, WV>(x, n, d, (b + 1 * G) * kGramStage, s1);
-  for (int64_t k = 0; k < mine; k += 3) {
-    ring_step<NB, WV>(x, n, d, k, mine, b, G, s0, s2, ref, acc64, g, r);
-    ring_step<NB, WV>(x, n, d, k + 1, mine, b, G, s1, s0, ref, acc64, g, r);
-    ring_step<NB, WV>(x, n, d, k + 2, mine, b, G, s2, s1, ref, acc64, g, r);
-  }
-  if (full * kGramStage < d && full % G == b) {
-    __syncthreads();  // every wave is done with the ring buffers
-    ring_fill_tail<NB>(x, n, d, full * kGramStage, d, s0);
-    __syncthreads();
-    ring_compute<NB, WV>(s0, n, ref, acc64, g, r);
+  const int64_t mine = (total > b) ? (total - b + G - 1) / G : 0;
+  f4 v[S::RPW];
+  f4 vr;
+  auto issue = [&](int64_t k) {
+    const int64_t st = b + k * G;
+    if (st < full) gram_issue<NB, true>(x, n, d, ref, wave, lane, st * kGramStage, v, vr);
+    else gram_issue<NB, false>(x, n, d, ref, wave, lane, st * kGramStage, v, vr);
+  };
+  if (mine > 0) issue(0);
+  for (int64_t k = 0; k < mine; ++k) {
+    lds_barrier();                    // every wave is done with the previous stage
+    gram_put<NB>(buf, wave, lane, v, vr);
+    if (k + 1 < mine) issue(k + 1);   // in flight during the multiply below
+    lds_barrier();                    // the whole stage is in LDS
+    gram_multiply<NB, PH>(buf, wave & 1, g, r, acc64);
   }
 }
 
 template <int NB>
-__global__ __launch_bounds__(kBlock) void k_dist_gram_lds(const float* __restrict__ x, int n,
-                                                           int64_t d, int64_t chunk,
-                                                           const int32_t* __restrict__ ref_idx,
-                                                           double* __restrict__ partial) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2)))
+void k_dist_gram(const float* __restrict__ x, int n, int64_t d,
+                 const int32_t* __restrict__ ref_idx, double* __restrict__ partial) {
   using S = GramShape<NB>;
-  __shared__ __attribute__((aligned(16))) float s0[Ring<NB>::FLOATS];
-  __shared__ __attribute__((aligned(16))) float s1[Ring<NB>::FLOATS];
-  __shared__ __attribute__((aligned(16))) float s2[Ring<NB>::FLOATS];
-  const int wave = threadIdx.x >> 6;
+  __shared__ __attribute__((aligned(16))) float buf[S::ROWS * kGramPitch];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, r = lane & 15;
   const int ref = *ref_idx;
-  (void)chunk;
-  double acc64[S::UPW][4];
+  double acc64[S::PPW][4];
 #pragma unroll
-  for (int i = 0; i < S::UPW; ++i)
+  for (int i = 0; i < S::PPW; ++i)
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc64[i][e] = 0.0;
-  switch (wave) {
-    case 0: ring_tile<NB, 0>(x, n, d, ref, s0, s1, s2, acc64); break;
-    case 1: ring_tile<NB, 1>(x, n, d, ref, s0, s1, s2, acc64); break;
-    case 2: ring_tile<NB, 2>(x, n, d, ref, s0, s1, s2, acc64); break;
-    default: ring_tile<NB, 3>(x, n, d, ref, s0, s1, s2, acc64); break;
-  }
+  if (wave < 2) gram_tile<NB, 0>(x, n, d, ref, wave, buf, acc64);
+  else gram_tile<NB, 1>(x, n, d, ref, wave, buf, acc64);
+
+  // Partials: entry q*256 + row*16 + col holds G[16*b1 + row][16*b2 + col]
+  // (MFMA output: lane l, component e is row 4*(l/16) + e, column l%16); the
+  // two halves of pair q are held by waves 2*(q%2) (h = 0) and 2*(q%2) + 1.
   __syncthreads();
-  // Combine the k-parts of each pair in ascending h (fixed order), one part at
-  // a time through a 256-double window of s0, and write the tile's partials:
-  // entry q*256 + row*16 + col holds G[16*b1 + row][16*b2 + col].
-  double* red = reinterpret_cast<double*>(s0);  // 256 doubles (2 KB <= every ring buffer)
+  double* red = reinterpret_cast<double*>(buf);  // 2 x 256 doubles (4 KB <= buf)
   double* __restrict__ out = partial + blockIdx.x;
   const int64_t stride = gridDim.x;
   const int t = threadIdx.x;
 #pragma unroll
   for (int q = 0; q < S::NBP; ++q) {
-    double v = 0.0;
+    if ((wave >> 1) == (q & 1)) {
 #pragma unroll
-    for (int h = 0; h < S::H; ++h) {
-      const int u = q * S::H + h;
-      if (wave == u % 4) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) red[(4 * g + e) * 16 + r] = acc64[u / 4][e];
-      }
-      __syncthreads();
-      v += red[t];
-      __syncthreads();
+      for (int e = 0; e < 4; ++e) red[(wave & 1) * 256 + (4 * g + e) * 16 + r] = acc64[q / 2][e];
     }
-    out[(q * 256 + t) * stride] = v;
+    __syncthreads();
+    out[(q * 256 + t) * stride] = red[t] + red[256 + t];
+    __syncthreads();
   }
 }
 
@@ -717,25 +455,12 @@ hipError_t launch_direct_dispatch(int n, const float* x, const DistPlan& p, doub
   }
 }
 
-template <int NB, int W>
-hipError_t launch_gram_nw(const float* x, const DistPlan& p, const int32_t* ref, double* partial,
-                          hipStream_t s) {
-  if constexpr (W == 4) {
-    launch("dist_gram", k_dist_gram_lds<NB>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock), 0,
-           s, x, p.n, p.d, p.chunk, ref, partial);
-  } else {
-    launch("dist_gram", k_dist_gram2<NB, W>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock), 0,
-           s, x, p.n, p.d, p.chunk, ref, partial);
-  }
-  return hipGetLastError();
-}
-
 template <int NB>
 hipError_t launch_gram_nb(const float* x, const DistPlan& p, const int32_t* ref, double* partial,
                           hipStream_t s) {
-  if (p.width == 4) return launch_gram_nw<NB, 4>(x, p, ref, partial, s);
-  if (p.width == 2) return launch_gram_nw<NB, 2>(x, p, ref, partial, s);
-  return launch_gram_nw<NB, 1>(x, p, ref, partial, s);
+  launch("dist_gram", k_dist_gram<NB>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock), 0, s, x,
+         p.n, p.d, ref, partial);
+  return hipGetLastError();
 }
 
 size_t align256(size_t b) { return (b + 255) & ~static_cast<size_t>(255); }
@@ -753,44 +478,29 @@ int device_cus() {
   return cus;
 }
 
-template <int NB, int W>
-int gram_blocks_per_cu_nw() {
+template <int NB>
+int gram_blocks_per_cu_nb() {
   int blocks = 0;
-  hipError_t e;
-  if constexpr (W == 4) {
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_dist_gram_lds<NB>, kBlock, 0);
-  } else {
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_dist_gram2<NB, W>, kBlock, 0);
-  }
-  if (e != hipSuccess || blocks <= 0) {
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_dist_gram<NB>, kBlock, 0) !=
+          hipSuccess ||
+      blocks <= 0) {
     (void)hipGetLastError();
     return 2;
   }
   return blocks;
 }
 
-// Resident workgroups per CU of the Gram kernel for (nb, width).
-int gram_blocks_per_cu(int nb, int width) {
-  static int cache[5][5] = {};
-  int& c = cache[nb][width];
+// Resident workgroups per CU of the Gram kernel for nb row blocks.
+int gram_blocks_per_cu(int nb) {
+  static int cache[kGramBlocks + 1] = {};
+  int& c = cache[nb];
   if (c == 0) {
-    int v = 2;
-    switch (nb * 8 + width) {
-      case 1 * 8 + 1: v = gram_blocks_per_cu_nw<1, 1>(); break;
-      case 1 * 8 + 2: v = gram_blocks_per_cu_nw<1, 2>(); break;
-      case 1 * 8 + 4: v = gram_blocks_per_cu_nw<1, 4>(); break;
-      case 2 * 8 + 1: v = gram_blocks_per_cu_nw<2, 1>(); break;
-      case 2 * 8 + 2: v = gram_blocks_per_cu_nw<2, 2>(); break;
-      case 2 * 8 + 4: v = gram_blocks_per_cu_nw<2, 4>(); break;
-      case 3 * 8 + 1: v = gram_blocks_per_cu_nw<3, 1>(); break;
-      case 3 * 8 + 2: v = gram_blocks_per_cu_nw<3, 2>(); break;
-      case 3 * 8 + 4: v = gram_blocks_per_cu_nw<3, 4>(); break;
-      case 4 * 8 + 1: v = gram_blocks_per_cu_nw<4, 1>(); break;
-      case 4 * 8 + 2: v = gram_blocks_per_cu_nw<4, 2>(); break;
-      case 4 * 8 + 4: v = gram_blocks_per_cu_nw<4, 4>(); break;
-      default: break;
+    switch (nb) {
+      case 1: c = gram_blocks_per_cu_nb<1>(); break;
+      case 2: c = gram_blocks_per_cu_nb<2>(); break;
+      case 3: c = gram_blocks_per_cu_nb<3>(); break;
+      default: c = gram_blocks_per_cu_nb<4>(); break;
     }
-    c = v;
   }
   return c;
 }
@@ -801,13 +511,6 @@ int g_direct_max_n = 20;
 
 int direct_max_n() { return __atomic_load_n(&g_direct_max_n, __ATOMIC_RELAXED); }
 void set_direct_max_n(int n) { __atomic_store_n(&g_direct_max_n, n, __ATOMIC_RELAXED); }
-
-int load_width(const float* x, int64_t d) {
-  const uintptr_t a = reinterpret_cast<uintptr_t>(x);
-  if (d % 4 == 0 && a % 16 == 0) return 4;
-  if (d % 2 == 0 && a % 8 == 0) return 2;
-  return 1;
-}
 
 int vector_width(const float* p) { return reinterpret_cast<uintptr_t>(p) % 4 == 0 ? 4 : 1; }
 
@@ -826,11 +529,11 @@ DistPlan plan_distances(int n, int64_t d, const float* x) {
     p.entries = n * (n - 1) / 2;
   } else {
     p.engine = kEngineGram;
-    p.width = load_width(x, d);
+    p.width = vector_width(x);
     // As many workgroups as the device holds resident (at most one per
-    // 64-coordinate stage); workgroup b takes stages b, b + tiles, ...
+    // stage); workgroup b takes stages b, b + tiles, ...
     const int nb = (n + 15) / 16;
-    const int64_t slots = static_cast<int64_t>(device_cus()) * gram_blocks_per_cu(nb, p.width);
+    const int64_t slots = static_cast<int64_t>(device_cus()) * gram_blocks_per_cu(nb);
     const int64_t stages = (d + kGramStage - 1) / kGramStage;
     p.chunk = kGramStage;
     p.entries = nb * (nb + 1) / 2 * 256;

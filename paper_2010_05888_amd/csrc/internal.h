@@ -79,11 +79,8 @@ hipError_t enqueue_bulyan_aggregate(const float* x, int n, int f, int64_t d, con
                                     float* out, hipStream_t s);
 
 // Widest vector load (4, 2 or 1 floats) every row of x supports.
-// Natural-alignment width: 4 if every row start is 16-byte aligned, else 2
-// if 8-byte aligned, else 1 (the Gram engine's direct-to-LDS stage needs it).
-int load_width(const float* x, int64_t d);
-// Width of the register loads of the streaming kernels and the direct
-// engine: 4 (16-byte accesses at dword alignment) for float-aligned pointers.
+// Width of the register loads of the streaming kernels and the distance
+// engines: 4 (16-byte accesses at dword alignment) for float-aligned pointers.
 int vector_width(const float* p);
 
 }  // namespace garfield

@@ -8,11 +8,12 @@ rounding inside a tile (everything across tiles is fp64). Per entry:
   fp32 subtraction; for positive terms that is a relative error of at most
   (16 + 2) u, u = 2^-24.
 * Gram engine: Y = X - x_ref is rounded once (relative u on every y), and each
-  fp32 accumulator sums at most 4 MFMA k-slices of 4 products (16 products,
-  counted as up to 16 roundings, each at most u times the running sum of
-  absolute products) before it is added in fp64. With N_i = ||x_i - x_ref||^2
-  and sum |y_i y_j| <= (N_i + N_j)/2: |dG_ij| <= 8u (N_i + N_j) + u (N_i + N_j)
-  and |dN_i| <= 16u N_i + 2u N_i, so |dD_ij| <= (8*4 + 4) u (N_i + N_j).
+  fp32 accumulator sums at most 8 MFMA k-slices of 4 products (P = 32
+  products, counted as up to P roundings, each at most u times the running
+  sum of absolute products) before it is added in fp64. With
+  N_i = ||x_i - x_ref||^2 and sum |y_i y_j| <= (N_i + N_j)/2:
+  |dG_ij| <= (P/2) u (N_i + N_j) + u (N_i + N_j) and |dN_i| <= P u N_i + 2u N_i,
+  so |dD_ij| <= (2P + 4) u (N_i + N_j).
 
 Decisions. A selection is "pinned" when every decision it makes is separated
 by more than the summed error bounds of the two quantities compared, so any
@@ -28,7 +29,8 @@ import numpy as np
 U = 2.0 ** -24
 DIRECT_LANE_COORDS = 16
 EPS_DIRECT = (DIRECT_LANE_COORDS + 2) * U
-EPS_GRAM = (8 * 4 + 4) * U
+GRAM_PRODUCTS = 32
+EPS_GRAM = (2 * GRAM_PRODUCTS + 4) * U
 
 
 def agg_close(got, want):
