@@ -179,8 +179,8 @@ __global__ __launch_bounds__(kBlock) void k_pick_ref(const double* __restrict__ 
 // Gram engine, step 3: partial sums of G = Y Y^T, Y = X - x_ref, on fp32 MFMA
 // (v_mfma_f32_16x16x4_f32), upper block triangle only.
 //
-// Streaming. A stage is the 16*NB rows (rows at or beyond n alias the
-// reference row, so their Y rows are exactly 0) times kGramStage = 256
+// Streaming. A stage is the 16*NB rows (rows at or beyond n are not loaded;
+// their Y rows are 0) times kGramStage = 256
 // consecutive coordinates: 1 KB of every row, the shortest run that streams
 // well from rows whose starts are not cache-line aligned (row i starts at
 // i * d floats). Wave w loads rows w*4NB .. w*4NB + 4NB - 1 with one 16-byte
@@ -264,21 +264,24 @@ __device__ __forceinline__ void gram_issue(const float* __restrict__ x, int n, i
   };
 #pragma unroll
   for (int i = 0; i < S::RPW; ++i) {
-    const int row = wave * S::RPW + i;
-    load(row < n ? row : ref, v[i]);
+    const int row = wave * S::RPW + i;  // wave-uniform
+    if (row < n) load(row, v[i]);
   }
   load(ref, vr);
 }
 
 // Y = X - x_ref for this wave's rows into the stage buffer (rows at or beyond
-// n hold the reference row, so theirs are exactly 0).
+// n are 0).
 template <int NB>
-__device__ __forceinline__ void gram_put(float* __restrict__ buf, int wave, int lane, const f4* v,
-                                         const f4& vr) {
+__device__ __forceinline__ void gram_put(float* __restrict__ buf, int n, int wave, int lane,
+                                         const f4* v, const f4& vr) {
   using S = GramShape<NB>;
 #pragma unroll
-  for (int i = 0; i < S::RPW; ++i)
-    *reinterpret_cast<f4*>(buf + (wave * S::RPW + i) * kGramPitch + 4 * lane) = v[i] - vr;
+  for (int i = 0; i < S::RPW; ++i) {
+    const int row = wave * S::RPW + i;  // wave-uniform
+    *reinterpret_cast<f4*>(buf + row * kGramPitch + 4 * lane) =
+        row < n ? v[i] - vr : f4{0.0f, 0.0f, 0.0f, 0.0f};
+  }
 }
 
 // Pairs I, I + 1, ... of this wave (pair q = 2I + PH) over two consecutive
@@ -347,7 +350,7 @@ __device__ __forceinline__ void gram_tile(const float* __restrict__ x, int n, in
   if (mine > 0) issue(0);
   for (int64_t k = 0; k < mine; ++k) {
     lds_barrier();                    // every wave is done with the previous stage
-    gram_put<NB>(buf, wave, lane, v, vr);
+    gram_put<NB>(buf, n, wave, lane, v, vr);
     if (k + 1 < mine) issue(k + 1);   // in flight during the multiply below
     lds_barrier();                    // the whole stage is in LDS
     gram_multiply<NB, PH>(buf, wave & 1, g, r, acc64);
@@ -431,14 +434,14 @@ hipError_t launch_direct_nw(const float* x, const DistPlan& p, double* partial, 
 // Widest per-lane load that keeps the n(n-1)/2 accumulators and the n x W
 // loaded values within the registers of four waves per SIMD (16-byte loads
 // stream an n-row read fastest).
-int direct_width_cap(int n) { return n <= 12 ? 4 : (n <= 16 ? 2 : 1); }
+int direct_width_cap(int n) { return n <= 12 ? 4 : (n <= 19 ? 2 : 1); }
 
 template <int N>
 hipError_t launch_direct_n(const float* x, const DistPlan& p, double* partial, hipStream_t s) {
   if constexpr (N <= 12) {
     if (p.width == 4) return launch_direct_nw<N, 4>(x, p, partial, s);
   }
-  if constexpr (N <= 16) {
+  if constexpr (N <= 19) {
     if (p.width >= 2) return launch_direct_nw<N, 2>(x, p, partial, s);
   }
   return launch_direct_nw<N, 1>(x, p, partial, s);
