@@ -134,8 +134,8 @@ def measured_traffic(kernel, key):
     root = os.path.dirname(os.path.abspath(__file__))
     try:
         with open(os.path.join(root, "profiles", "traffic.json")) as fh:
-            entry = json.load(fh).get(kernel)
-        if not entry or entry["workload"] != key:
+            entry = json.load(fh).get(f"{kernel}@workload{key}")
+        if not entry:
             return None
         with open(os.path.join(root, entry["source"]), "rb") as fh:
             digest = hashlib.sha256(fh.read()).hexdigest()[:16]
