@@ -43,6 +43,13 @@ def _parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="time a plain 1 GiB device-to-device copy instead (HBM calibration "
                          "and the reference for the FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--d", type=int, default=None,
+                    help="supplementary run: the workload's rules, n, f and attack at this "
+                         "dimension instead (labelled as such in config.workload)")
+    ap.add_argument("--fig3", action="store_true",
+                    help="the GAR micro-benchmark sweeps of the paper's Fig. 3 instead: one "
+                         "JSON line per (GAR, n, d), aggregation time without and with the "
+                         "copy of the result to host memory")
     return ap.parse_args()
 
 
@@ -192,15 +199,20 @@ def cpu_baseline(w, x_dev, seconds):
 
 
 def bench_workload(key, args):
+    import dataclasses
+
     import torch
 
     import paper_2010_05888_amd as gf
     from paper_2010_05888_amd import synth
 
     w = synth.WORKLOADS[key]
+    if args.d is not None and args.d != w.d:
+        w = dataclasses.replace(w, d=int(args.d),
+                                name=f"{w.name} [supplementary: d={int(args.d)}]")
     dev = torch.device("cuda:0")
     print(f"[bench] workload {key}: {w.name}: generating", file=sys.stderr, flush=True)
-    inp = synth.generate(w, dev)
+    inp = synth.generate(w, dev, d=w.d)
     x = inp.x
     # Consecutive steps alternate between two copies of the input when it is
     # small enough for a step to find the previous step's data still in the
@@ -229,7 +241,20 @@ def bench_workload(key, args):
     print(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step (wall {wall * 1e3 / args.steps:.4f})",
           file=sys.stderr, flush=True)
 
-    # second pass of the same steps with per-kernel HIP events
+    # second pass: the same steps, each between its own pair of events, for the
+    # median and minimum step time (kept out of the timed region above)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for k, (a, b) in enumerate(evs):
+        a.record()
+        step_k(args.warmup + args.steps + k)
+        b.record()
+    torch.cuda.synchronize()
+    per_step = sorted(a.elapsed_time(b) for a, b in evs)
+    ms_median = per_step[len(per_step) // 2]
+    ms_min = per_step[0]
+
+    # third pass of the same steps with per-kernel HIP events
     gf.set_kernel_timing(True)
     for k in range(args.steps):
         step_k(args.warmup + args.steps + k)
@@ -261,6 +286,8 @@ def bench_workload(key, args):
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 6),
+        "ms_per_step_median": round(ms_median, 6),
+        "ms_per_step_min": round(ms_min, 6),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -278,6 +305,73 @@ def bench_workload(key, args):
     del x, inp, steps, copies
     torch.cuda.empty_cache()
     return line
+
+
+FIG3_N = [7, 11, 15, 19, 23, 27, 31, 35, 39, 47, 55, 63]
+FIG3_D = [10**4, 10**5, 10**6, 10**7, 10**8]
+FIG3_MDA_MAX_SUBSETS = 5 * 10**6
+
+
+def fig3_sweep(args):
+    """The paper's GAR micro-benchmark (Section 5.3, Fig. 3): aggregation time of
+    Average, Median, Multi-Krum (m = n - f), Bulyan and MDA with f = floor((n-3)/4),
+    over n at d = 10^7 and over d at n = 17. Inputs: seeded N(0, 1) rows already in
+    HBM. Each point is the mean of `steps` calls after `warmup`; "ms_device" times
+    the calls alone (events around the batch), "ms_with_copy" each call followed by
+    the copy of the aggregate into pinned host memory (as the paper times it)."""
+    import math
+
+    import torch
+
+    import paper_2010_05888_amd as gf
+
+    lib = gf.load()
+    dev = torch.device("cuda:0")
+    s = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    points = [("n", n, 10**7) for n in FIG3_N] + [("d", 17, d) for d in FIG3_D]
+    for sweep, n, d in points:
+        f = (n - 3) // 4
+        g = torch.Generator(device=dev).manual_seed(2010058880 + 1000 * n + int(math.log10(d)))
+        x = torch.randn(n, d, device=dev, generator=g)
+        out = torch.empty(d, dtype=torch.float32, device=dev)
+        host = torch.empty(d, dtype=torch.float32, pin_memory=True)
+        sel = torch.empty(n, dtype=torch.int32, device=dev)
+        px, po, ps = (ctypes.c_void_p(t.data_ptr()) for t in (x, out, sel))
+        calls = {
+            "average": lambda: lib.garfield_average(px, n, d, po, s),
+            "median": lambda: lib.garfield_median(px, n, f, d, None, n, po, s),
+            "multikrum": lambda: lib.garfield_multikrum(px, n, f, d, n - f, po, ps, s),
+            "bulyan": lambda: lib.garfield_bulyan(px, n, f, d, po, ps, s),
+            "mda": lambda: lib.garfield_mda(px, n, f, d, po, ps, s),
+        }
+        for name, call in calls.items():
+            rec = {"sweep": f"fig3-{sweep}", "gar": name, "n": n, "f": f, "d": d}
+            if name == "mda" and math.comb(n, f) > FIG3_MDA_MAX_SUBSETS:
+                rec["skipped"] = f"C(n, f) = {math.comb(n, f)} subsets"
+                print(json.dumps(rec), flush=True)
+                continue
+            for _ in range(args.warmup):
+                if call():
+                    raise RuntimeError(f"libgarfield error in {name}")
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(args.steps):
+                call()
+            b.record()
+            torch.cuda.synchronize()
+            ms_dev = a.elapsed_time(b) / args.steps
+            t0 = time.perf_counter()
+            for _ in range(args.steps):
+                call()
+                host.copy_(out, non_blocking=True)
+                torch.cuda.synchronize()
+            ms_copy = (time.perf_counter() - t0) * 1e3 / args.steps
+            rec.update({"ms_device": round(ms_dev, 5), "ms_with_copy": round(ms_copy, 5),
+                        "input_GBps": round(n * d * 4 / (ms_dev * 1e-3) / 1e9, 2)})
+            print(json.dumps(rec), flush=True)
+        del x, out, host, sel
+        torch.cuda.empty_cache()
 
 
 def main():
@@ -299,6 +393,9 @@ def main():
     gf.load()  # fails loudly when the library is not built
     if args.direct_max_n is not None:
         gf.set_direct_max_n(args.direct_max_n)
+    if args.fig3:
+        fig3_sweep(args)
+        return
     keys = [1, 2, 3, 4, 5] if args.all else [args.workload]
     for key in keys:
         print(json.dumps(bench_workload(key, args)), flush=True)
