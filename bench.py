@@ -46,6 +46,11 @@ def _parse():
     ap.add_argument("--d", type=int, default=None,
                     help="supplementary run: the workload's rules, n, f and attack at this "
                          "dimension instead (labelled as such in config.workload)")
+    ap.add_argument("--segments", type=int, default=1,
+                    help="segmented aggregation: the input cut into this many column "
+                         "segments held as separate tensors (like per-layer gradients); a "
+                         "step accumulates their distances, selects once and aggregates "
+                         "each segment (workloads 2-4)")
     ap.add_argument("--fig3", action="store_true",
                     help="the GAR micro-benchmark sweeps of the paper's Fig. 3 instead: one "
                          "JSON line per (GAR, n, d), aggregation time without and with the "
@@ -220,7 +225,13 @@ def bench_workload(key, args):
     # fresh gradients would. (Reuse within a step is kept.)
     copies = [x] if x.numel() * 4 >= INPUT_RING_BYTES else [x, x.clone()]
     torch.cuda.synchronize()
-    steps = [Step(gf, w, xi) for xi in copies]
+    if args.segments > 1:
+        steps = [SegmentedStep(gf, w, xi, args.segments) for xi in copies]
+        del copies  # the segments are copies of their own
+        copies = [None] * len(steps)
+        torch.cuda.synchronize()
+    else:
+        steps = [Step(gf, w, xi) for xi in copies]
 
     def step_k(k):
         steps[k % len(steps)]()
@@ -264,6 +275,8 @@ def bench_workload(key, args):
     kernels = {k: {"launches": c, "avg_ms": round(t / c, 6)} for k, (c, t) in kt.items()}
     dominant = max(kt, key=lambda k: kt[k][1])
     bound, per_launch = algorithmic(dominant, w)
+    if per_launch and args.segments > 1:
+        per_launch /= args.segments  # every launch covers one of the (equal) segments
     avg_ms = kt[dominant][1] / kt[dominant][0]
     roofline = {"kernel": dominant, "bound": bound, "achieved": None, "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": None, "traffic": measured_traffic(dominant, key),
@@ -294,7 +307,9 @@ def bench_workload(key, args):
         "dtype": "f32",
         "data": "synthetic",
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
-        "config": {"workload": w.name, "rules": list(w.rules), "n": w.n, "f": w.f, "d": w.d,
+        "config": {"workload": w.name + (f" [segmented: {args.segments} segments]"
+                                          if args.segments > 1 else ""),
+                   "rules": list(w.rules), "n": w.n, "f": w.f, "d": w.d,
                    "m": w.m, "seed": w.seed, "byzantine_rows": inp.byzantine,
                    "distance_engine": gf.distance_engine(w.n, w.d),
                    "input_copies": len(copies)},
@@ -310,6 +325,41 @@ def bench_workload(key, args):
 FIG3_N = [7, 11, 15, 19, 23, 27, 31, 35, 39, 47, 55, 63]
 FIG3_D = [10**4, 10**5, 10**6, 10**7, 10**8]
 FIG3_MDA_MAX_SUBSETS = 5 * 10**6
+
+
+class SegmentedStep:
+    """One step of a workload's rule as a segmented aggregation over `k` column
+    segments (separate tensors), with preallocated outputs."""
+
+    RULE = {("multikrum",): "multikrum", ("bulyan",): "bulyan", ("mda",): "mda"}
+
+    def __init__(self, gf, w, x, k):
+        import torch
+
+        if w.rules not in self.RULE:
+            raise SystemExit(f"--segments: workload {w.key} has no segmented form")
+        self.rule = self.RULE[w.rules]
+        n, d = x.shape
+        cuts = [d * i // k for i in range(k + 1)]
+        self.segs = [x[:, a:b].contiguous() for a, b in zip(cuts[:-1], cuts[1:])]
+        self.outs = [torch.empty(s.shape[1], dtype=torch.float32, device=x.device)
+                     for s in self.segs]
+        self.session = gf.Segmented(self.rule, n, w.f, w.m)
+        self.lib = gf.load()
+        self.s = ctypes.c_void_p(torch.cuda.current_stream(x.device).cuda_stream)
+        p = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+        self.args = [(p(s), s.shape[1], p(o)) for s, o in zip(self.segs, self.outs)]
+
+    def __call__(self):
+        lib, h, s = self.lib, self.session._h, self.s
+        codes = [lib.garfield_seg_reset(h, s)]
+        for px, d, _ in self.args:
+            codes.append(lib.garfield_seg_accumulate(h, px, d, s))
+        codes.append(lib.garfield_seg_select(h, None, s))
+        for px, d, po in self.args:
+            codes.append(lib.garfield_seg_aggregate(h, px, d, po, s))
+        if any(codes):
+            raise RuntimeError(f"libgarfield returned {codes}")
 
 
 def fig3_sweep(args):

@@ -132,6 +132,52 @@ garfield_status garfield_mda(const float* x, int n, int f, int64_t d, float* out
 garfield_status garfield_average(const float* x, int n, int64_t d, float* out, void* stream);
 
 /*
+ * Segmented aggregation (per-layer aggregation, Section 4.2). A squared
+ * distance is a sum over coordinates, so the distances between the n full
+ * vectors are the sums of the distances between their segments (for
+ * instance one segment per layer, aggregated as the layers' gradients come
+ * in). A segmented aggregation accumulates the segments' distance matrices,
+ * makes the rule's one selection from the total, then aggregates every
+ * segment with that selection: the result equals the rule applied to the
+ * concatenated vectors (the selection up to the rounding of the fp64 sums,
+ * the aggregate of each segment exactly as the unsegmented call computes
+ * those coordinates).
+ *
+ *   garfield_seg_create(rule, n, f, m, &seg)   rule: GARFIELD_RULE_KRUM,
+ *       _MULTIKRUM (m as for garfield_multikrum), _BULYAN, _MDA, _MEDIAN or
+ *       _AVERAGE; the requirements of the rule are checked here (EINVAL,
+ *       EREQ, ETOOBIG as for the direct calls). Allocates the session's
+ *       n x n fp64 running sum and n int32 selection on the current device
+ *       (ENOMEM on failure) and waits for the device once. The sum starts at 0.
+ *   garfield_seg_accumulate(seg, x, d, stream)   x: device, n x d fp32
+ *       row-major, the same segment of each of the n vectors; adds its
+ *       distances (a no-op for Median and Average).
+ *   garfield_seg_select(seg, sel, stream)   the rule's selection on the sum;
+ *       sel: device, the rule's count of int32 (m, n-2f or n-f), ascending,
+ *       or NULL to keep it only inside the session (a no-op for Median and
+ *       Average).
+ *   garfield_seg_aggregate(seg, x, d, out, stream)   aggregates one segment
+ *       (n x d, as in accumulate) with the session's selection into out
+ *       (device, d fp32). EINVAL before the first select after a reset.
+ *   garfield_seg_reset(seg, stream)   zeroes the sum for the next step.
+ *   garfield_seg_destroy(seg)   waits for the session's device, frees it.
+ *
+ * All enqueued work goes on `stream` in call order; a session must not be
+ * used from two streams at once, and it shares the per-device workspace with
+ * every other call (see above).
+ */
+typedef struct garfield_segmented garfield_segmented;
+
+garfield_status garfield_seg_create(int rule, int n, int f, int m, garfield_segmented** out);
+garfield_status garfield_seg_reset(garfield_segmented* seg, void* stream);
+garfield_status garfield_seg_accumulate(garfield_segmented* seg, const float* x, int64_t d,
+                                        void* stream);
+garfield_status garfield_seg_select(garfield_segmented* seg, int32_t* sel, void* stream);
+garfield_status garfield_seg_aggregate(garfield_segmented* seg, const float* x, int64_t d,
+                                       float* out, void* stream);
+garfield_status garfield_seg_destroy(garfield_segmented* seg);
+
+/*
  * Bytes of workspace one call of `rule` with these sizes uses (0 if the
  * arguments are invalid). Informational: the library allocates it itself.
  */

@@ -74,6 +74,19 @@ def load():
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = st
+    pp = ctypes.POINTER(ctypes.c_void_p)
+    seg_sig = {
+        "garfield_seg_create": [i32, i32, i32, i32, pp],
+        "garfield_seg_reset": [vp, vp],
+        "garfield_seg_accumulate": [vp, vp, i64, vp],
+        "garfield_seg_select": [vp, vp, vp],
+        "garfield_seg_aggregate": [vp, vp, i64, vp, vp],
+        "garfield_seg_destroy": [vp],
+    }
+    for name, args in seg_sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = st
     lib.garfield_workspace_bytes.argtypes = [i32, i32, i32, i64, i32]
     lib.garfield_workspace_bytes.restype = ctypes.c_size_t
     lib.garfield_release.argtypes = []
@@ -226,6 +239,75 @@ def gar(name: str, x: torch.Tensor, f: int, **kw):
     except KeyError:
         raise ValueError(f"unknown rule {name!r}; known: {sorted(RULES)}") from None
     return rule(x, f, **kw)
+
+
+class Segmented:
+    """Segmented aggregation (per-layer, Section 4.2): accumulate the distances
+    of segments of the n vectors (each an n x d_s tensor: the same coordinates
+    of every vector), select once from their sum, then aggregate every segment
+    with that selection. Equal to the rule on the concatenated vectors.
+
+        seg = Segmented("bulyan", n, f)
+        for x_s in segments: seg.accumulate(x_s)
+        sel = seg.select()
+        outs = [seg.aggregate(x_s) for x_s in segments]
+        seg.reset()   # next step
+    """
+
+    def __init__(self, rule: str, n: int, f: int, m: int | None = None):
+        if rule not in ("krum", "multikrum", "bulyan", "mda", "median", "average"):
+            raise ValueError(f"unknown rule {rule!r}")
+        self.rule, self.n, self.f = rule, n, f
+        self.count = {"krum": 1, "multikrum": (n - f) if not m or m <= 0 else m,
+                      "bulyan": n - 2 * f, "mda": n - f}.get(rule, 0)
+        handle = ctypes.c_void_p()
+        _check(load().garfield_seg_create(RULE_IDS[rule], n, f, m or 0, ctypes.byref(handle)),
+               "garfield_seg_create")
+        self._h = handle
+
+    def _seg(self, x):
+        x = _input(x)
+        if x.shape[0] != self.n:
+            raise ValueError(f"segment has {x.shape[0]} rows, the session {self.n}")
+        return x
+
+    def reset(self):
+        s = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        _check(load().garfield_seg_reset(self._h, s), "garfield_seg_reset")
+
+    def accumulate(self, x: torch.Tensor):
+        x = self._seg(x)
+        _check(load().garfield_seg_accumulate(self._h, _ptr(x), x.shape[1], _stream(x)),
+               "garfield_seg_accumulate")
+
+    def select(self, device=None):
+        """The selection (device int32, ascending), or None for Median / Average."""
+        if self.count == 0:
+            return None
+        dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+        sel = torch.empty(self.count, dtype=torch.int32, device=dev)
+        s = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+        _check(load().garfield_seg_select(self._h, _ptr(sel), s), "garfield_seg_select")
+        return sel
+
+    def aggregate(self, x: torch.Tensor) -> torch.Tensor:
+        x = self._seg(x)
+        out = torch.empty(x.shape[1], dtype=torch.float32, device=x.device)
+        _check(load().garfield_seg_aggregate(self._h, _ptr(x), x.shape[1], _ptr(out), _stream(x)),
+               "garfield_seg_aggregate")
+        return out
+
+    def close(self):
+        if self._h:
+            _check(load().garfield_seg_destroy(self._h), "garfield_seg_destroy")
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            if self._h:
+                load().garfield_seg_destroy(self._h)
+        except Exception:
+            pass
 
 
 def workspace_bytes(rule: str, n: int, f: int, d: int, m: int = 0) -> int:

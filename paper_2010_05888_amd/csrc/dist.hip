@@ -422,6 +422,16 @@ __global__ __launch_bounds__(kBlock) void k_write_dist(DistSums ds, double* __re
   for (int idx = threadIdx.x; idx < n * n; idx += kBlock) dist[idx] = dist_entry(ds, idx / n, idx % n);
 }
 
+// Segmented aggregation: add one segment's D into the running n x n sum.
+__global__ __launch_bounds__(kBlock) void k_accumulate_dist(DistSums ds, double* __restrict__ acc) {
+  const int n = ds.n;
+  for (int idx = threadIdx.x; idx < n * n; idx += kBlock) acc[idx] += dist_entry(ds, idx / n, idx % n);
+}
+
+__global__ __launch_bounds__(kBlock) void k_zero_f64(double* __restrict__ p, int count) {
+  for (int idx = threadIdx.x; idx < count; idx += kBlock) p[idx] = 0.0;
+}
+
 
 // ---------------------------------------------------------------------------
 template <int N, int W>
@@ -614,6 +624,16 @@ hipError_t enqueue_distances(const float* x, const DistPlan& p, const DistWorksp
   if (e != hipSuccess) return e;
   launch("sum_tiles", k_sum_tiles, dim3(p.entries), dim3(kBlock), 0, s, ws.partial, p.tiles,
     ws.sums);
+  return hipGetLastError();
+}
+
+hipError_t enqueue_accumulate_dist(const DistSums& ds, double* acc, hipStream_t s) {
+  launch("accumulate_dist", k_accumulate_dist, dim3(1), dim3(kBlock), 0, s, ds, acc);
+  return hipGetLastError();
+}
+
+hipError_t enqueue_zero_f64(double* p, int count, hipStream_t s) {
+  launch("zero", k_zero_f64, dim3(1), dim3(kBlock), 0, s, p, count);
   return hipGetLastError();
 }
 

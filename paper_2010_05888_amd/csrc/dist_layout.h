@@ -14,7 +14,8 @@ namespace garfield {
 //  * direct engine: entry p = pair (i < j), row-major over i, holds D[i][j];
 //  * Gram engine: entry q*256 + r*16 + c holds G[16*b1 + r][16*b2 + c] for the
 //    q-th block pair (b1 <= b2) of the upper block triangle, G = Y Y^T;
-//  * no engine (n < 2 or d == 0): D is all zeros.
+//  * no engine (n < 2 or d == 0): D is all zeros;
+//  * matrix: sums is the full n x n fp64 matrix D, row-major.
 struct DistSums {
   const double* sums;
   int engine;
@@ -35,6 +36,7 @@ __device__ __forceinline__ int gram_entry(int nb, int i, int j) {  // i <= j
 // clamped at 0; identical rows give exactly 0 because their G entries agree.
 __device__ __forceinline__ double dist_entry(const DistSums& ds, int i, int j) {
   if (i == j || ds.engine == kEngineNone) return 0.0;
+  if (ds.engine == kEngineMatrix) return ds.sums[i * ds.n + j];
   const int a = i < j ? i : j, b = i < j ? j : i;
   if (ds.engine == kEngineDirect) return ds.sums[direct_entry(ds.n, a, b)];
   const int nb = (ds.n + 15) / 16;

@@ -6,6 +6,7 @@
 
 #include <map>
 #include <mutex>
+#include <new>
 
 #include "garfield.h"
 #include "garfield_tuning.h"
@@ -83,6 +84,43 @@ garfield_status run_distances(const float* x, int n, int64_t d, size_t extra, Di
   return to_status(enqueue_distances(x, plan, ws, s));
 }
 
+// Requirements of `rule` (Section 3.1) and the number of indices it selects
+// (0: no selection). m <= 0 means n - f for Multi-Krum.
+garfield_status rule_shape(int rule, int n, int f, int* m, int* k) {
+  if (n < 1 || f < 0) return GARFIELD_EINVAL;
+  if (n > GARFIELD_NMAX) return GARFIELD_ETOOBIG;
+  switch (rule) {
+    case GARFIELD_RULE_KRUM:
+    case GARFIELD_RULE_MULTIKRUM:
+      if (n < 2 * f + 3) return GARFIELD_EREQ;
+      if (rule == GARFIELD_RULE_KRUM) *m = 1;
+      if (*m <= 0) *m = n - f;
+      if (*m > n - f) return GARFIELD_EINVAL;
+      *k = *m;
+      return GARFIELD_OK;
+    case GARFIELD_RULE_BULYAN:
+      if (n < 4 * f + 3) return GARFIELD_EREQ;
+      *k = n - 2 * f;
+      return GARFIELD_OK;
+    case GARFIELD_RULE_MDA: {
+      if (n < 2 * f + 1) return GARFIELD_EREQ;
+      const int64_t subsets = binomial(n, f);
+      if (subsets < 0 || subsets > GARFIELD_MDA_MAX_SUBSETS) return GARFIELD_ETOOBIG;
+      *k = n - f;
+      return GARFIELD_OK;
+    }
+    case GARFIELD_RULE_MEDIAN:
+      if (n < 2 * f + 1) return GARFIELD_EREQ;
+      *k = 0;
+      return GARFIELD_OK;
+    case GARFIELD_RULE_AVERAGE:
+      *k = 0;
+      return GARFIELD_OK;
+    default:
+      return GARFIELD_EINVAL;
+  }
+}
+
 static_assert(GARFIELD_NMAX == kNmax, "kernel limit and public limit differ");
 static_assert(GARFIELD_DIRECT_MAX_N_LIMIT == kDirectMaxNLimit, "direct engine limit differs");
 
@@ -90,6 +128,16 @@ static_assert(GARFIELD_DIRECT_MAX_N_LIMIT == kDirectMaxNLimit, "direct engine li
 }  // namespace garfield
 
 using namespace garfield;
+
+// A segmented aggregation: the running sum of the segments' distance matrices
+// and the selection made from it, on the device that created it.
+struct garfield_segmented {
+  int rule = 0, n = 0, f = 0, m = 0, k = 0;
+  int device = 0;
+  double* dacc = nullptr;   // n x n fp64
+  int32_t* sel = nullptr;   // n int32 (the first k hold the selection)
+  bool selected = false;    // a selection has been enqueued since the last reset
+};
 
 extern "C" {
 
@@ -179,6 +227,117 @@ garfield_status garfield_average(const float* x, int n, int64_t d, float* out, v
   if (st != GARFIELD_OK) return st;
   if (d > 0 && !out) return GARFIELD_EINVAL;
   return to_status(enqueue_mean_rows(x, n, d, nullptr, n, out, static_cast<hipStream_t>(stream)));
+}
+
+garfield_status garfield_seg_create(int rule, int n, int f, int m, garfield_segmented** out) {
+  if (!out) return GARFIELD_EINVAL;
+  *out = nullptr;
+  int k = 0;
+  garfield_status st = rule_shape(rule, n, f, &m, &k);
+  if (st != GARFIELD_OK) return st;
+  garfield_segmented* seg = new (std::nothrow) garfield_segmented;
+  if (!seg) return GARFIELD_ENOMEM;
+  seg->rule = rule;
+  seg->n = n;
+  seg->f = f;
+  seg->m = m;
+  seg->k = k;
+  if (hipGetDevice(&seg->device) != hipSuccess ||
+      hipMalloc(&seg->dacc, sizeof(double) * n * n) != hipSuccess ||
+      hipMalloc(&seg->sel, sizeof(int32_t) * n) != hipSuccess ||
+      hipMemset(seg->dacc, 0, sizeof(double) * n * n) != hipSuccess ||
+      hipDeviceSynchronize() != hipSuccess) {
+    (void)hipGetLastError();
+    if (seg->dacc) (void)hipFree(seg->dacc);
+    if (seg->sel) (void)hipFree(seg->sel);
+    delete seg;
+    return GARFIELD_ENOMEM;
+  }
+  *out = seg;
+  return GARFIELD_OK;
+}
+
+garfield_status garfield_seg_reset(garfield_segmented* seg, void* stream) {
+  if (!seg) return GARFIELD_EINVAL;
+  seg->selected = false;
+  return to_status(enqueue_zero_f64(seg->dacc, seg->n * seg->n, static_cast<hipStream_t>(stream)));
+}
+
+garfield_status garfield_seg_accumulate(garfield_segmented* seg, const float* x, int64_t d,
+                                        void* stream) {
+  if (!seg) return GARFIELD_EINVAL;
+  garfield_status st = check_common(x, seg->n, seg->f, d);
+  if (st != GARFIELD_OK) return st;
+  if (seg->k == 0) return GARFIELD_OK;  // Median and Average use no distances
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  DistSums ds;
+  st = run_distances(x, seg->n, d, 0, &ds, nullptr, s);
+  if (st != GARFIELD_OK) return st;
+  return to_status(enqueue_accumulate_dist(ds, seg->dacc, s));
+}
+
+garfield_status garfield_seg_select(garfield_segmented* seg, int32_t* sel, void* stream) {
+  if (!seg) return GARFIELD_EINVAL;
+  if (seg->k == 0) return GARFIELD_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const DistSums ds{seg->dacc, kEngineMatrix, seg->n};
+  hipError_t e = hipSuccess;
+  switch (seg->rule) {
+    case GARFIELD_RULE_KRUM:
+    case GARFIELD_RULE_MULTIKRUM:
+      e = enqueue_krum_select(ds, seg->f, seg->m, seg->sel, s);
+      break;
+    case GARFIELD_RULE_BULYAN:
+      e = enqueue_bulyan_select(ds, seg->f, seg->sel, s);
+      break;
+    default: {  // MDA
+      void* scratch = nullptr;
+      garfield_status st = workspace(mda_scratch_bytes(seg->n, seg->f), &scratch);
+      if (st != GARFIELD_OK) return st;
+      e = enqueue_mda_select(ds, seg->f, scratch, seg->sel, s);
+      break;
+    }
+  }
+  if (e == hipSuccess && sel)
+    e = hipMemcpyAsync(sel, seg->sel, sizeof(int32_t) * seg->k, hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess) seg->selected = true;
+  return to_status(e);
+}
+
+garfield_status garfield_seg_aggregate(garfield_segmented* seg, const float* x, int64_t d,
+                                       float* out, void* stream) {
+  if (!seg) return GARFIELD_EINVAL;
+  garfield_status st = check_common(x, seg->n, seg->f, d);
+  if (st != GARFIELD_OK) return st;
+  if (d > 0 && !out) return GARFIELD_EINVAL;
+  if (seg->k > 0 && !seg->selected) return GARFIELD_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int n = seg->n;
+  switch (seg->rule) {
+    case GARFIELD_RULE_KRUM:
+    case GARFIELD_RULE_MULTIKRUM:
+    case GARFIELD_RULE_MDA:
+      return to_status(enqueue_mean_rows(x, n, d, seg->sel, seg->k, out, s));
+    case GARFIELD_RULE_BULYAN:
+      return to_status(enqueue_bulyan_aggregate(x, n, seg->f, d, seg->sel, out, s));
+    case GARFIELD_RULE_MEDIAN:
+      return to_status(enqueue_median(x, n, d, nullptr, n, out, s));
+    default:  // Average
+      return to_status(enqueue_mean_rows(x, n, d, nullptr, n, out, s));
+  }
+}
+
+garfield_status garfield_seg_destroy(garfield_segmented* seg) {
+  if (!seg) return GARFIELD_OK;
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  (void)hipSetDevice(seg->device);
+  const hipError_t e = hipDeviceSynchronize();
+  (void)hipFree(seg->dacc);
+  (void)hipFree(seg->sel);
+  (void)hipSetDevice(cur);
+  delete seg;
+  return to_status(e);
 }
 
 size_t garfield_workspace_bytes(int rule, int n, int f, int64_t d, int m) {

@@ -15,7 +15,9 @@ constexpr int kGramBlocks = 4;    // Gram engine: at most 4 blocks of 16 rows (n
 constexpr int kProbeRuns = 4;     // reference-row probe: runs of kBlock coordinates
 constexpr int kDirectLaneCoords = 16;  // direct engine: coordinates per lane per tile
 
-enum Engine { kEngineNone = 0, kEngineDirect = 1, kEngineGram = 2 };
+// Where D comes from: nothing ran (all zero), the direct or Gram engine's
+// entry sums, or a full n x n fp64 matrix (segmented aggregation).
+enum Engine { kEngineNone = 0, kEngineDirect = 1, kEngineGram = 2, kEngineMatrix = 3 };
 
 // How the distance step is tiled for (n, d).
 struct DistPlan {
@@ -82,5 +84,10 @@ hipError_t enqueue_bulyan_aggregate(const float* x, int n, int f, int64_t d, con
 // Width of the register loads of the streaming kernels and the distance
 // engines: 4 (16-byte accesses at dword alignment) for float-aligned pointers.
 int vector_width(const float* p);
+
+// Segmented aggregation: acc[i*n + j] += D[i][j] of one segment (all i, j < n;
+// the diagonal stays 0), and acc[0 .. count) = 0.
+hipError_t enqueue_accumulate_dist(const DistSums& ds, double* acc, hipStream_t s);
+hipError_t enqueue_zero_f64(double* p, int count, hipStream_t s);
 
 }  // namespace garfield

@@ -113,3 +113,25 @@ def test_binding_refuses_cpu_tensors():
         gf.krum(torch.zeros((7, 10)), 1)
     with pytest.raises(ValueError):
         gf.median(torch.zeros((7, 10), dtype=torch.float64))
+
+
+def test_segmented_validation_codes(lib):
+    out = ctypes.c_void_p()
+    ref = ctypes.byref(out)
+    R = gf.RULE_IDS
+    assert lib.garfield_seg_create(R["bulyan"], 10, 2, 0, ref) == gf.EREQ    # n < 4f+3
+    assert lib.garfield_seg_create(R["krum"], 6, 2, 0, ref) == gf.EREQ      # n < 2f+3
+    assert lib.garfield_seg_create(R["multikrum"], 7, 1, 7, ref) == gf.EINVAL  # m > n-f
+    assert lib.garfield_seg_create(R["mda"], 6, 3, 0, ref) == gf.EREQ
+    assert lib.garfield_seg_create(R["mda"], 64, 31, 0, ref) == gf.ETOOBIG
+    assert lib.garfield_seg_create(R["median"], 5, 3, 0, ref) == gf.EREQ
+    assert lib.garfield_seg_create(R["average"], 65, 0, 0, ref) == gf.ETOOBIG
+    assert lib.garfield_seg_create(R["dist"], 5, 0, 0, ref) == gf.EINVAL    # not a rule
+    assert lib.garfield_seg_create(42, 5, 0, 0, ref) == gf.EINVAL
+    assert lib.garfield_seg_create(R["average"], 5, 0, 0, None) == gf.EINVAL
+    assert not out.value  # nothing was created
+    assert lib.garfield_seg_accumulate(NULL, FAKE, 10, NULL) == gf.EINVAL
+    assert lib.garfield_seg_select(NULL, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_seg_aggregate(NULL, FAKE, 10, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_seg_reset(NULL, NULL) == gf.EINVAL
+    assert lib.garfield_seg_destroy(NULL) == gf.OK

@@ -1,0 +1,151 @@
+"""GPU parity of segmented aggregation (per-layer aggregation, Section 4.2).
+
+The n vectors are cut into column segments (ragged sizes, one of width 1 and
+one empty). The distances of the segments are accumulated, the rule selects
+once from their sum, and every segment is aggregated with that selection; the
+result must equal the oracle's rule on the concatenated vectors: the same
+selected indices whenever every decision is pinned (the error bound of the sum
+is the sum of the segments' bounds, each for the engine and reference row its
+segment ran with), and aggregates within max(1e-5 |oracle|, 1e-6), bit-exact
+for Krum and odd medians. Each segment's aggregate must also equal, bit for
+bit, the unsegmented library call over the same coordinates.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import parity
+import paper_2010_05888_amd as gf
+from paper_2010_05888_amd import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+SPLIT = [4096, 1, 0, 8191, 7723]   # 20,011 coordinates
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _library():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    gf.load()
+
+
+def _segments(xt):
+    cuts = np.cumsum([0] + SPLIT)
+    return [xt[:, a:b].contiguous() for a, b in zip(cuts[:-1], cuts[1:])]
+
+
+def _bounds(x, segs):
+    """Sum over segments of each segment's distance bound (oracle D of the segment)."""
+    n = x.shape[0]
+    B = np.zeros((n, n))
+    for s in segs:
+        if s.shape[1] == 0:
+            continue
+        xs = s.cpu().numpy()
+        eng = gf.distance_engine(n, xs.shape[1])
+        ref = gf.gram_reference(s) if eng == "gram" else None
+        B += parity.dist_bounds(oracle.pairwise_sqdist(xs), eng, ref)
+    return B
+
+
+def _pinned(rule, x, f, m, D, B):
+    same = parity.identical_rows(D)
+    if rule in ("krum", "multikrum"):
+        _, _, sc = oracle.multikrum(x, f, m, return_scores=True)
+        return parity.krum_pinned(sc, D, B, f, m, same)[0]
+    if rule == "bulyan":
+        _, _, picks, rs = oracle.bulyan(x, f, return_rounds=True)
+        return parity.bulyan_pinned(picks, rs, D, B, x.shape[0], f, same)[0]
+    if rule == "mda":
+        _, so = oracle.mda(x, f)
+        return parity.mda_pinned(D, B, x.shape[0], f, so)[0]
+    return True
+
+
+def _oracle(rule, x, f, m):
+    if rule == "krum":
+        return oracle.krum(x, f)
+    if rule == "multikrum":
+        return oracle.multikrum(x, f, m)
+    if rule == "bulyan":
+        return oracle.bulyan(x, f)
+    if rule == "mda":
+        return oracle.mda(x, f)
+    if rule == "median":
+        return oracle.median(x, f), None
+    return (x.astype(np.float64).sum(0) / x.shape[0]).astype(np.float32), None
+
+
+def _library_full(rule, xt, f, m):
+    if rule in ("krum", "multikrum"):
+        return gf.multikrum(xt, f, 1 if rule == "krum" else m)
+    if rule == "bulyan":
+        return gf.bulyan(xt, f)
+    if rule == "mda":
+        return gf.mda(xt, f)
+    if rule == "median":
+        return gf.median(xt, f), None
+    return gf.average(xt), None
+
+
+CASES = [("krum", 1), ("median", 1), ("multikrum", 2), ("bulyan", 3), ("mda", 4),
+         ("average", 2), ("multikrum", 5)]
+
+
+@pytest.mark.parametrize("rule,key", CASES)
+def test_segmented_equals_concatenated(rule, key):
+    w = synth.WORKLOADS[key]
+    n, f = w.n, w.f
+    m = {"krum": 1, "multikrum": w.m or n - f}.get(rule)
+    seg = gf.Segmented(rule, n, f, m)
+    try:
+        for step in range(2):  # the second step checks reset
+            for attempt in range(5):
+                seed = w.seed + 100 * step + attempt
+                xt = synth.generate(w, DEV, d=sum(SPLIT), seed=seed).x
+                x = xt.cpu().numpy()
+                segs = _segments(xt)
+                D = oracle.pairwise_sqdist(x)
+                if rule in ("krum", "multikrum", "bulyan", "mda") and \
+                        not _pinned(rule, x, f, m, D, _bounds(x, segs)):
+                    continue
+                seg.reset()
+                for s in segs:
+                    seg.accumulate(s)
+                sel = seg.select()
+                outs = [seg.aggregate(s) for s in segs]
+                got = torch.cat(outs).cpu().numpy()
+                want, want_sel = _oracle(rule, x, f, m)
+                if want_sel is not None:
+                    assert sel.cpu().numpy().tolist() == want_sel.tolist(), (rule, seed)
+                if rule in ("krum", "median"):
+                    assert np.array_equal(got, want), (rule, seed)
+                else:
+                    ok, at, err = parity.agg_close(got, want)
+                    assert ok, (rule, seed, at, err)
+                full, full_sel = _library_full(rule, xt, f, m)
+                if full_sel is None or full_sel.cpu().numpy().tolist() == \
+                        (sel.cpu().numpy().tolist() if sel is not None else None):
+                    assert np.array_equal(got, full.cpu().numpy()), (rule, seed)
+                break
+            else:
+                pytest.fail(f"{rule}: no pinned seed in 5 tries at step {step}")
+    finally:
+        seg.close()
+
+
+def test_aggregate_before_select_is_rejected():
+    seg = gf.Segmented("multikrum", 11, 2)
+    try:
+        xt = torch.randn(11, 100, device=DEV)
+        seg.accumulate(xt)
+        with pytest.raises(gf.GarfieldError):
+            seg.aggregate(xt)
+        seg.select()
+        seg.aggregate(xt)
+        seg.reset()
+        with pytest.raises(gf.GarfieldError):
+            seg.aggregate(xt)
+    finally:
+        seg.close()
