@@ -45,10 +45,27 @@ __device__ __forceinline__ double dist_entry(const DistSums& ds, int i, int j) {
   return v > 0.0 ? v : 0.0;
 }
 
-// D into a block-shared n x n array (all threads of the block take part).
+// D into a block-shared n x n array (all threads of the block take part). For
+// the Gram engine the diagonal G_ii is staged first, so that every entry then
+// takes one load; D[i][j] is formed exactly as dist_entry forms it.
 __device__ __forceinline__ void load_dist(const DistSums& ds, double* D) {
   const int n = ds.n;
-  for (int idx = threadIdx.x; idx < n * n; idx += blockDim.x) D[idx] = dist_entry(ds, idx / n, idx % n);
+  if (ds.engine == kEngineGram) {
+    __shared__ double diag[kNmax];
+    const int nb = (n + 15) / 16;
+    if (static_cast<int>(threadIdx.x) < n) diag[threadIdx.x] = ds.sums[gram_entry(nb, threadIdx.x, threadIdx.x)];
+    __syncthreads();
+#pragma unroll 4
+    for (int idx = threadIdx.x; idx < n * n; idx += blockDim.x) {
+      const int i = idx / n, j = idx % n;
+      const int a = i < j ? i : j, b = i < j ? j : i;
+      const double v = (diag[a] + diag[b]) - 2.0 * ds.sums[gram_entry(nb, a, b)];
+      D[idx] = (i == j) ? 0.0 : (v > 0.0 ? v : 0.0);
+    }
+  } else {
+#pragma unroll 4
+    for (int idx = threadIdx.x; idx < n * n; idx += blockDim.x) D[idx] = dist_entry(ds, idx / n, idx % n);
+  }
   __syncthreads();
 }
 

@@ -14,10 +14,12 @@ namespace garfield {
 
 namespace {
 
-// order[i*n + r] = the j != i whose (D[i][j], j) has rank r in row i.
-// Scores then walk a row in ascending distance order, which is the order the
-// distances are added in (so identical rows get bit-identical scores).
-__device__ void load_and_rank(const DistSums& ds, double* D, unsigned char* order) {
+// order[i*n + r] = the j != i whose (D[i][j], j) has rank r in row i (and,
+// if pos is given, pos[i*n + j] = r). Scores then walk a row in ascending
+// distance order, which is the order the distances are added in (so identical
+// rows get bit-identical scores).
+__device__ void load_and_rank(const DistSums& ds, double* D, unsigned char* order,
+                              unsigned char* pos = nullptr) {
   const int n = ds.n;
   load_dist(ds, D);
   for (int idx = threadIdx.x; idx < n * n; idx += blockDim.x) {
@@ -31,8 +33,25 @@ __device__ void load_and_rank(const DistSums& ds, double* D, unsigned char* orde
       rank += (w < v) || (w == v && j2 < j);
     }
     order[i * n + rank] = static_cast<unsigned char>(j);
+    if (pos) pos[idx] = static_cast<unsigned char>(rank);
   }
   __syncthreads();
+}
+
+// Index of the lowest (v, index) over lanes 0..63 of the calling wave (lanes
+// without a candidate pass +inf); every lane receives it. The minimum of
+// (value, index) pairs does not depend on the order of the comparisons.
+__device__ __forceinline__ int wave_argmin(double v, int idx) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const double ov = __shfl_xor(v, off, 64);
+    const int oi = __shfl_xor(idx, off, 64);
+    if (ov < v || (ov == v && oi < idx)) {
+      v = ov;
+      idx = oi;
+    }
+  }
+  return idx;
 }
 
 // Write the indices i < n with flag[i] set, ascending.
@@ -74,48 +93,60 @@ __global__ __launch_bounds__(kBlock) void k_krum_select(DistSums ds, int f, int 
 }
 
 // Bulyan's selection: theta = n-2f rounds; each round scores every remaining
-// vector against the other remaining ones with max(r-f-2, 0) neighbours
+// vector against the other remaining ones with k = max(r-f-2, 0) neighbours
 // (r = vectors remaining) and moves the lowest (score, index) to the
-// selection. The ranking of each row is computed once; a round walks it and
-// skips vectors already selected.
+// selection. Round 0 sums every row's k nearest in ascending order; after
+// that a row's score follows the removals: when the pick p leaves and k drops
+// by one, the new score is the old one minus D[i][p] if p was among i's k
+// nearest, else minus the k-th nearest (tracked by its position in the
+// row's ranking, which then steps back to the previous remaining vector).
+// Thread i < n owns row i; wave 0 takes the argmin.
 __global__ __launch_bounds__(kBlock) void k_bulyan_select(DistSums ds, int f,
                                                           int32_t* __restrict__ sel) {
   const int n = ds.n;
   __shared__ double D[kNmax * kNmax];
   __shared__ unsigned char order[kNmax * kNmax];
+  __shared__ unsigned char pos[kNmax * kNmax];
   __shared__ double score[kNmax];
   __shared__ int active[kNmax];
   __shared__ int picked[kNmax];
-  load_and_rank(ds, D, order);
+  __shared__ int pick;
+  load_and_rank(ds, D, order, pos);
   const int i = threadIdx.x;
+  const int k0 = n - f - 2 > 0 ? n - f - 2 : 0;
+  double s = 0.0;
+  int kth = k0 - 1;  // position in row i's ranking of its k-th nearest remaining
   if (i < n) {
+    for (int r = 0; r < k0; ++r) s += D[i * n + order[i * n + r]];
     active[i] = 1;
     picked[i] = 0;
   }
   __syncthreads();
   const int theta = n - 2 * f;
   for (int round = 0; round < theta; ++round) {
-    const int remaining = n - round;
-    const int k = remaining - f - 2 > 0 ? remaining - f - 2 : 0;
-    if (i < n && active[i]) {
-      double s = 0.0;
-      int taken = 0;
-      for (int r = 0; r < n - 1 && taken < k; ++r) {
-        const int j = order[i * n + r];
-        if (active[j]) {
-          s += D[i * n + j];
-          ++taken;
-        }
+    if (round > 0 && i < n && active[i]) {
+      const int p = pick;
+      const int k = n - round - f - 2;  // neighbours this round (one fewer than last round)
+      if (k <= 0) {
+        s = 0.0;
+      } else if (pos[i * n + p] < kth) {
+        s -= D[i * n + p];
+      } else {
+        s -= D[i * n + order[i * n + kth]];
+        do {
+          --kth;
+        } while (kth >= 0 && !active[order[i * n + kth]]);
       }
-      score[i] = s;
     }
+    if (i < n) score[i] = active[i] ? s : __builtin_inf();
     __syncthreads();
-    if (i == 0) {
-      int best = -1;
-      for (int j = 0; j < n; ++j)
-        if (active[j] && (best < 0 || score[j] < score[best])) best = j;
-      active[best] = 0;
-      picked[best] = 1;
+    if (i < 64) {
+      const int best = wave_argmin(i < n ? score[i] : __builtin_inf(), i < n ? i : kNmax);
+      if (i == 0) {
+        active[best] = 0;
+        picked[best] = 1;
+        pick = best;
+      }
     }
     __syncthreads();
   }
@@ -135,10 +166,18 @@ __device__ int64_t binom_dev(int a, int b) {
   return c;
 }
 
+// A thread's subset indices in LDS, position a at a stride of kBlock bytes
+// (neighbouring threads read neighbouring bytes: no bank conflicts).
+struct StridedIdx {
+  unsigned char* base;
+  __device__ unsigned char& operator[](int a) const { return base[a * kBlock]; }
+};
+
 // The rank-th s-subset of {0..n-1} in lexicographic order (rank < C(n, s)).
 // Every loop is bounded by n, so an out-of-range rank cannot hang a thread;
 // it yields the last subset instead.
-__device__ void unrank_subset(int64_t rank, int n, int s, unsigned char* idx) {
+template <typename Idx>
+__device__ void unrank_subset(int64_t rank, int n, int s, Idx idx) {
   int e = 0;
   for (int t = 0; t < s; ++t) {
     const int last = n - s + t;  // largest element position t can hold
@@ -157,12 +196,12 @@ __global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64
                                                        int64_t per, double* __restrict__ bdiam,
                                                        int64_t* __restrict__ brank) {
   __shared__ double D[kNmax * kNmax];
-  __shared__ unsigned char idx_all[kBlock * kNmax];
+  __shared__ unsigned char idx_all[kNmax * kBlock];  // position a of thread t at a*kBlock + t
   __shared__ double rd[kBlock];
   __shared__ int64_t rr[kBlock];
   const int n = ds.n;
   load_dist(ds, D);
-  unsigned char* idx = idx_all + threadIdx.x * kNmax;
+  const StridedIdx idx{idx_all + threadIdx.x};
   const int64_t g = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   const int64_t r0 = g * per;
   const int64_t r1 = (r0 + per < total) ? r0 + per : total;
@@ -194,16 +233,21 @@ __global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64
   rd[threadIdx.x] = best;
   rr[threadIdx.x] = best_r;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    double bd = rd[0];
-    int64_t br = rr[0];
-    for (int t = 1; t < kBlock; ++t)
-      if (rd[t] < bd || (rd[t] == bd && rr[t] < br)) {
-        bd = rd[t];
-        br = rr[t];
+  // minimum (diameter, rank) of the block by a tree (the minimum of such pairs
+  // does not depend on the order of the comparisons)
+  for (int h = kBlock / 2; h > 0; h >>= 1) {
+    if (static_cast<int>(threadIdx.x) < h) {
+      const int o = threadIdx.x + h;
+      if (rd[o] < rd[threadIdx.x] || (rd[o] == rd[threadIdx.x] && rr[o] < rr[threadIdx.x])) {
+        rd[threadIdx.x] = rd[o];
+        rr[threadIdx.x] = rr[o];
       }
-    bdiam[blockIdx.x] = bd;
-    brank[blockIdx.x] = br;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    bdiam[blockIdx.x] = rd[0];
+    brank[blockIdx.x] = rr[0];
   }
 }
 
