@@ -9,7 +9,8 @@
  *
  * Common conventions for every entry point below:
  *   - x is a DEVICE pointer to n input vectors of d fp32 values, row-major:
- *     vector i occupies x[i*d .. i*d+d-1]. It is only read.
+ *     vector i occupies x[i*d .. i*d+d-1]. It is only read. It must be
+ *     4-byte aligned (as every fp32 allocation is; GARFIELD_EINVAL otherwise).
  *   - out, sel, dist and rows are DEVICE pointers owned by the caller. The
  *     library never frees caller memory and never writes outside the sizes
  *     stated per function.

@@ -35,10 +35,11 @@ int garfield_tuning_distance_engine(int n, long long d);
 int garfield_tuning_gram_reference(const float* x, int n, long long d, void* stream);
 
 /*
- * Per-kernel timing. While on, every call records a HIP event before and
- * after each kernel it launches, on the call's stream. Turning it on or off
- * (either way) waits for the device and drops the records collected so far.
- * Returns the previous setting.
+ * Per-kernel timing. While on, every kernel a call launches is launched with
+ * a pair of HIP events that the runtime stamps at the start and the end of
+ * that kernel's own dispatch (hipExtLaunchKernelGGL), on the call's stream.
+ * Turning it on or off (either way) waits for the device and drops the
+ * records collected so far. Returns the previous setting.
  */
 int garfield_tuning_set_kernel_timing(int on);
 

@@ -3,12 +3,13 @@
 // the paper's complexity discussion in Section 5.3 attributes the quadratic
 // growth in n to it).
 //
-// The coordinates are cut into tiles of `chunk` consecutive coordinates, one
-// workgroup per tile. Each tile writes one fp64 partial sum per entry (entry-
-// major: partial[entry * tiles + tile]); k_sum_tiles then adds the tiles of
-// each entry in a fixed order, so D is deterministic and depends only on
-// (n, d), never on scheduling. The consumers build D from the entry sums
-// (dist_layout.h). Two engines:
+// Every workgroup of the distance kernel is a tile: the direct engine cuts the
+// coordinates into tiles of `chunk` consecutive coordinates, the Gram engine
+// gives workgroup b the 256-coordinate stages b, b + G, b + 2G, ... Each tile
+// writes one fp64 partial sum per entry (entry-major: partial[entry * tiles +
+// tile]); k_sum_tiles then adds the tiles of each entry in a fixed order, so D
+// is deterministic and depends only on (n, d), never on scheduling. The
+// consumers build D from the entry sums (dist_layout.h). Two engines:
 //
 //  * direct (n <= direct_max_n(), default 20): every lane accumulates (x_i - x_j)^2 for all
 //    n(n-1)/2 pairs in fp32 registers over its coordinates. No cancellation,
@@ -542,7 +543,7 @@ DistPlan plan_distances(int n, int64_t d, const float* x) {
     p.entries = n * (n - 1) / 2;
   } else {
     p.engine = kEngineGram;
-    p.width = vector_width(x);
+    p.width = 4;  // 16-byte loads of 1 KB row runs
     // As many workgroups as the device holds resident (at most one per
     // stage); workgroup b takes stages b, b + tiles, ...
     const int nb = (n + 15) / 16;

@@ -63,7 +63,7 @@ size_t align256(size_t b) { return (b + 255) & ~size_t{255}; }
 // Checks shared by every rule.
 garfield_status check_common(const float* x, int n, int f, int64_t d) {
   if (n < 1 || f < 0 || d < 0) return GARFIELD_EINVAL;
-  if (d > 0 && !x) return GARFIELD_EINVAL;
+  if (d > 0 && (!x || reinterpret_cast<uintptr_t>(x) % sizeof(float) != 0)) return GARFIELD_EINVAL;
   if (n > GARFIELD_NMAX) return GARFIELD_ETOOBIG;
   return GARFIELD_OK;
 }

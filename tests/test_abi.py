@@ -68,6 +68,9 @@ def test_validation_codes(lib):
     # mda: n < 2f+1, and C(n, f) above the cap
     assert lib.garfield_mda(FAKE, 6, 3, 10, FAKE, FAKE, NULL) == gf.EREQ
     assert lib.garfield_mda(FAKE, 64, 31, 10, FAKE, FAKE, NULL) == gf.ETOOBIG
+    # a float pointer that is not 4-byte aligned
+    assert lib.garfield_krum(ctypes.c_void_p(0x1002), 7, 1, 10, FAKE, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_median(ctypes.c_void_p(0x1001), 7, 1, 10, NULL, 0, FAKE, NULL) == gf.EINVAL
     # distances / average
     assert lib.garfield_pairwise_sqdist(FAKE, 5, 10, NULL, NULL) == gf.EINVAL
     assert lib.garfield_average(FAKE, 0, 10, FAKE, NULL) == gf.EINVAL
