@@ -247,7 +247,7 @@ __device__ __forceinline__ void lds_barrier() {
 // Issue the loads of the stage at c0: this wave's rows into v, the reference
 // row into vr (coordinates at or beyond d read as 0 when the stage is the
 // partial last one).
-template <int NB, bool FULL>
+template <int NB, bool PAD, bool FULL>
 __device__ __forceinline__ void gram_issue(const float* __restrict__ x, int n, int64_t d,
                                            int ref, int wave, int lane, int64_t c0, f4* v,
                                            f4& vr) {
@@ -266,37 +266,71 @@ __device__ __forceinline__ void gram_issue(const float* __restrict__ x, int n, i
 #pragma unroll
   for (int i = 0; i < S::RPW; ++i) {
     const int row = wave * S::RPW + i;  // wave-uniform
-    if (row < n) load(row, v[i]);
+    if (!PAD || row < n) load(row, v[i]);
   }
   load(ref, vr);
 }
 
 // Y = X - x_ref for this wave's rows into the stage buffer (rows at or beyond
 // n are 0).
-template <int NB>
+template <int NB, bool PAD>
 __device__ __forceinline__ void gram_put(float* __restrict__ buf, int n, int wave, int lane,
                                          const f4* v, const f4& vr) {
   using S = GramShape<NB>;
 #pragma unroll
   for (int i = 0; i < S::RPW; ++i) {
     const int row = wave * S::RPW + i;  // wave-uniform
-    *reinterpret_cast<f4*>(buf + row * kGramPitch + 4 * lane) =
-        row < n ? v[i] - vr : f4{0.0f, 0.0f, 0.0f, 0.0f};
+    f4 t = v[i] - vr;
+    if (PAD && row >= n) t = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    *reinterpret_cast<f4*>(buf + row * kGramPitch + 4 * lane) = t;
   }
 }
 
 // Pairs I, I + 1, ... of this wave (pair q = 2I + PH) over two consecutive
-// 16-coordinate groups (fragments y0, y1): a chain of eight MFMAs (32
-// products) from zero, then one addition into fp64. A template recursion, so
-// that every pair's blocks are compile-time constants (the fragments stay in
-// fixed registers).
+// 16-coordinate groups (fragments y0, y1): per pair a chain of eight MFMAs (32
+// products) from zero, then one addition into fp64. Two pairs at a time, their
+// chains interleaved, so that no MFMA waits on the one issued just before it.
+// A template recursion, so that every pair's blocks are compile-time
+// constants (the fragments stay in fixed registers).
+template <int NB, int Q>
+__device__ __forceinline__ void gram_flush(const f4& acc, double* acc64) {
+  (void)Q;
+  acc64[0] += static_cast<double>(acc.x);
+  acc64[1] += static_cast<double>(acc.y);
+  acc64[2] += static_cast<double>(acc.z);
+  acc64[3] += static_cast<double>(acc.w);
+}
+
 template <int NB, int PH, int I>
 __device__ __forceinline__ void gram_pairs(const f4* y0, const f4* y1, double (*acc64)[4]) {
   using S = GramShape<NB>;
   constexpr int q = 2 * I + PH;
-  if constexpr (I < S::PPW && q < S::NBP) {
+  constexpr int q2 = 2 * (I + 1) + PH;
+  const f4 zero = f4{0.0f, 0.0f, 0.0f, 0.0f};
+  if constexpr (I + 1 < S::PPW && q2 < S::NBP) {
+    constexpr int a1 = pair_b1(NB, q), a2 = pair_b2(NB, q);
+    constexpr int c1 = pair_b1(NB, q2), c2 = pair_b2(NB, q2);
+    f4 u = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[a1].x, y0[a2].x, zero, 0, 0, 0);
+    f4 w = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[c1].x, y0[c2].x, zero, 0, 0, 0);
+    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[a1].y, y0[a2].y, u, 0, 0, 0);
+    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[c1].y, y0[c2].y, w, 0, 0, 0);
+    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[a1].z, y0[a2].z, u, 0, 0, 0);
+    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[c1].z, y0[c2].z, w, 0, 0, 0);
+    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[a1].w, y0[a2].w, u, 0, 0, 0);
+    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[c1].w, y0[c2].w, w, 0, 0, 0);
+    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[a1].x, y1[a2].x, u, 0, 0, 0);
+    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[c1].x, y1[c2].x, w, 0, 0, 0);
+    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[a1].y, y1[a2].y, u, 0, 0, 0);
+    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[c1].y, y1[c2].y, w, 0, 0, 0);
+    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[a1].z, y1[a2].z, u, 0, 0, 0);
+    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[c1].z, y1[c2].z, w, 0, 0, 0);
+    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[a1].w, y1[a2].w, u, 0, 0, 0);
+    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[c1].w, y1[c2].w, w, 0, 0, 0);
+    gram_flush<NB, q>(u, acc64[I]);
+    gram_flush<NB, q2>(w, acc64[I + 1]);
+    gram_pairs<NB, PH, I + 2>(y0, y1, acc64);
+  } else if constexpr (I < S::PPW && q < S::NBP) {
     constexpr int b1 = pair_b1(NB, q), b2 = pair_b2(NB, q);
-    const f4 zero = f4{0.0f, 0.0f, 0.0f, 0.0f};
     f4 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[b1].x, y0[b2].x, zero, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[b1].y, y0[b2].y, acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[b1].z, y0[b2].z, acc, 0, 0, 0);
@@ -305,11 +339,7 @@ __device__ __forceinline__ void gram_pairs(const f4* y0, const f4* y1, double (*
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[b1].y, y1[b2].y, acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[b1].z, y1[b2].z, acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[b1].w, y1[b2].w, acc, 0, 0, 0);
-    acc64[I][0] += static_cast<double>(acc.x);
-    acc64[I][1] += static_cast<double>(acc.y);
-    acc64[I][2] += static_cast<double>(acc.z);
-    acc64[I][3] += static_cast<double>(acc.w);
-    gram_pairs<NB, PH, I + 1>(y0, y1, acc64);
+    gram_flush<NB, q>(acc, acc64[I]);
   }
 }
 
@@ -330,35 +360,42 @@ __device__ __forceinline__ void gram_multiply(const float* __restrict__ buf, int
   }
 }
 
-// The stages of this workgroup (b, b + G, ...): load, stage in LDS, multiply.
-template <int NB, int PH>
+// The stages of this workgroup: load, stage in LDS, multiply. Workgroups
+// 0 .. G-1 take the full stages b, b + G, ...; when kGramStage does not divide
+// d, one more workgroup (b = G) takes the partial last stage alone, so that the
+// loop over full stages carries no tail handling.
+template <int NB, bool PAD, int PH>
 __device__ __forceinline__ void gram_tile(const float* __restrict__ x, int n, int64_t d, int ref,
                                           int wave, float* __restrict__ buf, double (*acc64)[4]) {
   using S = GramShape<NB>;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, r = lane & 15;
-  const int64_t full = d / kGramStage;                      // full stages
-  const int64_t total = full + (full * kGramStage < d ? 1 : 0);
-  const int64_t b = blockIdx.x, G = gridDim.x;
-  const int64_t mine = (total > b) ? (total - b + G - 1) / G : 0;
+  const int64_t full = d / kGramStage;  // full stages
+  const int64_t b = blockIdx.x;
+  const int64_t G = gridDim.x - (full * kGramStage < d ? 1 : 0);
   f4 v[S::RPW];
   f4 vr;
-  auto issue = [&](int64_t k) {
-    const int64_t st = b + k * G;
-    if (st < full) gram_issue<NB, true>(x, n, d, ref, wave, lane, st * kGramStage, v, vr);
-    else gram_issue<NB, false>(x, n, d, ref, wave, lane, st * kGramStage, v, vr);
-  };
-  if (mine > 0) issue(0);
+  if (b == G) {
+    gram_issue<NB, PAD, false>(x, n, d, ref, wave, lane, full * kGramStage, v, vr);
+    lds_barrier();
+    gram_put<NB, PAD>(buf, n, wave, lane, v, vr);
+    lds_barrier();
+    gram_multiply<NB, PH>(buf, wave & 1, g, r, acc64);
+    return;
+  }
+  const int64_t mine = (full > b) ? (full - b + G - 1) / G : 0;
+  if (mine > 0) gram_issue<NB, PAD, true>(x, n, d, ref, wave, lane, b * kGramStage, v, vr);
   for (int64_t k = 0; k < mine; ++k) {
     lds_barrier();                    // every wave is done with the previous stage
-    gram_put<NB>(buf, n, wave, lane, v, vr);
-    if (k + 1 < mine) issue(k + 1);   // in flight during the multiply below
+    gram_put<NB, PAD>(buf, n, wave, lane, v, vr);
+    if (k + 1 < mine)                 // in flight during the multiply below
+      gram_issue<NB, PAD, true>(x, n, d, ref, wave, lane, (b + (k + 1) * G) * kGramStage, v, vr);
     lds_barrier();                    // the whole stage is in LDS
     gram_multiply<NB, PH>(buf, wave & 1, g, r, acc64);
   }
 }
 
-template <int NB>
+template <int NB, bool PAD>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2)))
 void k_dist_gram(const float* __restrict__ x, int n, int64_t d,
                  const int32_t* __restrict__ ref_idx, double* __restrict__ partial) {
@@ -373,8 +410,8 @@ void k_dist_gram(const float* __restrict__ x, int n, int64_t d,
   for (int i = 0; i < S::PPW; ++i)
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc64[i][e] = 0.0;
-  if (wave < 2) gram_tile<NB, 0>(x, n, d, ref, wave, buf, acc64);
-  else gram_tile<NB, 1>(x, n, d, ref, wave, buf, acc64);
+  if (wave < 2) gram_tile<NB, PAD, 0>(x, n, d, ref, wave, buf, acc64);
+  else gram_tile<NB, PAD, 1>(x, n, d, ref, wave, buf, acc64);
 
   // Partials: entry q*256 + row*16 + col holds G[16*b1 + row][16*b2 + col]
   // (MFMA output: lane l, component e is row 4*(l/16) + e, column l%16); the
@@ -472,8 +509,12 @@ hipError_t launch_direct_dispatch(int n, const float* x, const DistPlan& p, doub
 template <int NB>
 hipError_t launch_gram_nb(const float* x, const DistPlan& p, const int32_t* ref, double* partial,
                           hipStream_t s) {
-  launch("dist_gram", k_dist_gram<NB>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock), 0, s, x,
-         p.n, p.d, ref, partial);
+  if (p.n < 16 * NB)
+    launch("dist_gram", k_dist_gram<NB, true>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock),
+           0, s, x, p.n, p.d, ref, partial);
+  else
+    launch("dist_gram", k_dist_gram<NB, false>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock),
+           0, s, x, p.n, p.d, ref, partial);
   return hipGetLastError();
 }
 
@@ -494,14 +535,16 @@ int device_cus() {
 
 template <int NB>
 int gram_blocks_per_cu_nb() {
-  int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_dist_gram<NB>, kBlock, 0) !=
+  int blocks = 0, blocks_pad = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_dist_gram<NB, false>, kBlock, 0) !=
           hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks_pad, k_dist_gram<NB, true>, kBlock,
+                                                   0) != hipSuccess ||
       blocks <= 0) {
     (void)hipGetLastError();
     return 2;
   }
-  return blocks;
+  return blocks < blocks_pad ? blocks : blocks_pad;  // the grid fits either variant
 }
 
 // Resident workgroups per CU of the Gram kernel for nb row blocks.
@@ -547,11 +590,13 @@ DistPlan plan_distances(int n, int64_t d, const float* x) {
     // As many workgroups as the device holds resident (at most one per
     // stage); workgroup b takes stages b, b + tiles, ...
     const int nb = (n + 15) / 16;
+    // The partial last stage, if any, takes one workgroup of its own.
     const int64_t slots = static_cast<int64_t>(device_cus()) * gram_blocks_per_cu(nb);
-    const int64_t stages = (d + kGramStage - 1) / kGramStage;
+    const int64_t full = d / kGramStage;
+    const int64_t tail = full * kGramStage < d ? 1 : 0;
     p.chunk = kGramStage;
     p.entries = nb * (nb + 1) / 2 * 256;
-    p.tiles = stages < slots ? stages : slots;
+    p.tiles = (full < slots - tail ? full : slots - tail) + tail;
     return p;
   }
   p.tiles = (d + p.chunk - 1) / p.chunk;
