@@ -34,8 +34,10 @@ def _parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=21)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
-    ap.add_argument("--all", action="store_true", help="one line per workload (1..5)")
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6],
+                    help="1-5: the paper's workload shapes; 6: supplementary, the iterated "
+                         "Multi-Krum variant on workload 2's shape")
+    ap.add_argument("--all", action="store_true", help="one line per workload (1..6)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time of the oracle baseline (0 disables it)")
     ap.add_argument("--direct-max-n", type=int, default=None,
@@ -50,7 +52,7 @@ def _parse():
                     help="segmented aggregation: the input cut into this many column "
                          "segments held as separate tensors (like per-layer gradients); a "
                          "step accumulates their distances, selects once and aggregates "
-                         "each segment (workloads 2-4)")
+                         "each segment (workloads 2-4 and 6)")
     ap.add_argument("--fig3", action="store_true",
                     help="the GAR micro-benchmark sweeps of the paper's Fig. 3 instead: one "
                          "JSON line per (GAR, n, d), aggregation time without and with the "
@@ -109,6 +111,9 @@ class Step:
             codes.append(lib.garfield_median(self.px, n, f, d, None, n, self.pout2, s))
         elif rules == ("multikrum",):
             codes.append(lib.garfield_multikrum(self.px, n, f, d, w.m, self.pout, self.psel, s))
+        elif rules == ("multikrum_iterated",):
+            codes.append(lib.garfield_multikrum_iterated(self.px, n, f, d, w.m, self.pout,
+                                                         self.psel, s))
         elif rules == ("bulyan",):
             codes.append(lib.garfield_bulyan(self.px, n, f, d, self.pout, self.psel, s))
         elif rules == ("mda",):
@@ -128,7 +133,8 @@ def algorithmic(kernel, w):
     if kernel in ("dist_direct", "dist_gram"):
         return "hbm", 4.0 * n * d
     if kernel == "mean_rows":
-        k = {"krum": 1, "multikrum": w.m, "mda": n - f}.get(w.rules[0], n)
+        k = {"krum": 1, "multikrum": w.m, "multikrum_iterated": w.m,
+             "mda": n - f}.get(w.rules[0], n)
         return "hbm", 4.0 * (k + 1) * d
     if kernel == "median":
         k = w.m if w.rules == ("multikrum-median",) else n
@@ -138,19 +144,32 @@ def algorithmic(kernel, w):
     return None, None
 
 
+def source_digest(path):
+    """First 16 hex digits of the SHA-256 of a C/C++/HIP source with its
+    comments and whitespace removed: it changes when the code does, not when a
+    comment does. (String literals holding comment markers are not expected in
+    the kernel sources.)"""
+    import hashlib
+    import re
+
+    with open(path) as fh:
+        text = fh.read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    text = re.sub(r"\s+", "", text)
+    return hashlib.sha256(text.encode()).hexdigest()[:16]
+
+
 def measured_traffic(kernel, key):
     """HBM bytes per launch from the committed counter profile, or None when
-    there is none for this kernel and workload or its source changed since."""
-    import hashlib
-
+    there is none for this kernel and workload or its source code changed since."""
     root = os.path.dirname(os.path.abspath(__file__))
     try:
         with open(os.path.join(root, "profiles", "traffic.json")) as fh:
             entry = json.load(fh).get(f"{kernel}@workload{key}")
         if not entry:
             return None
-        with open(os.path.join(root, entry["source"]), "rb") as fh:
-            digest = hashlib.sha256(fh.read()).hexdigest()[:16]
+        digest = source_digest(os.path.join(root, entry["source"]))
         return entry["bytes_per_launch"] if digest == entry["source_sha256"] else None
     except (OSError, KeyError, ValueError):
         return None
@@ -177,6 +196,8 @@ def cpu_baseline(w, x_dev, seconds):
             oracle.median(xs, w.f)
         elif w.rules == ("multikrum",):
             oracle.multikrum(xs, w.f, w.m)
+        elif w.rules == ("multikrum_iterated",):
+            oracle.multikrum_iterated(xs, w.f, w.m)
         elif w.rules == ("bulyan",):
             oracle.bulyan(xs, w.f)
         elif w.rules == ("mda",):
@@ -331,7 +352,8 @@ class SegmentedStep:
     """One step of a workload's rule as a segmented aggregation over `k` column
     segments (separate tensors), with preallocated outputs."""
 
-    RULE = {("multikrum",): "multikrum", ("bulyan",): "bulyan", ("mda",): "mda"}
+    RULE = {("multikrum",): "multikrum", ("multikrum_iterated",): "multikrum_iterated",
+            ("bulyan",): "bulyan", ("mda",): "mda"}
 
     def __init__(self, gf, w, x, k):
         import torch
@@ -363,7 +385,7 @@ class SegmentedStep:
 
 
 def fig3_sweep(args):
-    """The paper's GAR micro-benchmark (Section 5.3, Fig. 3): aggregation time of
+    """The paper's GAR micro-benchmark (Section 6.3, Fig. 3): aggregation time of
     Average, Median, Multi-Krum (m = n - f), Bulyan and MDA with f = floor((n-3)/4),
     over n at d = 10^7 and over d at n = 17. Inputs: seeded N(0, 1) rows already in
     HBM. Each point is the mean of `steps` calls after `warmup`; "ms_device" times
@@ -446,7 +468,7 @@ def main():
     if args.fig3:
         fig3_sweep(args)
         return
-    keys = [1, 2, 3, 4, 5] if args.all else [args.workload]
+    keys = [1, 2, 3, 4, 5, 6] if args.all else [args.workload]
     for key in keys:
         print(json.dumps(bench_workload(key, args)), flush=True)
 

@@ -5,7 +5,7 @@
  * The rules are those of Section 3.1 of "Garfield: System Support for
  * Byzantine Machine Learning" (arXiv:2010.05888): coordinate-wise Median,
  * Krum and Multi-Krum, MDA (minimum-diameter averaging) and Bulyan, plus the
- * plain Average the paper benchmarks them against (Section 5.3).
+ * plain Average the paper benchmarks them against (Section 6.3).
  *
  * Common conventions for every entry point below:
  *   - x is a DEVICE pointer to n input vectors of d fp32 values, row-major:
@@ -64,7 +64,8 @@ typedef enum garfield_rule {
   GARFIELD_RULE_MEDIAN = 3,
   GARFIELD_RULE_BULYAN = 4,
   GARFIELD_RULE_MDA = 5,
-  GARFIELD_RULE_AVERAGE = 6
+  GARFIELD_RULE_AVERAGE = 6,
+  GARFIELD_RULE_MULTIKRUM_ITERATED = 7
 } garfield_rule;
 
 /*
@@ -94,6 +95,20 @@ garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int 
  * sel[0]. out may be NULL. */
 garfield_status garfield_krum(const float* x, int n, int f, int64_t d, float* out, int32_t* sel,
                               void* stream);
+
+/*
+ * Iterated Multi-Krum: Multi-Krum run as repeated Krum, the form Section 4.4
+ * names next to Bulyan when it caches distances across iterations. m rounds;
+ * each selects the vector of lowest (score, index) among those not yet
+ * selected, scoring against the not-yet-selected set with max(r-f-2, 0)
+ * neighbours (r = vectors left) -- the selection stage of garfield_bulyan,
+ * stopped after m rounds. Then the mean of the m selected vectors, as in
+ * garfield_multikrum. Requirements and m as for garfield_multikrum (m = 1 is
+ * Krum). The one-shot and the iterated selection can differ once m > 1.
+ * out: device, d fp32, or NULL.   sel: device, m int32, ascending.
+ */
+garfield_status garfield_multikrum_iterated(const float* x, int n, int f, int64_t d, int m,
+                                            float* out, int32_t* sel, void* stream);
 
 /*
  * Coordinate-wise median (Section 3.1 item 1) over the k vectors whose
@@ -129,7 +144,7 @@ garfield_status garfield_mda(const float* x, int n, int f, int64_t d, float* out
                              void* stream);
 
 /* Average, the non-robust baseline rule of the paper's micro-benchmark
- * (Section 5.3): out[c] = (1/n) sum_i x[i][c], summed in fp64. */
+ * (Section 6.3): out[c] = (1/n) sum_i x[i][c], summed in fp64. */
 garfield_status garfield_average(const float* x, int n, int64_t d, float* out, void* stream);
 
 /*
@@ -145,7 +160,8 @@ garfield_status garfield_average(const float* x, int n, int64_t d, float* out, v
  * those coordinates).
  *
  *   garfield_seg_create(rule, n, f, m, &seg)   rule: GARFIELD_RULE_KRUM,
- *       _MULTIKRUM (m as for garfield_multikrum), _BULYAN, _MDA, _MEDIAN or
+ *       _MULTIKRUM or _MULTIKRUM_ITERATED (m as for garfield_multikrum),
+ *       _BULYAN, _MDA, _MEDIAN or
  *       _AVERAGE; the requirements of the rule are checked here (EINVAL,
  *       EREQ, ETOOBIG as for the direct calls). Allocates the session's
  *       n x n fp64 running sum and n int32 selection on the current device

@@ -53,9 +53,12 @@ def _load():
         lib.oracle_multikrum.argtypes = [f32p, c_int, c_int, c_i64, c_int, f32p, i32p, f64p, f64p]
         lib.oracle_median.argtypes = [f32p, c_int, c_int, c_i64, i32p, c_int, f32p]
         lib.oracle_bulyan.argtypes = [f32p, c_int, c_int, c_i64, f32p, i32p, i32p, f64p, f64p]
+        lib.oracle_multikrum_iterated.argtypes = [f32p, c_int, c_int, c_i64, c_int, f32p, i32p,
+                                                  i32p, f64p, f64p]
         lib.oracle_mda.argtypes = [f32p, c_int, c_int, c_i64, f32p, i32p, f64p, f64p, i64p, f64p]
         for fn in (lib.oracle_pairwise_sqdist, lib.oracle_krum_scores, lib.oracle_multikrum,
-                   lib.oracle_median, lib.oracle_bulyan, lib.oracle_mda):
+                   lib.oracle_median, lib.oracle_bulyan, lib.oracle_mda,
+                   lib.oracle_multikrum_iterated):
             fn.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -121,6 +124,31 @@ def multikrum(x, f: int, m: int | None = None, return_scores: bool = False,
     res = (out, sel[:mm])
     if return_scores:
         res += (scores,)
+    if return_distances:
+        res += (D,)
+    return res
+
+
+def multikrum_iterated(x, f: int, m: int | None = None, return_rounds: bool = False,
+                       return_distances: bool = False):
+    """(aggregate, sel [m] ascending[, picks in order, round scores m x n][, D])."""
+    x = _rows(x)
+    n, d = x.shape
+    mm = (n - f) if (m is None or m <= 0) else m
+    out = np.zeros(d, dtype=np.float32)
+    sel = np.zeros(max(mm, 1), dtype=np.int32)
+    picks = np.zeros(max(mm, 1), dtype=np.int32)
+    rs = np.zeros((max(mm, 1), n), dtype=np.float64)
+    D = np.zeros((n, n), dtype=np.float64)
+    _check(_load().oracle_multikrum_iterated(_ptr(x, ctypes.c_float), n, f, d,
+                                             0 if m is None else m, _ptr(out, ctypes.c_float),
+                                             _ptr(sel, ctypes.c_int32),
+                                             _ptr(picks, ctypes.c_int32),
+                                             _ptr(rs, ctypes.c_double), _ptr(D, ctypes.c_double)),
+           "multikrum_iterated")
+    res = (out, sel[:mm])
+    if return_rounds:
+        res += (picks[:mm], rs[:mm])
     if return_distances:
         res += (D,)
     return res

@@ -12,7 +12,9 @@ pin each other:
   strictly below and at most (k-1)/2 strictly above it) instead of sorting;
 * Bulyan's beta closest values are the beta-subset (by position) whose sorted
   key list is lexicographically smallest;
-* MDA enumerates every (n-f)-subset.
+* MDA enumerates every (n-f)-subset;
+* iterated Multi-Krum repeats the subset-minimum Krum score over the rows
+  left, like Bulyan's selection here.
 
 Definitions follow Section 3.1 of the paper (items 1-4); the readings taken
 where it is silent are the same as the fp64 oracle's (see its header).
@@ -122,6 +124,25 @@ def bulyan(x, f):
         best = min(combinations(range(theta), beta), key=lambda sub: sorted(keys[t] for t in sub))
         out.append(sum((vals[t] for t in best), Fraction(0)) / beta)
     return out, sorted(picks), picks
+
+
+def multikrum_iterated(x, f, m=None):
+    """Returns (aggregate, sel ascending, picks in order) exactly: m rounds,
+    each taking the lowest (score, index) over the rows left, scored against
+    the rows left with max(r - f - 2, 0) neighbours."""
+    n = len(x)
+    if n < 2 * f + 3:
+        raise ValueError("Multi-Krum requires n >= 2f+3")
+    m = n - f if (m is None or m <= 0) else m
+    D = distance_matrix(x)
+    remaining = list(range(n))
+    picks = []
+    for _ in range(m):
+        k = max(len(remaining) - f - 2, 0)
+        _, w = min((krum_score(D, remaining, i, k), i) for i in remaining)
+        picks.append(w)
+        remaining.remove(w)
+    return mean(x, picks), sorted(picks), picks
 
 
 def mda(x, f):

@@ -27,6 +27,9 @@
 //       n_R-f-2 neighbours (clamped at 0), then per coordinate the
 //       beta = theta-2f values closest to the median under the key
 //       (|v - med|, v), averaged.
+//   R8  iterated Multi-Krum: the selection of R6 stopped after m rounds, then
+//       the mean of the m selected rows (Multi-Krum computed by repeating
+//       Krum, as Section 4.4 describes for Multi-Krum and Bulyan).
 //   R7  MDA enumerates the subsets of size n-f in lexicographic order and keeps
 //       the first one of strictly smaller diameter (diameter = largest squared
 //       distance inside the subset).
@@ -101,6 +104,38 @@ void mean_rows(const float* x, int64_t d, const std::vector<int>& rows, float* o
   }
 }
 
+// `rounds` rounds of Krum over the not-yet-selected rows (readings R6, R8):
+// round r scores every remaining row against the other remaining rows with
+// max(|remaining| - f - 2, 0) neighbours and moves the lowest (score, index)
+// to the selection. Returns the picks in the order they were made; fills
+// `picks` (rounds entries) and `round_scores` (rounds*n, +inf for rows already
+// picked) when given.
+std::vector<int> iterated_krum(const double* D, int n, int f, int rounds, int32_t* picks,
+                               double* round_scores) {
+  std::vector<int> remaining(n);
+  for (int i = 0; i < n; ++i) remaining[i] = i;
+  std::vector<int> chosen;
+  for (int r = 0; r < rounds; ++r) {
+    const int k = std::max(static_cast<int>(remaining.size()) - f - 2, 0);
+    double best = 0.0;
+    int best_i = -1;
+    if (round_scores)
+      for (int i = 0; i < n; ++i) round_scores[static_cast<int64_t>(r) * n + i] = 1.0 / 0.0;
+    for (int i : remaining) {  // ascending, so strict < keeps the lower index on ties
+      const double s = krum_score(D, n, remaining, i, k);
+      if (round_scores) round_scores[static_cast<int64_t>(r) * n + i] = s;
+      if (best_i < 0 || s < best) {
+        best = s;
+        best_i = i;
+      }
+    }
+    if (picks) picks[r] = best_i;
+    chosen.push_back(best_i);
+    remaining.erase(std::find(remaining.begin(), remaining.end(), best_i));
+  }
+  return chosen;
+}
+
 // Median of k values: middle element for odd k, mean of the two middle
 // elements for even k (Section 3.1 item 1, reading R5).
 double median_of(std::vector<double>& v) {
@@ -162,6 +197,28 @@ int oracle_multikrum(const float* x, int n, int f, int64_t d, int m, float* out,
   return kOk;
 }
 
+// Iterated Multi-Krum (reading R8): m rounds of Krum over the rows not yet
+// selected, then the mean of the m selected rows. m <= 0 selects n - f.
+// `picks` (optional, m entries) receives the rows in the order they were
+// picked, `round_scores` (optional, m*n fp64) every row's score per round
+// (+inf for rows already picked), `D_out` (optional, n*n) the distances.
+int oracle_multikrum_iterated(const float* x, int n, int f, int64_t d, int m, float* out,
+                              int32_t* sel, int32_t* picks, double* round_scores,
+                              double* D_out) {
+  if (n < 1 || f < 0 || d < 0 || !sel || (d > 0 && (!x || !out))) return kInval;
+  if (n < 2 * f + 3) return kReq;
+  if (m <= 0) m = n - f;
+  if (m > n - f) return kInval;
+  std::vector<double> D(static_cast<size_t>(n) * n);
+  distance_matrix(x, n, d, D.data());
+  if (D_out) std::copy(D.begin(), D.end(), D_out);
+  std::vector<int> chosen = iterated_krum(D.data(), n, f, m, picks, round_scores);
+  std::sort(chosen.begin(), chosen.end());
+  for (int t = 0; t < m; ++t) sel[t] = chosen[t];
+  mean_rows(x, d, chosen, out);
+  return kOk;
+}
+
 // Coordinate-wise median (Section 3.1 item 1) over the k rows listed in
 // `rows`, or over all n rows when rows is null (then k must be n).
 int oracle_median(const float* x, int n, int f, int64_t d, const int32_t* rows, int k,
@@ -206,27 +263,7 @@ int oracle_bulyan(const float* x, int n, int f, int64_t d, float* out, int32_t* 
   std::vector<double> D(static_cast<size_t>(n) * n);
   distance_matrix(x, n, d, D.data());
   if (D_out) std::copy(D.begin(), D.end(), D_out);
-  std::vector<int> remaining(n);
-  for (int i = 0; i < n; ++i) remaining[i] = i;
-  std::vector<int> chosen;
-  for (int r = 0; r < theta; ++r) {
-    const int k = std::max(static_cast<int>(remaining.size()) - f - 2, 0);
-    double best = 0.0;
-    int best_i = -1;
-    if (round_scores)
-      for (int i = 0; i < n; ++i) round_scores[static_cast<int64_t>(r) * n + i] = 1.0 / 0.0;
-    for (int i : remaining) {  // ascending, so strict < keeps the lower index on ties
-      const double s = krum_score(D.data(), n, remaining, i, k);
-      if (round_scores) round_scores[static_cast<int64_t>(r) * n + i] = s;
-      if (best_i < 0 || s < best) {
-        best = s;
-        best_i = i;
-      }
-    }
-    if (picks) picks[r] = best_i;
-    chosen.push_back(best_i);
-    remaining.erase(std::find(remaining.begin(), remaining.end(), best_i));
-  }
+  std::vector<int> chosen = iterated_krum(D.data(), n, f, theta, picks, round_scores);
   std::sort(chosen.begin(), chosen.end());
   for (int t = 0; t < theta; ++t) sel[t] = chosen[t];
 #pragma omp parallel

@@ -5,7 +5,7 @@ Thin Python binding over ``libgarfield.so`` (C-ABI declared in
 runs in the library's HIP kernels. PyTorch provides device memory (the input
 and output tensors) and the current stream; nothing here computes on the
 tensors. The interface mirrors the paper's ``init()`` / ``aggregate()`` pair
-(Section 3.3, Aggregation): ``gar(name, x, f)`` aggregates the n rows of an
+(Section 3.2, Aggregation): ``gar(name, x, f)`` aggregates the n rows of an
 ``n x d`` fp32 CUDA/HIP tensor.
 
 If the library has not been built, every call raises ``LibraryMissing``; there
@@ -20,7 +20,8 @@ import torch  # first: libgarfield must bind to the HIP runtime torch has loaded
 
 __all__ = [
     "GarfieldError", "LibraryMissing", "library_path", "load",
-    "pairwise_sqdist", "krum", "multikrum", "median", "bulyan", "mda", "average",
+    "pairwise_sqdist", "krum", "multikrum", "multikrum_iterated", "median", "bulyan", "mda",
+    "average",
     "multikrum_median", "gar", "workspace_bytes", "release", "set_direct_max_n",
     "distance_engine", "gram_reference", "set_kernel_timing", "kernel_timing", "RULES",
 ]
@@ -29,7 +30,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libgarfield.so")
 
 OK, EINVAL, EREQ, ETOOBIG, ENOMEM, EHIP = range(6)
-RULE_IDS = {"dist": 0, "krum": 1, "multikrum": 2, "median": 3, "bulyan": 4, "mda": 5, "average": 6}
+RULE_IDS = {"dist": 0, "krum": 1, "multikrum": 2, "median": 3, "bulyan": 4, "mda": 5, "average": 6,
+            "multikrum_iterated": 7}
 NMAX = 64
 
 
@@ -65,6 +67,7 @@ def load():
         "garfield_pairwise_sqdist": [vp, i32, i64, vp, vp],
         "garfield_krum": [vp, i32, i32, i64, vp, vp, vp],
         "garfield_multikrum": [vp, i32, i32, i64, i32, vp, vp, vp],
+        "garfield_multikrum_iterated": [vp, i32, i32, i64, i32, vp, vp, vp],
         "garfield_median": [vp, i32, i32, i64, vp, i32, vp, vp],
         "garfield_bulyan": [vp, i32, i32, i64, vp, vp, vp],
         "garfield_mda": [vp, i32, i32, i64, vp, vp, vp],
@@ -157,6 +160,20 @@ def multikrum(x: torch.Tensor, f: int, m: int | None = None, aggregate: bool = T
     return out, sel[:mm]
 
 
+def multikrum_iterated(x: torch.Tensor, f: int, m: int | None = None, aggregate: bool = True):
+    """(aggregate or None, sel) -- m rounds of Krum, each over the vectors not
+    selected yet (Bulyan's selection stopped after m rounds), then their mean."""
+    x = _input(x)
+    n, d = x.shape
+    mm = (n - f) if (m is None or m <= 0) else m
+    sel = torch.empty(max(mm, 1), dtype=torch.int32, device=x.device)
+    out = torch.empty(d, dtype=torch.float32, device=x.device) if aggregate else None
+    _check(load().garfield_multikrum_iterated(_ptr(x), n, f, d, 0 if m is None else m, _ptr(out),
+                                              _ptr(sel), _stream(x)),
+           "garfield_multikrum_iterated")
+    return out, sel[:mm]
+
+
 def krum(x: torch.Tensor, f: int):
     """(aggregate, sel[1]) -- the vector of lowest Krum score."""
     x = _input(x)
@@ -224,6 +241,7 @@ def multikrum_median(x: torch.Tensor, f: int, m: int | None = None):
 RULES = {
     "krum": lambda x, f, **kw: krum(x, f),
     "multikrum": lambda x, f, m=None, **kw: multikrum(x, f, m),
+    "multikrum_iterated": lambda x, f, m=None, **kw: multikrum_iterated(x, f, m),
     "median": lambda x, f, rows=None, **kw: (median(x, f, rows), None),
     "bulyan": lambda x, f, **kw: bulyan(x, f),
     "mda": lambda x, f, **kw: mda(x, f),
@@ -255,10 +273,12 @@ class Segmented:
     """
 
     def __init__(self, rule: str, n: int, f: int, m: int | None = None):
-        if rule not in ("krum", "multikrum", "bulyan", "mda", "median", "average"):
+        if rule not in ("krum", "multikrum", "multikrum_iterated", "bulyan", "mda", "median",
+                        "average"):
             raise ValueError(f"unknown rule {rule!r}")
         self.rule, self.n, self.f = rule, n, f
-        self.count = {"krum": 1, "multikrum": (n - f) if not m or m <= 0 else m,
+        mm = (n - f) if not m or m <= 0 else m
+        self.count = {"krum": 1, "multikrum": mm, "multikrum_iterated": mm,
                       "bulyan": n - 2 * f, "mda": n - f}.get(rule, 0)
         handle = ctypes.c_void_p()
         _check(load().garfield_seg_create(RULE_IDS[rule], n, f, m or 0, ctypes.byref(handle)),

@@ -1,6 +1,6 @@
 // Pairwise squared distances D[i][j] = sum_c (x_ic - x_jc)^2 -- the O(n^2 d)
 // step shared by Krum, Multi-Krum, MDA and Bulyan (Section 3.1 items 2-4;
-// the paper's complexity discussion in Section 5.3 attributes the quadratic
+// the paper's complexity discussion in Section 6.3 attributes the quadratic
 // growth in n to it).
 //
 // Every workgroup of the distance kernel is a tile: the direct engine cuts the

@@ -92,6 +92,7 @@ garfield_status rule_shape(int rule, int n, int f, int* m, int* k) {
   switch (rule) {
     case GARFIELD_RULE_KRUM:
     case GARFIELD_RULE_MULTIKRUM:
+    case GARFIELD_RULE_MULTIKRUM_ITERATED:
       if (n < 2 * f + 3) return GARFIELD_EREQ;
       if (rule == GARFIELD_RULE_KRUM) *m = 1;
       if (*m <= 0) *m = n - f;
@@ -173,6 +174,23 @@ garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int 
 garfield_status garfield_krum(const float* x, int n, int f, int64_t d, float* out, int32_t* sel,
                               void* stream) {
   return garfield_multikrum(x, n, f, d, 1, out, sel, stream);
+}
+
+garfield_status garfield_multikrum_iterated(const float* x, int n, int f, int64_t d, int m,
+                                            float* out, int32_t* sel, void* stream) {
+  garfield_status st = check_common(x, n, f, d);
+  if (st != GARFIELD_OK) return st;
+  if (!sel) return GARFIELD_EINVAL;
+  if (n < 2 * f + 3) return GARFIELD_EREQ;
+  if (m <= 0) m = n - f;
+  if (m > n - f) return GARFIELD_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  DistSums ds;
+  st = run_distances(x, n, d, 0, &ds, nullptr, s);
+  if (st != GARFIELD_OK) return st;
+  st = to_status(enqueue_krum_rounds(ds, f, m, sel, s));
+  if (st != GARFIELD_OK || !out) return st;
+  return to_status(enqueue_mean_rows(x, n, d, sel, m, out, s));
 }
 
 garfield_status garfield_median(const float* x, int n, int f, int64_t d, const int32_t* rows,
@@ -287,6 +305,9 @@ garfield_status garfield_seg_select(garfield_segmented* seg, int32_t* sel, void*
     case GARFIELD_RULE_MULTIKRUM:
       e = enqueue_krum_select(ds, seg->f, seg->m, seg->sel, s);
       break;
+    case GARFIELD_RULE_MULTIKRUM_ITERATED:
+      e = enqueue_krum_rounds(ds, seg->f, seg->m, seg->sel, s);
+      break;
     case GARFIELD_RULE_BULYAN:
       e = enqueue_bulyan_select(ds, seg->f, seg->sel, s);
       break;
@@ -316,6 +337,7 @@ garfield_status garfield_seg_aggregate(garfield_segmented* seg, const float* x, 
   switch (seg->rule) {
     case GARFIELD_RULE_KRUM:
     case GARFIELD_RULE_MULTIKRUM:
+    case GARFIELD_RULE_MULTIKRUM_ITERATED:
     case GARFIELD_RULE_MDA:
       return to_status(enqueue_mean_rows(x, n, d, seg->sel, seg->k, out, s));
     case GARFIELD_RULE_BULYAN:
@@ -350,6 +372,7 @@ size_t garfield_workspace_bytes(int rule, int n, int f, int64_t d, int m) {
     case GARFIELD_RULE_DIST:
     case GARFIELD_RULE_KRUM:
     case GARFIELD_RULE_MULTIKRUM:
+    case GARFIELD_RULE_MULTIKRUM_ITERATED:
     case GARFIELD_RULE_BULYAN:
       return dist_workspace_bytes(plan_distances(n, d, narrow));
     case GARFIELD_RULE_MDA: {

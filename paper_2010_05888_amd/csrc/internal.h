@@ -62,6 +62,9 @@ hipError_t enqueue_write_dist(const DistSums& ds, double* dist, hipStream_t s);
 // Selection on D (one workgroup each).
 hipError_t enqueue_krum_select(const DistSums& ds, int f, int m, int32_t* sel, hipStream_t s);
 hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStream_t s);
+// `rounds` rounds of Krum over the not-yet-selected vectors (iterated Multi-Krum).
+hipError_t enqueue_krum_rounds(const DistSums& ds, int f, int rounds, int32_t* sel,
+                               hipStream_t s);
 
 // MDA subset search. Scratch: mda_blocks(n, f) x 16 bytes.
 int64_t binomial(int a, int b);  // exact, or -1 if above 2^62

@@ -26,11 +26,12 @@ __device__ void load_and_rank(const DistSums& ds, double* D, unsigned char* orde
     const int i = idx / n, j = idx % n;
     if (i == j) continue;
     const double v = D[idx];
+    const double* row = D + i * n;
     int rank = 0;
-    for (int j2 = 0; j2 < n; ++j2) {
-      if (j2 == i) continue;
-      const double w = D[i * n + j2];
-      rank += (w < v) || (w == v && j2 < j);
+#pragma unroll 8
+    for (int j2 = 0; j2 < n; ++j2) {  // no branch: eight reads in flight at a time
+      const double w = row[j2];
+      rank += (j2 != i) & ((w < v) | ((w == v) & (j2 < j)));
     }
     order[i * n + rank] = static_cast<unsigned char>(j);
     if (pos) pos[idx] = static_cast<unsigned char>(rank);
@@ -92,7 +93,8 @@ __global__ __launch_bounds__(kBlock) void k_krum_select(DistSums ds, int f, int 
   write_flagged(flag, n, sel);
 }
 
-// Bulyan's selection: theta = n-2f rounds; each round scores every remaining
+// Iterated Krum, Bulyan's selection (theta = n-2f rounds) and the iterated
+// Multi-Krum variant (m rounds): each round scores every remaining
 // vector against the other remaining ones with k = max(r-f-2, 0) neighbours
 // (r = vectors remaining) and moves the lowest (score, index) to the
 // selection. Round 0 sums every row's k nearest in ascending order; after
@@ -100,32 +102,29 @@ __global__ __launch_bounds__(kBlock) void k_krum_select(DistSums ds, int f, int 
 // by one, the new score is the old one minus D[i][p] if p was among i's k
 // nearest, else minus the k-th nearest (tracked by its position in the
 // row's ranking, which then steps back to the previous remaining vector).
-// Thread i < n owns row i; wave 0 takes the argmin.
-__global__ __launch_bounds__(kBlock) void k_bulyan_select(DistSums ds, int f,
+// After the ranking the rounds run in wave 0 alone (n <= 64: lane i owns row
+// i), with the remaining set as a 64-bit mask every lane holds, so a round
+// needs no workgroup barrier.
+__global__ __launch_bounds__(kBlock) void k_bulyan_select(DistSums ds, int f, int rounds,
                                                           int32_t* __restrict__ sel) {
   const int n = ds.n;
   __shared__ double D[kNmax * kNmax];
   __shared__ unsigned char order[kNmax * kNmax];
   __shared__ unsigned char pos[kNmax * kNmax];
-  __shared__ double score[kNmax];
-  __shared__ int active[kNmax];
-  __shared__ int picked[kNmax];
-  __shared__ int pick;
   load_and_rank(ds, D, order, pos);
+  if (threadIdx.x >= 64) return;  // no barrier follows
   const int i = threadIdx.x;
   const int k0 = n - f - 2 > 0 ? n - f - 2 : 0;
   double s = 0.0;
   int kth = k0 - 1;  // position in row i's ranking of its k-th nearest remaining
-  if (i < n) {
+  if (i < n)
     for (int r = 0; r < k0; ++r) s += D[i * n + order[i * n + r]];
-    active[i] = 1;
-    picked[i] = 0;
-  }
-  __syncthreads();
-  const int theta = n - 2 * f;
-  for (int round = 0; round < theta; ++round) {
-    if (round > 0 && i < n && active[i]) {
-      const int p = pick;
+  uint64_t active = n == 64 ? ~uint64_t{0} : (uint64_t{1} << n) - 1;
+  uint64_t picked = 0;
+  int p = 0;
+  for (int round = 0; round < rounds; ++round) {
+    const bool mine = i < n && ((active >> i) & 1);
+    if (round > 0 && mine) {
       const int k = n - round - f - 2;  // neighbours this round (one fewer than last round)
       if (k <= 0) {
         s = 0.0;
@@ -135,22 +134,17 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_select(DistSums ds, int f,
         s -= D[i * n + order[i * n + kth]];
         do {
           --kth;
-        } while (kth >= 0 && !active[order[i * n + kth]]);
+        } while (kth >= 0 && !((active >> order[i * n + kth]) & 1));
       }
     }
-    if (i < n) score[i] = active[i] ? s : __builtin_inf();
-    __syncthreads();
-    if (i < 64) {
-      const int best = wave_argmin(i < n ? score[i] : __builtin_inf(), i < n ? i : kNmax);
-      if (i == 0) {
-        active[best] = 0;
-        picked[best] = 1;
-        pick = best;
-      }
-    }
-    __syncthreads();
+    p = __builtin_amdgcn_readfirstlane(
+        wave_argmin(mine ? s : __builtin_inf(), mine ? i : kNmax));
+    if (p >= n) break;  // no vector left (rounds <= n - f keeps this from happening)
+    active &= ~(uint64_t{1} << p);
+    picked |= uint64_t{1} << p;
   }
-  write_flagged(picked, n, sel);
+  if (i < n && ((picked >> i) & 1))
+    sel[__popcll(picked & ((uint64_t{1} << i) - 1))] = i;
 }
 
 // ---------------------------------------------------------------------------
@@ -308,7 +302,13 @@ hipError_t enqueue_krum_select(const DistSums& ds, int f, int m, int32_t* sel, h
 }
 
 hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStream_t s) {
-  launch("bulyan_select", k_bulyan_select, dim3(1), dim3(kBlock), 0, s, ds, f, sel);
+  launch("bulyan_select", k_bulyan_select, dim3(1), dim3(kBlock), 0, s, ds, f, ds.n - 2 * f, sel);
+  return hipGetLastError();
+}
+
+hipError_t enqueue_krum_rounds(const DistSums& ds, int f, int rounds, int32_t* sel,
+                               hipStream_t s) {
+  launch("krum_rounds", k_bulyan_select, dim3(1), dim3(kBlock), 0, s, ds, f, rounds, sel);
   return hipGetLastError();
 }
 

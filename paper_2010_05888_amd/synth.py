@@ -2,9 +2,9 @@
 
 No aggregation-rule arithmetic lives here: this module only draws input
 vectors. The dimensions are the parameter counts of the models the paper
-trains (Section 5.1, Table 1 lists ResNet-50 and VGG; ResNet-18 is used as
+trains (Section 6.1, Table 1 lists ResNet-50 and VGG; ResNet-18 is used as
 the mid-size case), counted with their ImageNet heads; the Byzantine vectors
-follow the attacks Garfield's Byzantine workers implement (Section 3.3: random
+follow the attacks Garfield's Byzantine workers implement (Section 3.2: random
 vectors, reversed/scaled vectors, "little is enough"). Nothing from any
 dataset is used: honest gradients are a shared Gaussian mean plus per-worker
 Gaussian noise.
@@ -49,6 +49,10 @@ WORKLOADS = {
     5: Workload(5, "multikrum m=49 -> median n=64 f=15 d=138357544 (VGG-16)",
                 ("multikrum-median",), 64, 15, 138_357_544, 49, 2010058885,
                 "scaled_mean_-4+gaussian_1", 0.01, 0.01, 15),
+    # supplementary: the iterated Multi-Krum variant on workload 2's shape and recipe
+    6: Workload(6, "multikrum (iterated) m=9 n=11 f=2 d=11173962 (ResNet-18)",
+                ("multikrum_iterated",), 11, 2, 11_173_962, 9, 2010058886, "gaussian_1",
+                0.01, 0.01, 2),
 }
 
 

@@ -58,6 +58,11 @@ def test_validation_codes(lib):
     assert lib.garfield_krum(FAKE, 7, 1, 10, FAKE, NULL, NULL) == gf.EINVAL
     # multikrum: m > n - f
     assert lib.garfield_multikrum(FAKE, 7, 1, 10, 7, FAKE, FAKE, NULL) == gf.EINVAL
+    # iterated multikrum: the same requirements
+    assert lib.garfield_multikrum_iterated(FAKE, 7, 1, 10, 7, FAKE, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_multikrum_iterated(FAKE, 6, 2, 10, 0, FAKE, FAKE, NULL) == gf.EREQ
+    assert lib.garfield_multikrum_iterated(FAKE, 65, 2, 10, 0, FAKE, FAKE, NULL) == gf.ETOOBIG
+    assert lib.garfield_multikrum_iterated(FAKE, 7, 1, 10, 0, FAKE, NULL, NULL) == gf.EINVAL
     # median: n < 2f+1, k out of range with a row list, null out
     assert lib.garfield_median(FAKE, 6, 3, 10, NULL, 0, FAKE, NULL) == gf.EREQ
     assert lib.garfield_median(FAKE, 6, 1, 10, FAKE, 7, FAKE, NULL) == gf.EINVAL
@@ -90,6 +95,7 @@ def test_workspace_bytes(lib):
     big = gf.workspace_bytes("multikrum", 64, 15, 138_357_544)
     assert 0 < small < 64 << 20 and 0 < big < 256 << 20
     assert gf.workspace_bytes("mda", 10, 3, 25_557_032) > 0
+    assert gf.workspace_bytes("multikrum_iterated", 11, 2, 11_173_962) == small
     assert gf.workspace_bytes("mda", 64, 31, 10) == 0
 
 
@@ -125,6 +131,8 @@ def test_segmented_validation_codes(lib):
     assert lib.garfield_seg_create(R["bulyan"], 10, 2, 0, ref) == gf.EREQ    # n < 4f+3
     assert lib.garfield_seg_create(R["krum"], 6, 2, 0, ref) == gf.EREQ      # n < 2f+3
     assert lib.garfield_seg_create(R["multikrum"], 7, 1, 7, ref) == gf.EINVAL  # m > n-f
+    assert lib.garfield_seg_create(R["multikrum_iterated"], 7, 1, 7, ref) == gf.EINVAL
+    assert lib.garfield_seg_create(R["multikrum_iterated"], 6, 2, 0, ref) == gf.EREQ
     assert lib.garfield_seg_create(R["mda"], 6, 3, 0, ref) == gf.EREQ
     assert lib.garfield_seg_create(R["mda"], 64, 31, 0, ref) == gf.ETOOBIG
     assert lib.garfield_seg_create(R["median"], 5, 3, 0, ref) == gf.EREQ

@@ -1,4 +1,4 @@
-"""Full-size parity: the five workloads at their real dimensions.
+"""Full-size parity: the workloads at their real dimensions.
 
 Each input is generated on the GPU, aggregated there exactly as bench.py times
 it (same entry points, same launch configuration), copied to the host and
@@ -41,6 +41,8 @@ def _gpu_results(w, xt):
         return {"krum": (out, sel), "median": (gf.median(xt, f), None)}
     if w.rules == ("multikrum",):
         return {"multikrum": gf.multikrum(xt, f, w.m)}
+    if w.rules == ("multikrum_iterated",):
+        return {"multikrum_iterated": gf.multikrum_iterated(xt, f, w.m)}
     if w.rules == ("bulyan",):
         return {"bulyan": gf.bulyan(xt, f)}
     if w.rules == ("mda",):
@@ -53,7 +55,7 @@ def _host(res):
     return {k: (o.cpu().numpy(), None if s is None else s.cpu().numpy()) for k, (o, s) in res.items()}
 
 
-@pytest.mark.parametrize("key", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("key", [1, 2, 3, 4, 5, 6])
 def test_full_size_workload(key):
     w = synth.WORKLOADS[key]
     for attempt in range(5):
@@ -82,6 +84,13 @@ def test_full_size_workload(key):
             B = parity.dist_bounds(Do, eng, ref)
             pinned, margin = parity.krum_pinned(sc, Do, B, f, w.m, parity.identical_rows(Do))
             want["multikrum"] = (oo, so)
+        elif w.rules == ("multikrum_iterated",):
+            oo, so, picks, rs, Do = oracle.multikrum_iterated(x, f, w.m, return_rounds=True,
+                                                              return_distances=True)
+            B = parity.dist_bounds(Do, eng, ref)
+            pinned, margin = parity.bulyan_pinned(picks, rs, Do, B, w.n, f,
+                                                  parity.identical_rows(Do))
+            want["multikrum_iterated"] = (oo, so)
         elif w.rules == ("bulyan",):
             oo, so, picks, rs, Do = oracle.bulyan(x, f, return_rounds=True, return_distances=True)
             B = parity.dist_bounds(Do, eng, ref)

@@ -120,6 +120,9 @@ def _pinned_inputs(key, d, max_tries=25):
             elif rule == "bulyan":
                 _, _, picks, rs = oracle.bulyan(x, w.f, return_rounds=True)
                 ok &= parity.bulyan_pinned(picks, rs, Do, B, w.n, w.f, same)[0]
+            elif rule == "multikrum_iterated":
+                _, _, picks, rs = oracle.multikrum_iterated(x, w.f, w.m, return_rounds=True)
+                ok &= parity.bulyan_pinned(picks, rs, Do, B, w.n, w.f, same)[0]
             elif rule == "mda":
                 _, sel = oracle.mda(x, w.f)
                 ok &= parity.mda_pinned(Do, B, w.n, w.f, sel)[0]
@@ -145,6 +148,12 @@ def _check_rule(rule, w, x, xt):
         assert sel.cpu().numpy().tolist() == so.tolist()
         ok, at, err = parity.agg_close(out.cpu().numpy(), oo)
         assert ok, (at, err)
+    elif rule == "multikrum_iterated":
+        out, sel = gf.multikrum_iterated(xt, f, w.m)
+        oo, so = oracle.multikrum_iterated(x, f, w.m)
+        assert sel.cpu().numpy().tolist() == so.tolist()
+        ok, at, err = parity.agg_close(out.cpu().numpy(), oo)
+        assert ok, (at, err)
     elif rule == "bulyan":
         out, sel = gf.bulyan(xt, f)
         oo, so = oracle.bulyan(x, f)
@@ -167,7 +176,7 @@ def _check_rule(rule, w, x, xt):
         raise AssertionError(rule)
 
 
-@pytest.mark.parametrize("key", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("key", [1, 2, 3, 4, 5, 6])
 @pytest.mark.parametrize("d", [1000, 4097, 65537])
 def test_workload_rules(key, d):
     w, seed, x, xt = _pinned_inputs(key, d)
@@ -175,7 +184,7 @@ def test_workload_rules(key, d):
         _check_rule(rule, w, x, xt)
 
 
-@pytest.mark.parametrize("key", [1, 2, 3, 4])
+@pytest.mark.parametrize("key", [1, 2, 3, 4, 6])
 def test_workload_rules_other_engine(key):
     # the same rules with the distances on the MFMA Gram engine
     old = gf.set_direct_max_n(1)
@@ -198,6 +207,8 @@ def test_zero_dimension_selects_lowest_indices():
     out, sel = gf.bulyan(x, 1)
     assert sel.cpu().tolist() == [0, 1, 2, 3, 4] and out.numel() == 0
     assert gf.median(x, 1).numel() == 0
+    out, sel = gf.multikrum_iterated(x, 1, 3)
+    assert sel.cpu().tolist() == [0, 1, 2] and out.numel() == 0
     D = gf.pairwise_sqdist(x).cpu().numpy()
     assert np.all(D == 0)
 
@@ -287,6 +298,45 @@ def test_krum_and_mda_small_integer_ties():
                 assert np.array_equal(out.cpu().numpy(), oo)
 
 
+@pytest.mark.parametrize("n,f", [(5, 1), (7, 2), (11, 2), (19, 4), (21, 4), (33, 7), (40, 9),
+                                 (64, 15), (64, 0)])
+def test_multikrum_iterated_shapes(n, f):
+    # both distance engines (n <= 20 direct, larger n Gram), m from 1 to n-f
+    for m in sorted({1, max(1, (n - f) // 2), n - f}):
+        for attempt in range(5):
+            rng = np.random.default_rng(n * 37 + f + 7 * m + 1000 * attempt)
+            x = rng.standard_normal((n, 2999)).astype(np.float32)
+            x *= (1.0 + 0.5 * rng.permutation(n) / n).astype(np.float32)[:, None]
+            x[:f] *= 20.0
+            xt = _to_dev(x)
+            Do = oracle.pairwise_sqdist(x)
+            B, _ = _bounds(x, xt, Do)
+            oo, so, picks, rs = oracle.multikrum_iterated(x, f, m, return_rounds=True)
+            if not parity.bulyan_pinned(picks, rs, Do, B, n, f, parity.identical_rows(Do))[0]:
+                continue
+            out, sel = gf.multikrum_iterated(xt, f, m)
+            assert sel.cpu().numpy().tolist() == so.tolist(), (m, attempt)
+            ok, at, err = parity.agg_close(out.cpu().numpy(), oo)
+            assert ok, (m, attempt, at, err)
+            break
+        else:
+            pytest.fail(f"m={m}: no pinned seed in 5 tries")
+
+
+def test_multikrum_iterated_small_integer_ties():
+    # exact distances on both sides; ties in every round go to the lower index
+    rng = np.random.default_rng(5)
+    for trial in range(30):
+        n = int(rng.integers(3, 20))
+        x = rng.integers(-2, 3, size=(n, 65)).astype(np.float32)
+        for f in range(0, (n - 3) // 2 + 1):
+            for m in sorted({1, n - f}):
+                out, sel = gf.multikrum_iterated(_to_dev(x), f, m)
+                oo, so = oracle.multikrum_iterated(x, f, m)
+                assert sel.cpu().numpy().tolist() == so.tolist(), (trial, n, f, m)
+                assert np.array_equal(out.cpu().numpy(), oo), (trial, n, f, m)
+
+
 @pytest.mark.parametrize("m", [1, 2, 5, 9])
 def test_multikrum_m_range(m):
     w, seed, x, xt = _pinned_inputs(2, 30001)
@@ -358,6 +408,8 @@ def test_invalid_arguments_are_rejected():
     cases = [
         (lambda: gf.krum(x, 2), gf.EREQ),
         (lambda: gf.multikrum(x, 1, 6), gf.EINVAL),
+        (lambda: gf.multikrum_iterated(x, 2), gf.EREQ),
+        (lambda: gf.multikrum_iterated(x, 1, 6), gf.EINVAL),
         (lambda: gf.bulyan(x, 1), gf.EREQ),
         (lambda: gf.median(x, 3), gf.EREQ),
         (lambda: gf.mda(x, 3), gf.EREQ),

@@ -57,6 +57,9 @@ def _pinned(rule, x, f, m, D, B):
     if rule == "bulyan":
         _, _, picks, rs = oracle.bulyan(x, f, return_rounds=True)
         return parity.bulyan_pinned(picks, rs, D, B, x.shape[0], f, same)[0]
+    if rule == "multikrum_iterated":
+        _, _, picks, rs = oracle.multikrum_iterated(x, f, m, return_rounds=True)
+        return parity.bulyan_pinned(picks, rs, D, B, x.shape[0], f, same)[0]
     if rule == "mda":
         _, so = oracle.mda(x, f)
         return parity.mda_pinned(D, B, x.shape[0], f, so)[0]
@@ -68,6 +71,8 @@ def _oracle(rule, x, f, m):
         return oracle.krum(x, f)
     if rule == "multikrum":
         return oracle.multikrum(x, f, m)
+    if rule == "multikrum_iterated":
+        return oracle.multikrum_iterated(x, f, m)
     if rule == "bulyan":
         return oracle.bulyan(x, f)
     if rule == "mda":
@@ -80,6 +85,8 @@ def _oracle(rule, x, f, m):
 def _library_full(rule, xt, f, m):
     if rule in ("krum", "multikrum"):
         return gf.multikrum(xt, f, 1 if rule == "krum" else m)
+    if rule == "multikrum_iterated":
+        return gf.multikrum_iterated(xt, f, m)
     if rule == "bulyan":
         return gf.bulyan(xt, f)
     if rule == "mda":
@@ -90,14 +97,14 @@ def _library_full(rule, xt, f, m):
 
 
 CASES = [("krum", 1), ("median", 1), ("multikrum", 2), ("bulyan", 3), ("mda", 4),
-         ("average", 2), ("multikrum", 5)]
+         ("average", 2), ("multikrum", 5), ("multikrum_iterated", 6)]
 
 
 @pytest.mark.parametrize("rule,key", CASES)
 def test_segmented_equals_concatenated(rule, key):
     w = synth.WORKLOADS[key]
     n, f = w.n, w.f
-    m = {"krum": 1, "multikrum": w.m or n - f}.get(rule)
+    m = {"krum": 1, "multikrum": w.m or n - f, "multikrum_iterated": w.m or n - f}.get(rule)
     seg = gf.Segmented(rule, n, f, m)
     try:
         for step in range(2):  # the second step checks reset
@@ -107,7 +114,7 @@ def test_segmented_equals_concatenated(rule, key):
                 x = xt.cpu().numpy()
                 segs = _segments(xt)
                 D = oracle.pairwise_sqdist(x)
-                if rule in ("krum", "multikrum", "bulyan", "mda") and \
+                if rule in ("krum", "multikrum", "multikrum_iterated", "bulyan", "mda") and \
                         not _pinned(rule, x, f, m, D, _bounds(x, segs)):
                     continue
                 seg.reset()

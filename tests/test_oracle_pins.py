@@ -52,6 +52,10 @@ def test_bruteforce_matches_hand_worked(ex):
         assert sel == bu["sel"] and [str(v) for v in out] == bu["out"]
         if "picks" in bu:
             assert picks == bu["picks"]
+    for mi in ex.get("multikrum_iterated", []):
+        out, sel, picks = bf.multikrum_iterated(x, mi["f"], mi["m"])
+        assert sel == mi["sel"] and picks == mi["picks"]
+        assert [str(v) for v in out] == mi["out"]
 
 
 @pytest.mark.parametrize("ex", _examples(), ids=lambda e: e["name"])
@@ -75,6 +79,10 @@ def test_oracle_matches_hand_worked(ex):
         assert sel.tolist() == bu["sel"] and out.tolist() == [_f32(v) for v in bu["out"]]
         if "picks" in bu:
             assert picks.tolist() == bu["picks"]
+    for mi in ex.get("multikrum_iterated", []):
+        out, sel, picks, _ = oracle.multikrum_iterated(x, mi["f"], mi["m"], return_rounds=True)
+        assert sel.tolist() == mi["sel"] and picks.tolist() == mi["picks"]
+        assert out.tolist() == [_f32(v) for v in mi["out"]]
 
 
 def _tiny_cases(seed, count):
@@ -100,6 +108,10 @@ def _check_against_bf(x):
                 oo, so, sco = oracle.multikrum(x, f, m, return_scores=True)
                 assert so.tolist() == sb, (x, f, m)
                 assert sco.tolist() == [float(s) for s in scb]
+                assert oo.tolist() == [_f32(v) for v in ob], (x, f, m)
+                ob, sb, pb = bf.multikrum_iterated(xl, f, m)
+                oo, so, po, _ = oracle.multikrum_iterated(x, f, m, return_rounds=True)
+                assert so.tolist() == sb and po.tolist() == pb, (x, f, m)
                 assert oo.tolist() == [_f32(v) for v in ob], (x, f, m)
         if n >= 2 * f + 1:
             assert oracle.median(x, f).tolist() == [_f32(v) for v in bf.median(xl, f)], (x, f)
@@ -176,6 +188,22 @@ def test_f_zero_rules_reduce_to_the_mean(n):
     out, sel = oracle.mda(x, 0)
     assert sel.tolist() == list(range(n))
     np.testing.assert_allclose(out, mean, rtol=1e-6, atol=1e-7)
+    out, sel = oracle.multikrum_iterated(x, 0, n)
+    assert sel.tolist() == list(range(n))
+    np.testing.assert_allclose(out, mean, rtol=1e-6, atol=1e-7)
+
+
+def test_iterated_multikrum_m1_is_krum_and_theta_rounds_are_bulyans_picks():
+    rng = np.random.default_rng(12)
+    for n, f in [(5, 1), (7, 1), (11, 2), (19, 4)]:
+        x = rng.standard_normal((n, 64)).astype(np.float32)
+        o1, s1 = oracle.multikrum_iterated(x, f, 1)
+        o2, s2 = oracle.krum(x, f)
+        assert s1.tolist() == s2.tolist() and np.array_equal(o1, o2)
+        if n >= 4 * f + 3:
+            _, sel, picks, _ = oracle.multikrum_iterated(x, f, n - 2 * f, return_rounds=True)
+            _, bsel, bpicks, _ = oracle.bulyan(x, f, return_rounds=True)
+            assert picks.tolist() == bpicks.tolist() and sel.tolist() == bsel.tolist()
 
 
 def test_multikrum_m1_is_krum_and_krum_returns_an_input():
@@ -196,6 +224,7 @@ def _all_rules(x, f):
     if n >= 2 * f + 3:
         res["krum"] = oracle.krum(x, f)
         res["multikrum"] = oracle.multikrum(x, f)
+        res["multikrum_iterated"] = oracle.multikrum_iterated(x, f)
     if n >= 2 * f + 1:
         res["median"] = (oracle.median(x, f), None)
         res["mda"] = oracle.mda(x, f)
@@ -216,6 +245,10 @@ def test_permutation_invariance(n, f):
             # Bulyan's last round runs Krum on 2f+1 vectors with f-1 neighbours:
             # for f = 1 every score is 0 and for f = 2 the closest pair always
             # ties, so the lower index decides and row order matters.
+            continue
+        if name == "multikrum_iterated":
+            # its last two rounds (m = n-f) score with 0 neighbours, so the
+            # lower index decides there as well
             continue
         np.testing.assert_allclose(b[name][0], a[name][0], rtol=1e-6, atol=1e-7, err_msg=name)
         if a[name][1] is not None:
@@ -271,6 +304,12 @@ def test_requirements_are_enforced():
     with pytest.raises(oracle.OracleError) as e:
         oracle.multikrum(x, 1, 6)  # m <= n-f = 5
     assert e.value.code == oracle.EINVAL
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.multikrum_iterated(x, 2)  # needs n >= 2f+3 = 7
+    assert e.value.code == oracle.EREQ
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.multikrum_iterated(x, 1, 6)
+    assert e.value.code == oracle.EINVAL
     # at the bound every rule runs
     oracle.krum(np.zeros((7, 4), np.float32), 2)
     oracle.bulyan(np.zeros((7, 4), np.float32), 1)
@@ -281,6 +320,8 @@ def test_requirements_are_enforced():
 def test_empty_dimension_selects_lowest_indices():
     x = np.zeros((7, 0), dtype=np.float32)
     out, sel = oracle.multikrum(x, 1, 3)
+    assert sel.tolist() == [0, 1, 2] and out.size == 0
+    out, sel = oracle.multikrum_iterated(x, 1, 3)
     assert sel.tolist() == [0, 1, 2] and out.size == 0
     out, sel = oracle.mda(x, 2)
     assert sel.tolist() == [0, 1, 2, 3, 4]
