@@ -53,6 +53,9 @@ def _parse():
                          "segments held as separate tensors (like per-layer gradients); a "
                          "step accumulates their distances, selects once and aggregates "
                          "each segment (workloads 2-4 and 6)")
+    ap.add_argument("--byzantine", action="store_true",
+                    help="the device attack generators and the variance statistics instead: one "
+                         "JSON line per case, at workload 3's and 2's shapes")
     ap.add_argument("--fig3", action="store_true",
                     help="the GAR micro-benchmark sweeps of the paper's Fig. 3 instead: one "
                          "JSON line per (GAR, n, d), aggregation time without and with the "
@@ -446,6 +449,84 @@ def fig3_sweep(args):
         torch.cuda.empty_cache()
 
 
+def byzantine_bench(args):
+    """Byzantine vectors (Section 3.2, Main objects; Section 6.5) and the variance
+    condition's statistics (Section 3.1, Tradeoffs) at the workloads' shapes:
+    the attacks of workload 3 (15 honest rows, 4 Byzantine, ResNet-50 size) and
+    workload 2 (2 random rows, ResNet-18 size), and the variance statistics of
+    workload 2's 9 honest rows against a true gradient. Each line: mean time of
+    `steps` calls after `warmup`, algorithmic bytes (rows read once, rows
+    written once) over that time, and the per-kernel HIP-event times."""
+    import torch
+
+    import paper_2010_05888_amd as gf
+
+    dev = torch.device("cuda:0")
+    cases = [
+        ("little", 15, 4, 25_557_032, 1.5), ("empire", 15, 4, 25_557_032, 0.1),
+        ("reverse", 15, 4, 25_557_032, -100.0), ("random", 0, 2, 11_173_962, 1.0),
+        ("variance", 9, 0, 11_173_962, None),
+    ]
+    for kind, h, nbyz, d, param in cases:
+        g = torch.Generator(device=dev).manual_seed(2010058880 + h + nbyz)
+        honest = torch.randn((max(h, 1), d), device=dev, generator=g) * 0.01 if h else None
+        if kind == "variance":
+            grad = torch.randn(d, device=dev, generator=g) * 0.01
+            stats = torch.empty(2, dtype=torch.float64, device=dev)
+            lib, s = gf.load(), ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+            args_ = (ctypes.c_void_p(honest.data_ptr()), h, d, ctypes.c_void_p(grad.data_ptr()),
+                     ctypes.c_void_p(stats.data_ptr()), s)
+
+            def call():
+                return lib.garfield_variance_stats(*args_)
+            nbytes = (h + 1) * d * 4
+            label = f"variance statistics h={h} d={d} (workload 2's honest rows + true gradient)"
+        else:
+            out = torch.empty((nbyz, d), dtype=torch.float32, device=dev)
+            lib, s = gf.load(), ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+            hp = ctypes.c_void_p(honest.data_ptr()) if honest is not None else None
+            args_ = (gf.ATTACKS[kind], hp, h, d, float(param), 12345, ctypes.c_void_p(out.data_ptr()),
+                     nbyz, s)
+
+            def call():
+                return lib.garfield_attack(*args_)
+            nbytes = {"little": h + nbyz, "empire": h + nbyz, "reverse": 2 * nbyz,
+                      "random": nbyz}[kind] * d * 4
+            label = f"attack {kind} param={param} h={h} nbyz={nbyz} d={d}"
+        for _ in range(args.warmup):
+            if call():
+                raise RuntimeError(f"libgarfield error in {label}")
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(args.steps):
+            call()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / args.steps
+        gf.set_kernel_timing(True)
+        for _ in range(args.steps):
+            call()
+        torch.cuda.synchronize()
+        kt = gf.kernel_timing()
+        gf.set_kernel_timing(False)
+        kernels = {k: {"launches": c, "avg_ms": round(t / c, 6)} for k, (c, t) in kt.items()}
+        dominant = max(kt, key=lambda k: kt[k][1])
+        dom_ms = kt[dominant][1] / kt[dominant][0]
+        dom_bytes = nbytes if kind != "variance" else h * d * 4  # the distance pass reads g
+        print(json.dumps({
+            "bench": "byzantine", "case": label, "ms": round(ms, 5),
+            "algorithmic_bytes": nbytes, "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "pct_hbm_peak": round(100 * nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 1),
+            "roofline": {"kernel": dominant, "bound": "hbm", "bytes_per_launch": dom_bytes,
+                         "avg_ms": round(dom_ms, 6),
+                         "achieved": round(dom_bytes / (dom_ms * 1e-3) / 1e9, 1),
+                         "frac": round(dom_bytes / (dom_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+            "kernels": kernels, "steps": args.steps, "warmup": args.warmup}), flush=True)
+        del honest
+        torch.cuda.empty_cache()
+
+
 def main():
     args = _parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -467,6 +548,9 @@ def main():
         gf.set_direct_max_n(args.direct_max_n)
     if args.fig3:
         fig3_sweep(args)
+        return
+    if args.byzantine:
+        byzantine_bench(args)
         return
     keys = [1, 2, 3, 4, 5, 6] if args.all else [args.workload]
     for key in keys:

@@ -148,6 +148,68 @@ garfield_status garfield_mda(const float* x, int n, int f, int64_t d, float* out
 garfield_status garfield_average(const float* x, int n, int64_t d, float* out, void* stream);
 
 /*
+ * Byzantine rows on the device: the attacks Garfield's Byzantine workers and
+ * servers implement (Section 3.2, Main objects; Section 6.5 uses random
+ * vectors and vectors reversed and amplified by -100). From the h honest
+ * vectors `honest` (device, h x d fp32 row-major, read only), write nbyz
+ * Byzantine vectors to `byz` (device, nbyz x d fp32 row-major, e.g. the last
+ * rows of a rule's input). byz must not overlap honest.
+ *   GARFIELD_ATTACK_REVERSE  byz[b] = param * honest[b % h] (param = -100:
+ *                            reversed and amplified), the product formed in
+ *                            fp64 and rounded once.
+ *   GARFIELD_ATTACK_RANDOM   byz[b][c] = param * N(0, 1) (param = the standard
+ *                            deviation); honest and h are not used. Normals by
+ *                            Box-Muller from Philox4x32-10 (Salmon et al.,
+ *                            SC'11) with key = seed and counter (c/4 low and
+ *                            high 32 bits, b, 0): words 0-1 give coordinates
+ *                            4q and 4q+1, words 2-3 give 4q+2 and 4q+3, each
+ *                            word w mapped to ((w >> 9) + 1/2) 2^-23. A value
+ *                            depends only on (seed, b, c). fp32 arithmetic.
+ *   GARFIELD_ATTACK_LITTLE   "little is enough": byz[b][c] = mean_c - param *
+ *                            std_c, over the h honest values of coordinate c
+ *                            (population standard deviation), in fp64, rounded
+ *                            once; every Byzantine vector is the same.
+ *   GARFIELD_ATTACK_EMPIRE   "fall of empires": byz[b][c] = -param * mean_c.
+ * Requires 0 <= nbyz <= GARFIELD_NMAX, finite param, and for every kind but
+ * RANDOM 1 <= h <= GARFIELD_NMAX.
+ */
+typedef enum garfield_attack_kind {
+  GARFIELD_ATTACK_REVERSE = 0,
+  GARFIELD_ATTACK_RANDOM = 1,
+  GARFIELD_ATTACK_LITTLE = 2,
+  GARFIELD_ATTACK_EMPIRE = 3
+} garfield_attack_kind;
+
+garfield_status garfield_attack(int kind, const float* honest, int h, int64_t d, double param,
+                                uint64_t seed, float* byz, int nbyz, void* stream);
+
+/*
+ * The variance condition of Section 3.1 (Tradeoffs): a rule is safe when
+ * kappa * Delta * sigma <= ||grad L|| for some kappa > 1, with sigma^2 =
+ * E||g - E g||^2 the variance of an honest gradient estimate.
+ *
+ * garfield_variance_stats: from h >= 2 honest gradient estimates g (device,
+ * h x d fp32 row-major) and the true gradient grad (device, d fp32, e.g.
+ * computed on a very large batch), writes stats (device, 2 fp64):
+ *   stats[0] = sum_{i<j} ||g_i - g_j||^2 / (h (h-1)), the unbiased estimate of
+ *              sigma^2 (equal to sum_i ||g_i - mean||^2 / (h-1)), from the
+ *              same distance step the rules use;
+ *   stats[1] = ||grad||^2, summed in fp64 in a fixed order.
+ * h <= GARFIELD_NMAX.
+ *
+ * garfield_delta: Delta for rule GARFIELD_RULE_MDA (the paper's minimum-
+ * diameter rule: 2 sqrt(2) f / (n-f)), GARFIELD_RULE_KRUM
+ * (sqrt(2 (n-f + (f (n-f-2) + f^2 (n-f-1)) / (n-2f-2)))) or
+ * GARFIELD_RULE_MEDIAN (sqrt(n-f)); NaN for other rules, n < 1, f < 0, or n
+ * below the rule's requirement. Host function.
+ * The condition holds for some kappa > 1 iff sqrt(stats[1]) > Delta *
+ * sqrt(stats[0]).
+ */
+garfield_status garfield_variance_stats(const float* g, int h, int64_t d, const float* grad,
+                                        double* stats, void* stream);
+double garfield_delta(int rule, int n, int f);
+
+/*
  * Segmented aggregation (per-layer aggregation, Section 4.2). A squared
  * distance is a sum over coordinates, so the distances between the n full
  * vectors are the sums of the distances between their segments (for

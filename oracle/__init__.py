@@ -55,10 +55,16 @@ def _load():
         lib.oracle_bulyan.argtypes = [f32p, c_int, c_int, c_i64, f32p, i32p, i32p, f64p, f64p]
         lib.oracle_multikrum_iterated.argtypes = [f32p, c_int, c_int, c_i64, c_int, f32p, i32p,
                                                   i32p, f64p, f64p]
+        u32p = ctypes.POINTER(ctypes.c_uint32)
+        lib.oracle_philox4x32_10.argtypes = [u32p, u32p, u32p]
+        lib.oracle_philox4x32_10.restype = None
+        lib.oracle_attack.argtypes = [c_int, f32p, c_int, c_i64, ctypes.c_double, ctypes.c_uint64,
+                                      f32p, c_int]
+        lib.oracle_variance_stats.argtypes = [f32p, c_int, c_i64, f32p, f64p]
         lib.oracle_mda.argtypes = [f32p, c_int, c_int, c_i64, f32p, i32p, f64p, f64p, i64p, f64p]
         for fn in (lib.oracle_pairwise_sqdist, lib.oracle_krum_scores, lib.oracle_multikrum,
                    lib.oracle_median, lib.oracle_bulyan, lib.oracle_mda,
-                   lib.oracle_multikrum_iterated):
+                   lib.oracle_multikrum_iterated, lib.oracle_attack, lib.oracle_variance_stats):
             fn.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -214,3 +220,64 @@ def mda(x, f: int, return_diameters: bool = False, return_distances: bool = Fals
     if return_distances:
         res += (D,)
     return res
+
+
+# --- Byzantine vectors and the variance condition ----------------------------------
+
+ATTACKS = {"reverse": 0, "random": 1, "little": 2, "empire": 3}
+
+
+def philox4x32_10(ctr, key):
+    """The four output words of Philox4x32-10 for a counter (4 words) and key (2)."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    _load().oracle_philox4x32_10(_ptr(c, ctypes.c_uint32), _ptr(k, ctypes.c_uint32),
+                                 _ptr(out, ctypes.c_uint32))
+    return out.tolist()
+
+
+def attack(kind: str, honest, nbyz: int, param: float, seed: int = 0, d: int | None = None):
+    """nbyz x d fp32 Byzantine vectors (reading R9 of the oracle's header)."""
+    if honest is None:
+        h, dd, hp = 0, int(d), None
+    else:
+        honest = _rows(honest)
+        h, dd = honest.shape
+        hp = _ptr(honest, ctypes.c_float)
+    out = np.zeros((nbyz, dd), dtype=np.float32)
+    _check(_load().oracle_attack(ATTACKS[kind], hp, h, dd, float(param),
+                                 seed & 0xFFFFFFFFFFFFFFFF, _ptr(out, ctypes.c_float), nbyz),
+           "attack")
+    return out
+
+
+def variance_stats(g, grad):
+    """[sum_i ||g_i - mean||^2 / (h - 1), ||grad||^2] in fp64 (reading R10)."""
+    g = _rows(g)
+    h, d = g.shape
+    t = np.ascontiguousarray(grad, dtype=np.float32).reshape(-1)
+    stats = np.zeros(2, dtype=np.float64)
+    _check(_load().oracle_variance_stats(_ptr(g, ctypes.c_float), h, d, _ptr(t, ctypes.c_float),
+                                         _ptr(stats, ctypes.c_double)), "variance_stats")
+    return stats
+
+
+def delta(rule: str, n: int, f: int) -> float:
+    """Delta of the variance condition (Section 3.1, Tradeoffs): the minimum-
+    diameter rule 2 sqrt(2) f / (n - f), Krum sqrt(2 (n - f + (f (n - f - 2) +
+    f^2 (n - f - 1)) / (n - 2f - 2))), Median sqrt(n - f); NaN for other rules
+    or n below the rule's requirement (2f+1, 2f+3, 2f+1)."""
+    import math
+
+    if n < 1 or f < 0:
+        return math.nan
+    if rule == "mda":
+        return 2.0 * math.sqrt(2.0) * f / (n - f) if n >= 2 * f + 1 else math.nan
+    if rule == "krum":
+        if n < 2 * f + 3:
+            return math.nan
+        return math.sqrt(2.0 * ((n - f) + (f * (n - f - 2) + f * f * (n - f - 1)) / (n - 2 * f - 2)))
+    if rule == "median":
+        return math.sqrt(n - f) if n >= 2 * f + 1 else math.nan
+    return math.nan

@@ -30,6 +30,16 @@
 //   R8  iterated Multi-Krum: the selection of R6 stopped after m rounds, then
 //       the mean of the m selected rows (Multi-Krum computed by repeating
 //       Krum, as Section 4.4 describes for Multi-Krum and Bulyan).
+//   R9  attacks (Section 3.2, Main objects; Section 6.5): reversed vectors are
+//       param times an honest vector (row b uses honest row b mod h); random
+//       vectors are param times standard normals drawn by Box-Muller from
+//       Philox4x32-10 words (counter = (c/4 low, c/4 high, b, 0), key = seed;
+//       a word w becomes the uniform ((w >> 9) + 1/2) 2^-23); "little is
+//       enough" is mean - param * std per coordinate with the population
+//       standard deviation; "fall of empires" is -param * mean.
+//   R10 variance condition (Section 3.1, Tradeoffs): sigma^2 = E||g - E g||^2
+//       is estimated without bias over the h honest vectors,
+//       sum_i ||g_i - mean||^2 / (h - 1).
 //   R7  MDA enumerates the subsets of size n-f in lexicographic order and keeps
 //       the first one of strictly smaller diameter (diameter = largest squared
 //       distance inside the subset).
@@ -38,6 +48,7 @@
 // for the rule's requirement in f.
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <cstring>
 #include <utility>
@@ -332,6 +343,99 @@ int oracle_mda(const float* x, int n, int f, int64_t d, float* out, int32_t* sel
   if (second_diam) *second_diam = second;
   if (n_best) *n_best = count_best;
   mean_rows(x, d, best_set, out);
+  return kOk;
+}
+
+// Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC'11): ten rounds; in each,
+// the products M0 * c0 and M1 * c2 (32 x 32 -> 64 bits) give the new words
+// (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1, lo(M0 c0)); the key
+// gains (W0, W1) before every round after the first.
+void oracle_philox4x32_10(const uint32_t* ctr, const uint32_t* key, uint32_t* out) {
+  const uint64_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+  uint32_t c[4] = {ctr[0], ctr[1], ctr[2], ctr[3]};
+  uint32_t k[2] = {key[0], key[1]};
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k[0] += 0x9E3779B9u;
+      k[1] += 0xBB67AE85u;
+    }
+    const uint64_t a = M0 * c[0], b = M1 * c[2];
+    const uint32_t next[4] = {static_cast<uint32_t>(b >> 32) ^ c[1] ^ k[0],
+                              static_cast<uint32_t>(b),
+                              static_cast<uint32_t>(a >> 32) ^ c[3] ^ k[1],
+                              static_cast<uint32_t>(a)};
+    for (int t = 0; t < 4; ++t) c[t] = next[t];
+  }
+  for (int t = 0; t < 4; ++t) out[t] = c[t];
+}
+
+// Byzantine vectors (reading R9). kind: 0 reversed, 1 random, 2 little is
+// enough, 3 fall of empires. honest: h x d (unused for random); byz: nbyz x d.
+int oracle_attack(int kind, const float* honest, int h, int64_t d, double param, uint64_t seed,
+                  float* byz, int nbyz) {
+  if (kind < 0 || kind > 3 || d < 0 || nbyz < 0 || (d > 0 && nbyz > 0 && !byz)) return kInval;
+  if (kind != 1 && (h < 1 || (d > 0 && !honest))) return kInval;
+  const double two_pi = 6.283185307179586476925286766559;
+  for (int b = 0; b < nbyz; ++b) {
+    float* row = byz + static_cast<int64_t>(b) * d;
+    if (kind == 0) {
+      for (int64_t c = 0; c < d; ++c) row[c] = static_cast<float>(param * at(honest, d, b % h, c));
+    } else if (kind == 1) {
+      for (int64_t q = 0; 4 * q < d; ++q) {
+        const uint32_t ctr[4] = {static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32),
+                                 static_cast<uint32_t>(b), 0u};
+        const uint32_t key[2] = {static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32)};
+        uint32_t w[4];
+        oracle_philox4x32_10(ctr, key, w);
+        double z[4];
+        for (int pair = 0; pair < 2; ++pair) {
+          const double u1 = (static_cast<double>(w[2 * pair] >> 9) + 0.5) / 8388608.0;
+          const double u2 = (static_cast<double>(w[2 * pair + 1] >> 9) + 0.5) / 8388608.0;
+          const double r = std::sqrt(-2.0 * std::log(u1));
+          z[2 * pair] = r * std::cos(two_pi * u2);
+          z[2 * pair + 1] = r * std::sin(two_pi * u2);
+        }
+        for (int e = 0; e < 4 && 4 * q + e < d; ++e) row[4 * q + e] = static_cast<float>(param * z[e]);
+      }
+    } else {
+      for (int64_t c = 0; c < d; ++c) {
+        double sum = 0.0;
+        for (int i = 0; i < h; ++i) sum += at(honest, d, i, c);
+        const double mean = sum / h;
+        if (kind == 3) {
+          row[c] = static_cast<float>(-param * mean);
+        } else {
+          double ss = 0.0;
+          for (int i = 0; i < h; ++i) {
+            const double t = at(honest, d, i, c) - mean;
+            ss += t * t;
+          }
+          row[c] = static_cast<float>(mean - param * std::sqrt(ss / h));
+        }
+      }
+    }
+  }
+  return kOk;
+}
+
+// Variance condition (reading R10): stats[0] = sum_i ||g_i - mean||^2 / (h-1)
+// over the h rows of g, stats[1] = ||grad||^2.
+int oracle_variance_stats(const float* g, int h, int64_t d, const float* grad, double* stats) {
+  if (h < 2 || d < 0 || !stats || (d > 0 && (!g || !grad))) return kInval;
+  double dev = 0.0;
+  for (int64_t c = 0; c < d; ++c) {
+    double sum = 0.0;
+    for (int i = 0; i < h; ++i) sum += at(g, d, i, c);
+    const double mean = sum / h;
+    for (int i = 0; i < h; ++i) {
+      const double t = at(g, d, i, c) - mean;
+      dev += t * t;
+    }
+  }
+  double norm = 0.0;
+  for (int64_t c = 0; c < d; ++c) norm += static_cast<double>(grad[c]) * static_cast<double>(grad[c]);
+  stats[0] = dev / (h - 1);
+  stats[1] = norm;
   return kOk;
 }
 

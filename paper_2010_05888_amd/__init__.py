@@ -24,6 +24,7 @@ __all__ = [
     "average",
     "multikrum_median", "gar", "workspace_bytes", "release", "set_direct_max_n",
     "distance_engine", "gram_reference", "set_kernel_timing", "kernel_timing", "RULES",
+    "ATTACKS", "attack", "variance_stats", "delta", "variance_condition",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -32,6 +33,7 @@ _LIB_PATH = os.path.join(_HERE, "libgarfield.so")
 OK, EINVAL, EREQ, ETOOBIG, ENOMEM, EHIP = range(6)
 RULE_IDS = {"dist": 0, "krum": 1, "multikrum": 2, "median": 3, "bulyan": 4, "mda": 5, "average": 6,
             "multikrum_iterated": 7}
+ATTACKS = {"reverse": 0, "random": 1, "little": 2, "empire": 3}
 NMAX = 64
 
 
@@ -90,6 +92,13 @@ def load():
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = st
+    lib.garfield_attack.argtypes = [i32, vp, i32, i64, ctypes.c_double, ctypes.c_uint64, vp, i32,
+                                    vp]
+    lib.garfield_attack.restype = st
+    lib.garfield_variance_stats.argtypes = [vp, i32, i64, vp, vp, vp]
+    lib.garfield_variance_stats.restype = st
+    lib.garfield_delta.argtypes = [i32, i32, i32]
+    lib.garfield_delta.restype = ctypes.c_double
     lib.garfield_workspace_bytes.argtypes = [i32, i32, i32, i64, i32]
     lib.garfield_workspace_bytes.restype = ctypes.c_size_t
     lib.garfield_release.argtypes = []
@@ -257,6 +266,73 @@ def gar(name: str, x: torch.Tensor, f: int, **kw):
     except KeyError:
         raise ValueError(f"unknown rule {name!r}; known: {sorted(RULES)}") from None
     return rule(x, f, **kw)
+
+
+def attack(kind: str, honest: torch.Tensor | None, nbyz: int, param: float, seed: int = 0,
+           d: int | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
+    """nbyz Byzantine vectors (nbyz x d) from the honest rows (h x d): "reverse"
+    (param * honest[b % h]), "random" (param * N(0, 1); honest may be None, then
+    d or out gives the dimension), "little" (mean - param * std per coordinate)
+    or "empire" (-param * mean). `out` (nbyz x d, contiguous fp32 on the same
+    device) may be a view into a rule's input, e.g. its last rows."""
+    if kind not in ATTACKS:
+        raise ValueError(f"unknown attack {kind!r}; known: {sorted(ATTACKS)}")
+    if honest is not None:
+        honest = _input(honest)
+        h, dd = honest.shape
+        dev = honest.device
+    else:
+        if kind != "random":
+            raise ValueError(f"attack {kind!r} needs the honest rows")
+        h = 0
+        dd = d if d is not None else (out.shape[1] if out is not None else None)
+        if dd is None:
+            raise ValueError("give d or out for a random attack without honest rows")
+        dev = out.device if out is not None else torch.device("cuda", torch.cuda.current_device())
+    if out is None:
+        out = torch.empty((nbyz, dd), dtype=torch.float32, device=dev)
+    elif (out.dtype != torch.float32 or out.device != dev or tuple(out.shape) != (nbyz, dd)
+          or not out.is_contiguous()):
+        raise ValueError("out must be a contiguous nbyz x d fp32 tensor on the input's device")
+    s = _stream(out) if honest is None else _stream(honest)
+    _check(load().garfield_attack(ATTACKS[kind], _ptr(honest), h, dd, float(param),
+                                  seed & 0xFFFFFFFFFFFFFFFF, _ptr(out), nbyz, s),
+           "garfield_attack")
+    return out
+
+
+def variance_stats(g: torch.Tensor, grad: torch.Tensor) -> torch.Tensor:
+    """Device fp64 [2]: the unbiased estimate of E||g - Eg||^2 over the rows of
+    g (from their pairwise distances) and ||grad||^2."""
+    g = _input(g)
+    h, d = g.shape
+    grad = _input(grad.reshape(1, -1)).reshape(-1)
+    if grad.numel() != d or grad.device != g.device:
+        raise ValueError("grad must hold d values on g's device")
+    stats = torch.empty(2, dtype=torch.float64, device=g.device)
+    _check(load().garfield_variance_stats(_ptr(g), h, d, _ptr(grad), _ptr(stats), _stream(g)),
+           "garfield_variance_stats")
+    return stats
+
+
+def delta(rule: str, n: int, f: int) -> float:
+    """Delta of the variance condition (Section 3.1) for "mda", "krum" or
+    "median"; NaN for other rules or n below the rule's requirement."""
+    return load().garfield_delta(RULE_IDS[rule], n, f)
+
+
+def variance_condition(g: torch.Tensor, grad: torch.Tensor, n: int, f: int) -> dict:
+    """For each rule with a Delta: whether kappa * Delta * sigma <= ||grad||
+    can hold for some kappa > 1, i.e. ||grad|| / (Delta * sigma) > 1, with
+    sigma estimated from the honest gradient estimates g."""
+    var, sq = (float(v) for v in variance_stats(g, grad).cpu())
+    sigma, norm = var ** 0.5, sq ** 0.5
+    res = {"sigma": sigma, "grad_norm": norm}
+    for rule in ("mda", "krum", "median"):
+        dl = delta(rule, n, f)
+        ratio = norm / (dl * sigma) if dl == dl and dl * sigma > 0 else float("inf")
+        res[rule] = {"delta": dl, "ratio": ratio, "holds": ratio > 1.0 if dl == dl else None}
+    return res
 
 
 class Segmented:

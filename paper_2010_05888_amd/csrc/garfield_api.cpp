@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <map>
 #include <mutex>
 #include <new>
@@ -245,6 +246,63 @@ garfield_status garfield_average(const float* x, int n, int64_t d, float* out, v
   if (st != GARFIELD_OK) return st;
   if (d > 0 && !out) return GARFIELD_EINVAL;
   return to_status(enqueue_mean_rows(x, n, d, nullptr, n, out, static_cast<hipStream_t>(stream)));
+}
+
+garfield_status garfield_attack(int kind, const float* honest, int h, int64_t d, double param,
+                                uint64_t seed, float* byz, int nbyz, void* stream) {
+  if (kind < GARFIELD_ATTACK_REVERSE || kind > GARFIELD_ATTACK_EMPIRE) return GARFIELD_EINVAL;
+  if (d < 0 || nbyz < 0 || !std::isfinite(param)) return GARFIELD_EINVAL;
+  if (nbyz > GARFIELD_NMAX) return GARFIELD_ETOOBIG;
+  const bool uses_honest = kind != GARFIELD_ATTACK_RANDOM;
+  if (uses_honest) {
+    if (h < 1) return GARFIELD_EINVAL;
+    if (h > GARFIELD_NMAX) return GARFIELD_ETOOBIG;
+  }
+  if (d > 0 && nbyz > 0) {
+    if (!byz || reinterpret_cast<uintptr_t>(byz) % sizeof(float) != 0) return GARFIELD_EINVAL;
+    if (uses_honest && (!honest || reinterpret_cast<uintptr_t>(honest) % sizeof(float) != 0))
+      return GARFIELD_EINVAL;
+  }
+  return to_status(enqueue_attack(kind, uses_honest ? honest : nullptr, h, d, param, seed, byz,
+                                  nbyz, static_cast<hipStream_t>(stream)));
+}
+
+garfield_status garfield_variance_stats(const float* g, int h, int64_t d, const float* grad,
+                                        double* stats, void* stream) {
+  garfield_status st = check_common(g, h, 0, d);
+  if (st != GARFIELD_OK) return st;
+  if (h < 2 || !stats) return GARFIELD_EINVAL;
+  if (d > 0 && (!grad || reinterpret_cast<uintptr_t>(grad) % sizeof(float) != 0))
+    return GARFIELD_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t parts = d > 0 ? sqnorm_parts(d, grad) : 0;
+  DistSums ds;
+  void* scratch = nullptr;
+  st = run_distances(g, h, d, static_cast<size_t>(parts) * sizeof(double), &ds, &scratch, s);
+  if (st != GARFIELD_OK) return st;
+  return to_status(
+      enqueue_variance_stats(ds, h, grad, d, static_cast<double*>(scratch), stats, s));
+}
+
+double garfield_delta(int rule, int n, int f) {
+  const double nan = std::nan("");
+  if (n < 1 || f < 0) return nan;
+  const double nf = static_cast<double>(n - f);
+  switch (rule) {
+    case GARFIELD_RULE_MDA:
+      if (n < 2 * f + 1) return nan;
+      return 2.0 * std::sqrt(2.0) * f / nf;
+    case GARFIELD_RULE_KRUM:
+      if (n < 2 * f + 3) return nan;
+      return std::sqrt(2.0 * (nf + (static_cast<double>(f) * (n - f - 2) +
+                                    static_cast<double>(f) * f * (n - f - 1)) /
+                                       static_cast<double>(n - 2 * f - 2)));
+    case GARFIELD_RULE_MEDIAN:
+      if (n < 2 * f + 1) return nan;
+      return std::sqrt(nf);
+    default:
+      return nan;
+  }
 }
 
 garfield_status garfield_seg_create(int rule, int n, int f, int m, garfield_segmented** out) {

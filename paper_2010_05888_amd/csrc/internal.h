@@ -66,6 +66,17 @@ hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStr
 hipError_t enqueue_krum_rounds(const DistSums& ds, int f, int rounds, int32_t* sel,
                                hipStream_t s);
 
+// Byzantine rows from the honest ones (byzantine.hip); kinds as garfield_attack.
+enum AttackKind { kAttackReverse = 0, kAttackRandom = 1, kAttackLittle = 2, kAttackEmpire = 3 };
+hipError_t enqueue_attack(int kind, const float* honest, int h, int64_t d, double param,
+                          uint64_t seed, float* byz, int nbyz, hipStream_t s);
+// Variance condition: stats[0] = sum_{i<j} D[i][j] / (h (h-1)) over the h rows
+// the distance sums `ds` came from, stats[1] = ||grad||^2. Scratch:
+// sqnorm_parts(d, grad) fp64 partials.
+int64_t sqnorm_parts(int64_t d, const float* grad);
+hipError_t enqueue_variance_stats(const DistSums& ds, int h, const float* grad, int64_t d,
+                                  double* partial, double* stats, hipStream_t s);
+
 // MDA subset search. Scratch: mda_blocks(n, f) x 16 bytes.
 int64_t binomial(int a, int b);  // exact, or -1 if above 2^62
 int mda_blocks(int n, int f);

@@ -88,6 +88,37 @@ def test_strerror_and_version(lib):
     assert lib.garfield_version().startswith(b"garfield")
 
 
+def test_attack_and_variance_validation(lib):
+    A = gf.ATTACKS
+    nan = float("nan")
+    assert lib.garfield_attack(4, FAKE, 3, 10, 1.0, 0, FAKE, 2, NULL) == gf.EINVAL
+    assert lib.garfield_attack(-1, FAKE, 3, 10, 1.0, 0, FAKE, 2, NULL) == gf.EINVAL
+    assert lib.garfield_attack(A["little"], FAKE, 3, 10, 1.0, 0, FAKE, 65, NULL) == gf.ETOOBIG
+    assert lib.garfield_attack(A["little"], FAKE, 65, 10, 1.0, 0, FAKE, 2, NULL) == gf.ETOOBIG
+    assert lib.garfield_attack(A["little"], FAKE, 0, 10, 1.0, 0, FAKE, 2, NULL) == gf.EINVAL
+    assert lib.garfield_attack(A["reverse"], NULL, 3, 10, 1.0, 0, FAKE, 2, NULL) == gf.EINVAL
+    assert lib.garfield_attack(A["empire"], FAKE, 3, 10, nan, 0, FAKE, 2, NULL) == gf.EINVAL
+    assert lib.garfield_attack(A["random"], NULL, 0, 10, 1.0, 0, NULL, 2, NULL) == gf.EINVAL
+    assert lib.garfield_attack(A["random"], NULL, 0, -1, 1.0, 0, FAKE, 2, NULL) == gf.EINVAL
+    assert lib.garfield_attack(A["little"], FAKE, 3, 10, 1.0, 0, ctypes.c_void_p(0x1002), 2,
+                               NULL) == gf.EINVAL
+    # nothing to write: accepted without touching the device
+    assert lib.garfield_attack(A["little"], FAKE, 3, 10, 1.0, 0, FAKE, 0, NULL) == gf.OK
+    assert lib.garfield_attack(A["random"], NULL, 0, 0, 1.0, 0, NULL, 4, NULL) == gf.OK
+    # variance statistics: h >= 2, grad and stats required
+    assert lib.garfield_variance_stats(FAKE, 1, 10, FAKE, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_variance_stats(FAKE, 3, 10, NULL, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_variance_stats(FAKE, 3, 10, FAKE, NULL, NULL) == gf.EINVAL
+    assert lib.garfield_variance_stats(FAKE, 65, 10, FAKE, FAKE, NULL) == gf.ETOOBIG
+    # Delta (host closed forms, Section 3.1): n = 11, f = 2
+    R = gf.RULE_IDS
+    assert lib.garfield_delta(R["median"], 11, 2) == 3.0
+    assert lib.garfield_delta(R["krum"], 11, 2) == pytest.approx(36.4 ** 0.5, rel=1e-15)
+    assert lib.garfield_delta(R["mda"], 11, 2) == pytest.approx(4 * 2 ** 0.5 / 9, rel=1e-15)
+    assert lib.garfield_delta(R["bulyan"], 11, 2) != lib.garfield_delta(R["bulyan"], 11, 2)  # NaN
+    assert lib.garfield_delta(R["krum"], 6, 2) != lib.garfield_delta(R["krum"], 6, 2)
+
+
 def test_workspace_bytes(lib):
     assert gf.workspace_bytes("median", 64, 15, 10 ** 8) == 0
     assert gf.workspace_bytes("krum", 0, 0, 10) == 0
