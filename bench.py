@@ -53,6 +53,9 @@ def _parse():
                          "segments held as separate tensors (like per-layer gradients); a "
                          "step accumulates their distances, selects once and aggregates "
                          "each segment (workloads 2-4 and 6)")
+    ap.add_argument("--table", action="store_true",
+                    help="with --segments: feed the segments as a segment table (vectors stored "
+                         "apart; one launch per 96 segments) instead of one call per segment")
     ap.add_argument("--byzantine", action="store_true",
                     help="the device attack generators and the variance statistics instead: one "
                          "JSON line per case, at workload 3's and 2's shapes")
@@ -133,6 +136,7 @@ class Step:
 def algorithmic(kernel, w):
     """(bound, algorithmic bytes or flops per launch, unit) of a kernel of workload w."""
     n, f, d = w.n, w.f, w.d
+    kernel = kernel[:-4] if kernel.endswith("_seg") else kernel  # segment-table forms
     if kernel in ("dist_direct", "dist_gram"):
         return "hbm", 4.0 * n * d
     if kernel == "mean_rows":
@@ -250,7 +254,7 @@ def bench_workload(key, args):
     copies = [x] if x.numel() * 4 >= INPUT_RING_BYTES else [x, x.clone()]
     torch.cuda.synchronize()
     if args.segments > 1:
-        steps = [SegmentedStep(gf, w, xi, args.segments) for xi in copies]
+        steps = [SegmentedStep(gf, w, xi, args.segments, args.table) for xi in copies]
         del copies  # the segments are copies of their own
         copies = [None] * len(steps)
         torch.cuda.synchronize()
@@ -300,7 +304,9 @@ def bench_workload(key, args):
     dominant = max(kt, key=lambda k: kt[k][1])
     bound, per_launch = algorithmic(dominant, w)
     if per_launch and args.segments > 1:
-        per_launch /= args.segments  # every launch covers one of the (equal) segments
+        # per-segment calls: one launch per (equal) segment; a segment table: one
+        # launch per 96 segments
+        per_launch /= -(-args.segments // 96) if args.table else args.segments
     avg_ms = kt[dominant][1] / kt[dominant][0]
     roofline = {"kernel": dominant, "bound": bound, "achieved": None, "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": None, "traffic": measured_traffic(dominant, key),
@@ -331,7 +337,8 @@ def bench_workload(key, args):
         "dtype": "f32",
         "data": "synthetic",
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
-        "config": {"workload": w.name + (f" [segmented: {args.segments} segments]"
+        "config": {"workload": w.name + (f" [segmented: {args.segments} segments"
+                                          f"{', segment table' if args.table else ''}]"
                                           if args.segments > 1 else ""),
                    "rules": list(w.rules), "n": w.n, "f": w.f, "d": w.d,
                    "m": w.m, "seed": w.seed, "byzantine_rows": inp.byzantine,
@@ -358,7 +365,7 @@ class SegmentedStep:
     RULE = {("multikrum",): "multikrum", ("multikrum_iterated",): "multikrum_iterated",
             ("bulyan",): "bulyan", ("mda",): "mda"}
 
-    def __init__(self, gf, w, x, k):
+    def __init__(self, gf, w, x, k, table=False):
         import torch
 
         if w.rules not in self.RULE:
@@ -374,8 +381,16 @@ class SegmentedStep:
         self.s = ctypes.c_void_p(torch.cuda.current_stream(x.device).cuda_stream)
         p = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
         self.args = [(p(s), s.shape[1], p(o)) for s, o in zip(self.segs, self.outs)]
+        self.table = gf.SegmentTable([[s[i] for s in self.segs] for i in range(n)]) if table else None
 
     def __call__(self):
+        if self.table is not None:
+            t, sess = self.table, self.session
+            sess.reset()
+            sess.accumulate_table(t)
+            sess.select()
+            sess.aggregate_table(t, outs=self.outs)
+            return
         lib, h, s = self.lib, self.session._h, self.s
         codes = [lib.garfield_seg_reset(h, s)]
         for px, d, _ in self.args:

@@ -257,6 +257,31 @@ garfield_status garfield_seg_aggregate(garfield_segmented* seg, const float* x, 
 garfield_status garfield_seg_destroy(garfield_segmented* seg);
 
 /*
+ * Segment tables: the same session fed with vectors stored apart, K segments
+ * at a time. ptrs (DEVICE, K*n pointers): ptrs[s*n + i] points to segment s of
+ * vector i, dims[s] fp32 values (HOST array of K lengths, each >= 0; every
+ * pointer 4-byte aligned). Typical uses: each worker's per-layer gradients
+ * (K = number of layers), or n whole vectors in separate buffers (K = 1, the
+ * row-pointer form of every rule: create, accumulate_table, select,
+ * aggregate_table).
+ *   garfield_seg_accumulate_table(seg, ptrs, dims, K, stream)   adds the
+ *       distances of all K segments; one launch per 96 segments, whatever
+ *       their sizes, instead of one distance step per segment.
+ *   garfield_seg_aggregate_table(seg, ptrs, dims, K, outs, stream)   aggregates
+ *       every segment with the session's selection; outs (HOST array of K
+ *       DEVICE pointers, each to dims[s] fp32 values, 4-byte aligned).
+ * Requires n <= 20 (the direct distance engine's limit; GARFIELD_ETOOBIG
+ * otherwise). Results equal those of garfield_seg_accumulate /
+ * garfield_seg_aggregate on the same segments held as n x d matrices, except
+ * that the distances come from the direct engine for every n <= 20.
+ */
+garfield_status garfield_seg_accumulate_table(garfield_segmented* seg, const float* const* ptrs,
+                                              const int64_t* dims, int K, void* stream);
+garfield_status garfield_seg_aggregate_table(garfield_segmented* seg, const float* const* ptrs,
+                                             const int64_t* dims, int K, float* const* outs,
+                                             void* stream);
+
+/*
  * Bytes of workspace one call of `rule` with these sizes uses (0 if the
  * arguments are invalid). Informational: the library allocates it itself.
  */

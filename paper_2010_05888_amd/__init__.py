@@ -24,7 +24,8 @@ __all__ = [
     "average",
     "multikrum_median", "gar", "workspace_bytes", "release", "set_direct_max_n",
     "distance_engine", "gram_reference", "set_kernel_timing", "kernel_timing", "RULES",
-    "ATTACKS", "attack", "variance_stats", "delta", "variance_condition",
+    "ATTACKS", "attack", "variance_stats", "delta", "variance_condition", "Segmented",
+    "SegmentTable",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -87,6 +88,8 @@ def load():
         "garfield_seg_select": [vp, vp, vp],
         "garfield_seg_aggregate": [vp, vp, i64, vp, vp],
         "garfield_seg_destroy": [vp],
+        "garfield_seg_accumulate_table": [vp, vp, vp, i32, vp],
+        "garfield_seg_aggregate_table": [vp, vp, vp, i32, vp, vp],
     }
     for name, args in seg_sig.items():
         fn = getattr(lib, name)
@@ -335,6 +338,45 @@ def variance_condition(g: torch.Tensor, grad: torch.Tensor, n: int, f: int) -> d
     return res
 
 
+class SegmentTable:
+    """n vectors held as K segments stored apart: vectors[i][s] is segment s of
+    vector i (a contiguous fp32 tensor on the GPU; every vector's segment s has
+    the same number of values). The device table of the K*n pointers is built
+    once here; the tensors must stay alive and in place while the table is
+    used. `SegmentTable.rows(list of n tensors)` is the K = 1 form: n whole
+    vectors in separate buffers."""
+
+    def __init__(self, vectors):
+        n = len(vectors)
+        if n < 1:
+            raise ValueError("no vectors")
+        K = len(vectors[0])
+        dev = None
+        for row in vectors:
+            if len(row) != K:
+                raise ValueError("every vector needs the same number of segments")
+            for t in row:
+                if (not isinstance(t, torch.Tensor) or t.device.type != "cuda"
+                        or t.dtype != torch.float32 or not t.is_contiguous()):
+                    raise ValueError("segments must be contiguous float32 GPU tensors")
+                dev = t.device if dev is None else dev
+                if t.device != dev:
+                    raise ValueError("all segments must be on one device")
+        self.dims = [int(vectors[0][s].numel()) for s in range(K)]
+        for row in vectors:
+            if [int(t.numel()) for t in row] != self.dims:
+                raise ValueError("segment s must have the same length in every vector")
+        self.n, self.K, self.device = n, K, dev
+        self._keep = [list(row) for row in vectors]
+        flat = [vectors[i][s].data_ptr() for s in range(K) for i in range(n)]
+        self.ptrs = torch.tensor(flat, dtype=torch.int64).to(dev)
+        self._dims = (ctypes.c_int64 * max(K, 1))(*self.dims)
+
+    @classmethod
+    def rows(cls, vectors):
+        return cls([[v.reshape(-1) if v.is_contiguous() else v] for v in vectors])
+
+
 class Segmented:
     """Segmented aggregation (per-layer, Section 4.2): accumulate the distances
     of segments of the n vectors (each an n x d_s tensor: the same coordinates
@@ -392,6 +434,34 @@ class Segmented:
         _check(load().garfield_seg_aggregate(self._h, _ptr(x), x.shape[1], _ptr(out), _stream(x)),
                "garfield_seg_aggregate")
         return out
+
+    def accumulate_table(self, table: "SegmentTable"):
+        """Add the distances of every segment of the table (one launch per 96
+        segments)."""
+        if table.n != self.n:
+            raise ValueError(f"table has {table.n} vectors, the session {self.n}")
+        s = ctypes.c_void_p(torch.cuda.current_stream(table.device).cuda_stream)
+        _check(load().garfield_seg_accumulate_table(self._h, _ptr(table.ptrs), table._dims,
+                                                    table.K, s),
+               "garfield_seg_accumulate_table")
+
+    def aggregate_table(self, table: "SegmentTable", outs=None):
+        """Aggregate every segment of the table with the session's selection;
+        returns the K outputs (or fills `outs`, K contiguous fp32 tensors)."""
+        if table.n != self.n:
+            raise ValueError(f"table has {table.n} vectors, the session {self.n}")
+        if outs is None:
+            outs = [torch.empty(dk, dtype=torch.float32, device=table.device) for dk in table.dims]
+        elif len(outs) != table.K or any(
+                o.numel() != dk or o.dtype != torch.float32 or not o.is_contiguous()
+                or o.device != table.device for o, dk in zip(outs, table.dims)):
+            raise ValueError("outs must be K contiguous fp32 tensors of the segments' lengths")
+        optrs = (ctypes.c_void_p * max(table.K, 1))(*[o.data_ptr() for o in outs])
+        s = ctypes.c_void_p(torch.cuda.current_stream(table.device).cuda_stream)
+        _check(load().garfield_seg_aggregate_table(self._h, _ptr(table.ptrs), table._dims,
+                                                   table.K, optrs, s),
+               "garfield_seg_aggregate_table")
+        return outs
 
     def close(self):
         if self._h:

@@ -19,8 +19,8 @@ INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libgarfield.so")
 
-SOURCES = ["dist.hip", "select.hip", "aggregate.hip", "byzantine.hip", "garfield_api.cpp",
-           "timing.cpp"]
+SOURCES = ["dist.hip", "select.hip", "aggregate.hip", "byzantine.hip", "segtable.hip",
+           "garfield_api.cpp", "timing.cpp"]
 
 ARCH = "gfx950"
 FLAGS = [

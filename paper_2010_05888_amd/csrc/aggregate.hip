@@ -16,74 +16,26 @@
 // Row indices come from device memory (the selection kernels write them), so
 // no host round trip separates selection from aggregation.
 
+#include "aggregate_body.h"
 #include "device_common.h"
 #include "internal.h"
 #include "timing.h"
 
 namespace garfield {
 
-#include "networks.inc"
-
 namespace {
 
-__device__ __forceinline__ int64_t row_of(const int32_t* __restrict__ rows, int t, int n) {
-  if (!rows) return t;
-  const int r = rows[t];
-  return static_cast<int64_t>(r < 0 ? 0 : (r >= n ? n - 1 : r));
-}
-
-// ---------------------------------------------------------------------------
-// fp64 sum of the k rows at coordinates c .. c+W-1, eight loads in flight at a
-// time; FULL: all W coordinates exist (else the guarded tail loads).
-template <int W, bool FULL>
-__device__ __forceinline__ void sum_rows_at(const float* __restrict__ x, int n, int64_t d,
-                                            const int32_t* __restrict__ rows, int k, int64_t c,
-                                            double* acc) {
-  int t = 0;
-  for (; t + 8 <= k; t += 8) {
-    float v[8][W];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const float* p = x + row_of(rows, t + u, n) * d + c;
-      if constexpr (FULL) load_w<W>(p, v[u]); else load_w_tail<W>(p, d - c, v[u]);
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-#pragma unroll
-      for (int e = 0; e < W; ++e) acc[e] += static_cast<double>(v[u][e]);
-  }
-  for (; t < k; ++t) {
-    float v[W];
-    const float* p = x + row_of(rows, t, n) * d + c;
-    if constexpr (FULL) load_w<W>(p, v); else load_w_tail<W>(p, d - c, v);
-#pragma unroll
-    for (int e = 0; e < W; ++e) acc[e] += static_cast<double>(v[e]);
-  }
-}
-
+// The kernels over one row-major n x d matrix; the per-coordinate work is in
+// aggregate_body.h (shared with the segment-table kernels).
 template <int W>
 __global__ __launch_bounds__(kBlock) void k_mean_rows(const float* __restrict__ x, int n,
                                                       int64_t d, const int32_t* __restrict__ rows,
                                                       int k, float* __restrict__ out) {
+  const MatrixRows src{x, d};
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * W;
-  const double count = static_cast<double>(k);
   for (int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W; c < d;
-       c += stride) {
-    double acc[W];
-#pragma unroll
-    for (int e = 0; e < W; ++e) acc[e] = 0.0;
-    const bool full = c + W <= d;
-    if (full) sum_rows_at<W, true>(x, n, d, rows, k, c, acc);
-    else sum_rows_at<W, false>(x, n, d, rows, k, c, acc);
-    float o[W];
-#pragma unroll
-    for (int e = 0; e < W; ++e) o[e] = static_cast<float>(acc[e] / count);
-    if (full) {
-      store_w<W>(out + c, o);
-    } else {
-      for (int e = 0; e < W && c + e < d; ++e) out[c + e] = o[e];
-    }
-  }
+       c += stride)
+    mean_at<W>(src, n, d, rows, k, c, out);
 }
 
 // ---------------------------------------------------------------------------
@@ -97,114 +49,25 @@ template <int K, int W>
 __global__ __launch_bounds__(kBlock) void k_median(const float* __restrict__ x, int n, int64_t d,
                                                    const int32_t* __restrict__ rows,
                                                    float* __restrict__ out) {
-  using Net = MedianNet<K>;
+  const MatrixRows src{x, d};
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * W;
   for (int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W; c < d;
-       c += stride) {
-    float v[K][W];
-    const bool full = c + W <= d;
-    if (full) {  // all K loads back to back, then the network
-#pragma unroll
-      for (int t = 0; t < K; ++t) load_w<W>(x + row_of(rows, t, n) * d + c, v[t]);
-    } else {
-#pragma unroll
-      for (int t = 0; t < K; ++t) load_w_tail<W>(x + row_of(rows, t, n) * d + c, d - c, v[t]);
-    }
-    float o[W];
-#pragma unroll
-    for (int e = 0; e < W; ++e) {
-      float a[K];
-#pragma unroll
-      for (int t = 0; t < K; ++t) a[t] = v[t][e];
-      Net::run(a);
-      if constexpr (K % 2 == 1) {
-        o[e] = a[Net::LO];
-      } else {  // mean of the two middle values, exact in fp64, rounded once
-        o[e] = static_cast<float>((static_cast<double>(a[Net::LO]) +
-                                   static_cast<double>(a[Net::HI])) * 0.5);
-      }
-    }
-    if (full) {
-      store_w<W>(out + c, o);
-    } else {
-      for (int e = 0; e < W && c + e < d; ++e) out[c + e] = o[e];
-    }
-  }
+       c += stride)
+    median_at<K, W>(src, n, d, rows, c, out);
 }
 
-// ---------------------------------------------------------------------------
-// Bulyan aggregation for theta = T selected rows, beta = T - 2f closest.
-//
-// With s[0..T-1] sorted: odd T has the median s[c], c = (T-1)/2, always kept,
-// and K = beta-1 more to take; even T has med = (s[c-1]+s[c])/2, c = T/2, and
-// K = beta to take. Left candidates L_a = s[c-a] (a = 1, 2, ...) and right
-// candidates R_b (s[c+b] for odd T, s[c-1+b] for even T) are each ordered by
-// increasing key, so the K taken are the first K of their merge: L_a is taken
-// iff key(L_a) < key(R_{K+1-a}) (a missing R counts as +inf). The number of
-// left values taken is the count of such a.
+// Bulyan aggregation for theta = T selected rows (bulyan_at); the sorted
+// column of each thread goes through LDS.
 template <int T, int W>
 __global__ __launch_bounds__(kBlock) void k_bulyan_agg(const float* __restrict__ x, int n,
                                                        int64_t d, const int32_t* __restrict__ sel,
                                                        int beta, float* __restrict__ out) {
-  using Net = SortNet<T>;
   __shared__ float sorted[T * kBlock];
-  float* col = sorted + threadIdx.x;  // column of this thread: col[r * kBlock]
-  constexpr bool kOdd = (T % 2) == 1;
-  constexpr int c = kOdd ? (T - 1) / 2 : T / 2;
-  constexpr int n_left = c;                          // L_a exists for a <= n_left
-  constexpr int n_right = kOdd ? T - 1 - c : T - c;  // R_b exists for b <= n_right
-  const int K = kOdd ? beta - 1 : beta;
+  const MatrixRows src{x, d};
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * W;
   for (int64_t cc = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W; cc < d;
-       cc += stride) {
-    float v[T][W];
-    const bool full = cc + W <= d;
-    if (full) {
-#pragma unroll
-      for (int t = 0; t < T; ++t) load_w<W>(x + row_of(sel, t, n) * d + cc, v[t]);
-    } else {
-#pragma unroll
-      for (int t = 0; t < T; ++t) load_w_tail<W>(x + row_of(sel, t, n) * d + cc, d - cc, v[t]);
-    }
-    float o[W];
-#pragma unroll
-    for (int e = 0; e < W; ++e) {
-      float a[T];
-#pragma unroll
-      for (int t = 0; t < T; ++t) a[t] = v[t][e];
-      Net::run(a);
-#pragma unroll
-      for (int r = 0; r < T; ++r) col[r * kBlock] = a[Net::reg(r)];
-      const double med = kOdd ? static_cast<double>(col[c * kBlock])
-                              : (static_cast<double>(col[(c - 1) * kBlock]) +
-                                 static_cast<double>(col[c * kBlock])) * 0.5;
-      int a_taken = 0;
-      for (int i = 1; i <= K; ++i) {
-        if (i > n_left) break;
-        const int b = K + 1 - i;
-        bool take = true;
-        if (b <= n_right) {
-          const float lv = col[(c - i) * kBlock];
-          const float rv = col[(kOdd ? c + b : c - 1 + b) * kBlock];
-          const double dl = med - static_cast<double>(lv);
-          const double dr = static_cast<double>(rv) - med;
-          take = (dl < dr) || (dl == dr && lv < rv);
-        }
-        if (!take) break;
-        a_taken = i;
-      }
-      const int lo = c - a_taken;
-      const int hi = lo + beta - 1;  // inclusive
-      double sum = 0.0;
-      for (int r = lo; r <= hi; ++r) sum += static_cast<double>(col[r * kBlock]);
-      o[e] = static_cast<float>(sum / static_cast<double>(beta));
-    }
-    if (full) {
-      store_w<W>(out + cc, o);
-    } else {
-      for (int e = 0; e < W && cc + e < d; ++e) out[cc + e] = o[e];
-    }
-  }
+       cc += stride)
+    bulyan_at<T, W>(src, n, d, sel, beta, cc, sorted + threadIdx.x, out);
 }
 
 // ---------------------------------------------------------------------------

@@ -23,6 +23,7 @@
 //    an exact 0 between them.
 
 #include "device_common.h"
+#include "direct_body.h"
 #include "dist_layout.h"
 #include "internal.h"
 #include "timing.h"
@@ -32,43 +33,8 @@ namespace garfield {
 namespace {
 
 // ---------------------------------------------------------------------------
-// Block-wide reduction of P per-thread fp32 accumulators into P fp64 sums,
-// through LDS in chunks of 32 columns (33-float row stride: conflict-free).
-// Every sum is formed in the same order (eight fixed groups of 32 threads,
-// each summed in ascending thread order), whatever the pair.
-template <int P>
-__device__ __forceinline__ void block_reduce_pairs(const float* acc, double* __restrict__ out,
-                                                   int64_t stride) {
-  __shared__ float cols[kBlock * 33];
-  __shared__ double part[8][32];
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int base = 0; base < P; base += 32) {
-#pragma unroll
-    for (int q = 0; q < 32; ++q)
-      if (base + q < P) cols[t * 33 + q] = acc[base + q];
-    __syncthreads();
-    const int q = t & 31, r = t >> 5;
-    double s = 0.0;
-    if (base + q < P) {
-#pragma unroll 8
-      for (int u = 0; u < 32; ++u) s += static_cast<double>(cols[(r * 32 + u) * 33 + q]);
-    }
-    part[r][q] = s;
-    __syncthreads();
-    if (t < 32 && base + t < P) {
-      double a = part[0][t];
-#pragma unroll
-      for (int g = 1; g < 8; ++g) a += part[g][t];
-      out[(base + t) * stride] = a;
-    }
-    __syncthreads();
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Direct engine. Tile = `chunk` coordinates (a multiple of kBlock * W); lane t
-// takes W consecutive coordinates every kBlock * W.
+// Direct engine (direct_body.h). Tile = `chunk` coordinates (a multiple of
+// kBlock * W); lane t takes W consecutive coordinates every kBlock * W.
 template <int N, int W>
 __global__ __launch_bounds__(kBlock) void k_dist_direct(const float* __restrict__ x, int64_t d,
                                                          int64_t chunk,
@@ -79,29 +45,7 @@ __global__ __launch_bounds__(kBlock) void k_dist_direct(const float* __restrict_
   for (int p = 0; p < P; ++p) acc[p] = 0.0f;
   const int64_t start = static_cast<int64_t>(blockIdx.x) * chunk;
   const int64_t end = (start + chunk < d) ? start + chunk : d;
-  for (int64_t c = start + static_cast<int64_t>(threadIdx.x) * W; c < end; c += kBlock * W) {
-    float v[N][W];
-    if (c + W <= end) {
-#pragma unroll
-      for (int i = 0; i < N; ++i) load_w<W>(x + static_cast<int64_t>(i) * d + c, v[i]);
-    } else {
-#pragma unroll
-      for (int i = 0; i < N; ++i) load_w_tail<W>(x + static_cast<int64_t>(i) * d + c, end - c, v[i]);
-    }
-#pragma unroll
-    for (int e = 0; e < W; ++e) {
-      int p = 0;
-#pragma unroll
-      for (int i = 0; i < N; ++i) {
-#pragma unroll
-        for (int j = i + 1; j < N; ++j) {
-          const float t = v[i][e] - v[j][e];
-          acc[p] = __builtin_fmaf(t, t, acc[p]);
-          ++p;
-        }
-      }
-    }
-  }
+  direct_accumulate<N, W>(MatrixRows{x, d}, start, end, acc);
   block_reduce_pairs<P>(acc, partial + blockIdx.x, gridDim.x);
 }
 
@@ -670,6 +614,12 @@ hipError_t enqueue_distances(const float* x, const DistPlan& p, const DistWorksp
   if (e != hipSuccess) return e;
   launch("sum_tiles", k_sum_tiles, dim3(p.entries), dim3(kBlock), 0, s, ws.partial, p.tiles,
     ws.sums);
+  return hipGetLastError();
+}
+
+hipError_t enqueue_sum_tiles(const double* partial, int64_t tiles, int entries, double* sums,
+                             hipStream_t s) {
+  launch("sum_tiles", k_sum_tiles, dim3(entries), dim3(kBlock), 0, s, partial, tiles, sums);
   return hipGetLastError();
 }
 

@@ -407,6 +407,64 @@ garfield_status garfield_seg_aggregate(garfield_segmented* seg, const float* x, 
   }
 }
 
+// Checks shared by the segment-table calls.
+static garfield_status check_table(const garfield_segmented* seg, const float* const* ptrs,
+                            const int64_t* dims, int K) {
+  if (!seg || K < 0 || (K > 0 && (!ptrs || !dims))) return GARFIELD_EINVAL;
+  if (seg->n > GARFIELD_DIRECT_MAX_N_LIMIT) return GARFIELD_ETOOBIG;
+  for (int s = 0; s < K; ++s)
+    if (dims[s] < 0) return GARFIELD_EINVAL;
+  return GARFIELD_OK;
+}
+
+garfield_status garfield_seg_accumulate_table(garfield_segmented* seg, const float* const* ptrs,
+                                              const int64_t* dims, int K, void* stream) {
+  garfield_status st = check_table(seg, ptrs, dims, K);
+  if (st != GARFIELD_OK) return st;
+  if (seg->k == 0 || seg->n < 2) return GARFIELD_OK;  // no distances (Median, Average, n = 1)
+  const int64_t tiles = table_tiles(dims, K);
+  if (tiles == 0) return GARFIELD_OK;  // every segment is empty: all distances 0
+  const int entries = seg->n * (seg->n - 1) / 2;
+  void* base = nullptr;
+  const size_t partial_bytes = align256(static_cast<size_t>(tiles) * entries * sizeof(double));
+  st = workspace(partial_bytes + align256(entries * sizeof(double)), &base);
+  if (st != GARFIELD_OK) return st;
+  double* partial = static_cast<double*>(base);
+  double* sums = reinterpret_cast<double*>(static_cast<char*>(base) + partial_bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = enqueue_distances_table(ptrs, seg->n, dims, K, partial, tiles, s);
+  if (e == hipSuccess) e = enqueue_sum_tiles(partial, tiles, entries, sums, s);
+  if (e == hipSuccess) e = enqueue_accumulate_dist(DistSums{sums, kEngineDirect, seg->n}, seg->dacc, s);
+  return to_status(e);
+}
+
+garfield_status garfield_seg_aggregate_table(garfield_segmented* seg, const float* const* ptrs,
+                                             const int64_t* dims, int K, float* const* outs,
+                                             void* stream) {
+  garfield_status st = check_table(seg, ptrs, dims, K);
+  if (st != GARFIELD_OK) return st;
+  if (K > 0 && !outs) return GARFIELD_EINVAL;
+  for (int s = 0; s < K; ++s)
+    if (dims[s] > 0 && (!outs[s] || reinterpret_cast<uintptr_t>(outs[s]) % sizeof(float) != 0))
+      return GARFIELD_EINVAL;
+  if (seg->k > 0 && !seg->selected) return GARFIELD_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int n = seg->n;
+  switch (seg->rule) {
+    case GARFIELD_RULE_KRUM:
+    case GARFIELD_RULE_MULTIKRUM:
+    case GARFIELD_RULE_MULTIKRUM_ITERATED:
+    case GARFIELD_RULE_MDA:
+      return to_status(enqueue_mean_rows_table(ptrs, n, dims, outs, K, seg->sel, seg->k, s));
+    case GARFIELD_RULE_BULYAN:
+      return to_status(enqueue_bulyan_table(ptrs, n, seg->f, dims, outs, K, seg->sel, s));
+    case GARFIELD_RULE_MEDIAN:
+      return to_status(enqueue_median_table(ptrs, n, dims, outs, K, nullptr, n, s));
+    default:  // Average
+      return to_status(enqueue_mean_rows_table(ptrs, n, dims, outs, K, nullptr, n, s));
+  }
+}
+
 garfield_status garfield_seg_destroy(garfield_segmented* seg) {
   if (!seg) return GARFIELD_OK;
   int cur = 0;

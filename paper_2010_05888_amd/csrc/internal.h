@@ -66,6 +66,27 @@ hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStr
 hipError_t enqueue_krum_rounds(const DistSums& ds, int f, int rounds, int32_t* sel,
                                hipStream_t s);
 
+// Tile partials (entry-major, `tiles` per entry) -> one fp64 sum per entry.
+hipError_t enqueue_sum_tiles(const double* partial, int64_t tiles, int entries, double* sums,
+                             hipStream_t s);
+
+// Segment tables (segtable.hip): K segments of n <= kDirectMaxNLimit vectors
+// stored apart, ptrs[s * n + i] -> segment s of vector i (dims[s] floats, host
+// array). Distances: direct-engine tile partials, entry-major with `tiles` =
+// table_tiles(dims, K) per entry. Aggregation: one output per segment (host
+// array of device pointers).
+int64_t table_tiles(const int64_t* dims, int K);
+hipError_t enqueue_distances_table(const float* const* ptrs, int n, const int64_t* dims, int K,
+                                   double* partial, int64_t tiles, hipStream_t s);
+hipError_t enqueue_mean_rows_table(const float* const* ptrs, int n, const int64_t* dims,
+                                   float* const* outs, int K, const int32_t* rows, int k,
+                                   hipStream_t s);
+hipError_t enqueue_median_table(const float* const* ptrs, int n, const int64_t* dims,
+                                float* const* outs, int K, const int32_t* rows, int k,
+                                hipStream_t s);
+hipError_t enqueue_bulyan_table(const float* const* ptrs, int n, int f, const int64_t* dims,
+                                float* const* outs, int K, const int32_t* sel, hipStream_t s);
+
 // Byzantine rows from the honest ones (byzantine.hip); kinds as garfield_attack.
 enum AttackKind { kAttackReverse = 0, kAttackRandom = 1, kAttackLittle = 2, kAttackEmpire = 3 };
 hipError_t enqueue_attack(int kind, const float* honest, int h, int64_t d, double param,
