@@ -301,7 +301,10 @@ def bench_workload(key, args):
     kt = gf.kernel_timing()
     gf.set_kernel_timing(False)
     kernels = {k: {"launches": c, "avg_ms": round(t / c, 6)} for k, (c, t) in kt.items()}
-    dominant = max(kt, key=lambda k: kt[k][1])
+    # the streaming kernel that took the most time (selection kernels have no
+    # algorithmic byte count; in latency-bound workloads they can take as long)
+    priced = [k for k in kt if algorithmic(k, w)[1]]
+    dominant = max(priced or kt, key=lambda k: kt[k][1])
     bound, per_launch = algorithmic(dominant, w)
     if per_launch and args.segments > 1:
         # per-segment calls: one launch per (equal) segment; a segment table: one

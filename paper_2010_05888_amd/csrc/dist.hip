@@ -515,6 +515,19 @@ void set_direct_max_n(int n) { __atomic_store_n(&g_direct_max_n, n, __ATOMIC_REL
 
 int vector_width(const float* p) { return reinterpret_cast<uintptr_t>(p) % 4 == 0 ? 4 : 1; }
 
+// Coordinates per tile of the direct engine: at most kDirectLaneCoords per lane
+// (each fp32 accumulator sums at most that many squares before the tile is
+// reduced in fp64), fewer when d is small, so that the grid still has about two
+// tiles per CU; always a multiple of one pass of the block (kBlock * width).
+int64_t direct_chunk(int64_t d, int width) {
+  const int64_t pass = static_cast<int64_t>(kBlock) * width;
+  const int64_t most = static_cast<int64_t>(kBlock) * kDirectLaneCoords;
+  const int64_t want = 2 * static_cast<int64_t>(device_cus());
+  int64_t chunk = (d + want - 1) / want;
+  chunk = (chunk + pass - 1) / pass * pass;
+  return chunk < pass ? pass : (chunk > most ? most : chunk);
+}
+
 DistPlan plan_distances(int n, int64_t d, const float* x) {
   DistPlan p;
   p.n = n;
@@ -524,9 +537,7 @@ DistPlan plan_distances(int n, int64_t d, const float* x) {
     p.engine = kEngineDirect;
     p.width = vector_width(x);
     if (p.width > direct_width_cap(n)) p.width = direct_width_cap(n);
-    // kDirectLaneCoords coordinates per lane per tile: each fp32 accumulator
-    // sums at most that many squares before the tile is reduced in fp64.
-    p.chunk = static_cast<int64_t>(kBlock) * kDirectLaneCoords;
+    p.chunk = direct_chunk(d, p.width);
     p.entries = n * (n - 1) / 2;
   } else {
     p.engine = kEngineGram;

@@ -422,7 +422,7 @@ garfield_status garfield_seg_accumulate_table(garfield_segmented* seg, const flo
   garfield_status st = check_table(seg, ptrs, dims, K);
   if (st != GARFIELD_OK) return st;
   if (seg->k == 0 || seg->n < 2) return GARFIELD_OK;  // no distances (Median, Average, n = 1)
-  const int64_t tiles = table_tiles(dims, K);
+  const int64_t tiles = table_tiles(dims, K, seg->n);
   if (tiles == 0) return GARFIELD_OK;  // every segment is empty: all distances 0
   const int entries = seg->n * (seg->n - 1) / 2;
   void* base = nullptr;

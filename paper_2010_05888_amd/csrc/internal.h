@@ -35,6 +35,9 @@ int direct_max_n();
 void set_direct_max_n(int n);
 
 DistPlan plan_distances(int n, int64_t d, const float* x);
+// Direct engine: coordinates per tile for a segment of length d read with
+// `width`-float loads.
+int64_t direct_chunk(int64_t d, int width);
 
 // Device workspace of the distance step (256-byte aligned sections).
 struct DistWorkspace {
@@ -73,9 +76,9 @@ hipError_t enqueue_sum_tiles(const double* partial, int64_t tiles, int entries, 
 // Segment tables (segtable.hip): K segments of n <= kDirectMaxNLimit vectors
 // stored apart, ptrs[s * n + i] -> segment s of vector i (dims[s] floats, host
 // array). Distances: direct-engine tile partials, entry-major with `tiles` =
-// table_tiles(dims, K) per entry. Aggregation: one output per segment (host
+// table_tiles(dims, K, n) per entry. Aggregation: one output per segment (host
 // array of device pointers).
-int64_t table_tiles(const int64_t* dims, int K);
+int64_t table_tiles(const int64_t* dims, int K, int n);
 hipError_t enqueue_distances_table(const float* const* ptrs, int n, const int64_t* dims, int K,
                                    double* partial, int64_t tiles, hipStream_t s);
 hipError_t enqueue_mean_rows_table(const float* const* ptrs, int n, const int64_t* dims,

@@ -22,13 +22,14 @@ struct TableRows {
 };
 
 // A batch of segments for one launch, passed by value in the kernel
-// arguments: each segment's length, its first workgroup and, for the
-// aggregation kernels, its output. Workgroup b works on the segment s with
-// first[s] <= b < first[s + 1].
+// arguments: each segment's length, the coordinates one of its workgroups
+// covers, its first workgroup and, for the aggregation kernels, its output.
+// Workgroup b works on the segment s with first[s] <= b < first[s + 1].
 constexpr int kSegMax = 96;
 struct SegTable {
   int count;
   int32_t first[kSegMax + 1];  // first[count] = workgroups of the launch
+  int32_t span[kSegMax];
   int64_t dims[kSegMax];
   float* outs[kSegMax];
 };

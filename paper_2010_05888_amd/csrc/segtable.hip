@@ -16,10 +16,9 @@ namespace garfield {
 
 namespace {
 
-constexpr int64_t kDirectChunk = static_cast<int64_t>(kBlock) * kDirectLaneCoords;
-
-// Distances: tiles of kDirectChunk coordinates, a segment's tiles consecutive;
-// tile b of this launch writes column tile_base + b of the entry-major partials.
+// Distances: a segment's tiles are consecutive, span[s] coordinates each (the
+// matrix engine's tile for that length, direct_chunk); tile b of this launch
+// writes column tile_base + b of the entry-major partials.
 template <int N, int W>
 __global__ __launch_bounds__(kBlock) void k_dist_direct_seg(const float* const* __restrict__ ptrs,
                                                              SegTable tab, int64_t tile_base,
@@ -31,14 +30,15 @@ __global__ __launch_bounds__(kBlock) void k_dist_direct_seg(const float* const* 
   for (int p = 0; p < P; ++p) acc[p] = 0.0f;
   const int b = blockIdx.x;
   const int s = seg_of(tab, b);
-  const int64_t start = static_cast<int64_t>(b - tab.first[s]) * kDirectChunk;
+  const int64_t start = static_cast<int64_t>(b - tab.first[s]) * tab.span[s];
   const int64_t d = tab.dims[s];
-  const int64_t end = start + kDirectChunk < d ? start + kDirectChunk : d;
+  const int64_t end = start + tab.span[s] < d ? start + tab.span[s] : d;
   direct_accumulate<N, W>(TableRows{ptrs + static_cast<int64_t>(s) * N}, start, end, acc);
   block_reduce_pairs<P>(acc, partial + tile_base + b, tiles);
 }
 
-// Aggregation: workgroup b covers kBlock * W coordinates of its segment.
+// Aggregation: workgroup b covers kBlock * W coordinates of its segment (W = 4).
+constexpr auto kAggSpan = [](int64_t) { return static_cast<int64_t>(kBlock) * 4; };
 template <int W>
 __device__ __forceinline__ int64_t seg_coord(const SegTable& tab, int s, int b) {
   return (static_cast<int64_t>(b - tab.first[s]) * kBlock + threadIdx.x) * W;
@@ -80,18 +80,20 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_agg_seg(const float* const* _
 
 // Cut a batch of K segments into launches of at most kSegMax segments and
 // call f(first segment, table, workgroups) for each launch that has work;
-// `per` = coordinates per workgroup.
-template <class F>
-hipError_t for_each_launch(const int64_t* dims, float* const* outs, int K, int64_t per, F&& f) {
+// per(d) = coordinates per workgroup for a segment of length d.
+template <class Per, class F>
+hipError_t for_each_launch(const int64_t* dims, float* const* outs, int K, Per&& per, F&& f) {
   for (int g0 = 0; g0 < K; g0 += kSegMax) {
     SegTable tab{};
     tab.count = K - g0 < kSegMax ? K - g0 : kSegMax;
     int64_t total = 0;
     for (int s = 0; s < tab.count; ++s) {
+      const int64_t span = per(dims[g0 + s]);
       tab.first[s] = static_cast<int32_t>(total);
+      tab.span[s] = static_cast<int32_t>(span);
       tab.dims[s] = dims[g0 + s];
       tab.outs[s] = outs ? outs[g0 + s] : nullptr;
-      total += (dims[g0 + s] + per - 1) / per;
+      total += (dims[g0 + s] + span - 1) / span;
       if (total > 0x7fffffff) return hipErrorInvalidValue;
     }
     tab.first[tab.count] = static_cast<int32_t>(total);
@@ -106,8 +108,9 @@ template <int N, int W>
 hipError_t dist_seg_nw(const float* const* ptrs, const int64_t* dims, int K, double* partial,
                        int64_t tiles, hipStream_t s) {
   int64_t base = 0;
-  return for_each_launch(dims, nullptr, K, kDirectChunk, [&](int g0, const SegTable& tab,
-                                                             int64_t total) {
+  auto per = [](int64_t d) { return direct_chunk(d, W); };
+  return for_each_launch(dims, nullptr, K, per, [&](int g0, const SegTable& tab,
+                                                    int64_t total) {
     launch("dist_direct_seg", k_dist_direct_seg<N, W>, dim3(static_cast<unsigned>(total)),
            dim3(kBlock), 0, s, ptrs + static_cast<int64_t>(g0) * N, tab, base, tiles, partial);
     base += total;
@@ -136,7 +139,7 @@ hipError_t median_seg_dispatch(int k, const float* const* ptrs, int n, const int
     return hipErrorInvalidValue;
   } else {
     if (k != K) return median_seg_dispatch<K + 1>(k, ptrs, n, rows, dims, outs, nseg, s);
-    return for_each_launch(dims, outs, nseg, kBlock * 4, [&](int g0, const SegTable& tab,
+    return for_each_launch(dims, outs, nseg, kAggSpan, [&](int g0, const SegTable& tab,
                                                             int64_t total) {
       launch("median_seg", k_median_seg<K, 4>, dim3(static_cast<unsigned>(total)), dim3(kBlock), 0,
              s, ptrs + static_cast<int64_t>(g0) * n, n, rows, tab);
@@ -154,7 +157,7 @@ hipError_t bulyan_seg_dispatch(int theta, int beta, const float* const* ptrs, in
   } else {
     if (theta != T)
       return bulyan_seg_dispatch<T + 1>(theta, beta, ptrs, n, sel, dims, outs, nseg, s);
-    return for_each_launch(dims, outs, nseg, kBlock * 4, [&](int g0, const SegTable& tab,
+    return for_each_launch(dims, outs, nseg, kAggSpan, [&](int g0, const SegTable& tab,
                                                             int64_t total) {
       launch("bulyan_agg_seg", k_bulyan_agg_seg<T, 4>, dim3(static_cast<unsigned>(total)),
              dim3(kBlock), 0, s, ptrs + static_cast<int64_t>(g0) * n, n, sel, beta, tab);
@@ -165,9 +168,15 @@ hipError_t bulyan_seg_dispatch(int theta, int beta, const float* const* ptrs, in
 
 }  // namespace
 
-int64_t table_tiles(const int64_t* dims, int K) {
+int table_width(int n) { return n <= 12 ? 4 : (n <= 19 ? 2 : 1); }
+
+int64_t table_tiles(const int64_t* dims, int K, int n) {
+  const int w = table_width(n);
   int64_t t = 0;
-  for (int s = 0; s < K; ++s) t += (dims[s] + kDirectChunk - 1) / kDirectChunk;
+  for (int s = 0; s < K; ++s) {
+    const int64_t c = direct_chunk(dims[s], w);
+    t += (dims[s] + c - 1) / c;
+  }
   return t;
 }
 
@@ -179,7 +188,7 @@ hipError_t enqueue_distances_table(const float* const* ptrs, int n, const int64_
 hipError_t enqueue_mean_rows_table(const float* const* ptrs, int n, const int64_t* dims,
                                    float* const* outs, int K, const int32_t* rows, int k,
                                    hipStream_t s) {
-  return for_each_launch(dims, outs, K, kBlock * 4, [&](int g0, const SegTable& tab,
+  return for_each_launch(dims, outs, K, kAggSpan, [&](int g0, const SegTable& tab,
                                                         int64_t total) {
     launch("mean_rows_seg", k_mean_rows_seg<4>, dim3(static_cast<unsigned>(total)), dim3(kBlock),
            0, s, ptrs + static_cast<int64_t>(g0) * n, n, rows, k, tab);

@@ -39,20 +39,17 @@ __device__ void load_and_rank(const DistSums& ds, double* D, unsigned char* orde
   __syncthreads();
 }
 
-// Index of the lowest (v, index) over lanes 0..63 of the calling wave (lanes
-// without a candidate pass +inf); every lane receives it. The minimum of
-// (value, index) pairs does not depend on the order of the comparisons.
-__device__ __forceinline__ int wave_argmin(double v, int idx) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const double ov = __shfl_xor(v, off, 64);
-    const int oi = __shfl_xor(idx, off, 64);
-    if (ov < v || (ov == v && oi < idx)) {
-      v = ov;
-      idx = oi;
-    }
-  }
-  return idx;
+// Lowest lane of the calling wave (all 64 lanes active) holding the smallest
+// v, or 64 when every v is +inf; every lane receives it. With lane i owning
+// index i this is the lowest (v, index). The minimum is the device library's
+// wave reduction (cross-lane DPP moves), then one ballot of the lanes that
+// hold it.
+extern "C" __device__ __attribute__((const)) double __ockl_wfred_min_f64(double);
+
+__device__ __forceinline__ int wave_argmin_lane(double v) {
+  const double m = __ockl_wfred_min_f64(v);
+  if (m == __builtin_inf()) return 64;
+  return __builtin_ctzll(__ballot(v == m));
 }
 
 // Write the indices i < n with flag[i] set, ascending.
@@ -112,7 +109,7 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_select(DistSums ds, int f, in
   __shared__ unsigned char order[kNmax * kNmax];
   __shared__ unsigned char pos[kNmax * kNmax];
   load_and_rank(ds, D, order, pos);
-  if (threadIdx.x >= 64) return;  // no barrier follows
+  if (threadIdx.x >= 64) return;  // no barrier follows; wave 0 stays whole
   const int i = threadIdx.x;
   const int k0 = n - f - 2 > 0 ? n - f - 2 : 0;
   double s = 0.0;
@@ -137,8 +134,7 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_select(DistSums ds, int f, in
         } while (kth >= 0 && !((active >> order[i * n + kth]) & 1));
       }
     }
-    p = __builtin_amdgcn_readfirstlane(
-        wave_argmin(mine ? s : __builtin_inf(), mine ? i : kNmax));
+    p = __builtin_amdgcn_readfirstlane(wave_argmin_lane(mine ? s : __builtin_inf()));
     if (p >= n) break;  // no vector left (rounds <= n - f keeps this from happening)
     active &= ~(uint64_t{1} << p);
     picked |= uint64_t{1} << p;
