@@ -56,6 +56,9 @@ def _parse():
     ap.add_argument("--table", action="store_true",
                     help="with --segments: feed the segments as a segment table (vectors stored "
                          "apart; one launch per 96 segments) instead of one call per segment")
+    ap.add_argument("--contract", action="store_true",
+                    help="contraction steps instead: 20 nodes of ResNet-18 size, each "
+                         "aggregating 17 peers (f = 3), one JSON line per rule")
     ap.add_argument("--byzantine", action="store_true",
                     help="the device attack generators and the variance statistics instead: one "
                          "JSON line per case, at workload 3's and 2's shapes")
@@ -545,6 +548,68 @@ def byzantine_bench(args):
         torch.cuda.empty_cache()
 
 
+def contract_bench(args):
+    """Contraction steps (Section 5, decentralized learning): n = 20 nodes of
+    ResNet-18 size, each node aggregating q = 17 random peers with f = 3, the
+    whole step (distances of all rows once, one selection workgroup per node,
+    one aggregation launch for all nodes). Algorithmic bytes: the distance
+    pass reads the n rows once; the aggregation reads the n rows once and
+    writes the n outputs (8 n d: the nodes share their peers' rows, which the
+    launch reads once into L2); `node_bytes` is what the nodes read one by one
+    (k rows each, k = q for Median, the selection size otherwise)."""
+    import torch
+
+    import paper_2010_05888_amd as gf
+
+    dev = torch.device("cuda:0")
+    n, q, f, d = 20, 17, 3, 11_173_962
+    g = torch.Generator(device=dev).manual_seed(2010058887)
+    x = torch.randn((n, d), device=dev, generator=g) * 0.01
+    perm = torch.Generator().manual_seed(2010058887)
+    peers = torch.stack([torch.randperm(n, generator=perm)[:q] for _ in range(n)]).to(
+        device=dev, dtype=torch.int32)
+    y = torch.empty_like(x)
+    for rule, m, k in (("median", None, q), ("multikrum", q - f, q - f),
+                       ("bulyan", None, q - 2 * f)):
+        def call():
+            gf.contract_step(rule, x, peers, f, m, out=y)
+        for _ in range(args.warmup):
+            call()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(args.steps):
+            call()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / args.steps
+        gf.set_kernel_timing(True)
+        for _ in range(args.steps):
+            call()
+        torch.cuda.synchronize()
+        kt = gf.kernel_timing()
+        gf.set_kernel_timing(False)
+        agg = {"median": "median_nodes", "multikrum": "mean_nodes", "bulyan": "bulyan_nodes"}[rule]
+        agg_bytes = 8.0 * n * d
+        rows = {agg: agg_bytes}
+        if rule != "median":
+            rows["dist_direct"] = 4.0 * n * d
+        roof = {}
+        for kern, nbytes in rows.items():
+            if kern in kt:
+                kms = kt[kern][1] / kt[kern][0]
+                roof[kern] = {"bytes_per_launch": nbytes, "avg_ms": round(kms, 6),
+                              "achieved": round(nbytes / (kms * 1e-3) / 1e9, 1),
+                              "frac": round(nbytes / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        print(json.dumps({
+            "bench": "contract", "rule": rule, "nodes": n, "peers": q, "f": f, "d": d,
+            "ms_per_step": round(ms, 5), "node_bytes": 4.0 * n * (k + 1) * d,
+            "GBps_input": round(n * d * 4 / (ms * 1e-3) / 1e9, 1),
+            "roofline": roof,
+            "kernels": {kk: {"launches": c, "avg_ms": round(t / c, 6)} for kk, (c, t) in kt.items()},
+            "steps": args.steps, "warmup": args.warmup}), flush=True)
+
+
 def main():
     args = _parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -569,6 +634,9 @@ def main():
         return
     if args.byzantine:
         byzantine_bench(args)
+        return
+    if args.contract:
+        contract_bench(args)
         return
     keys = [1, 2, 3, 4, 5, 6] if args.all else [args.workload]
     for key in keys:

@@ -148,6 +148,27 @@ garfield_status garfield_mda(const float* x, int n, int f, int64_t d, float* out
 garfield_status garfield_average(const float* x, int n, int64_t d, float* out, void* stream);
 
 /*
+ * One contraction step for n nodes at once (decentralized learning, Section 5:
+ * each node aggregates, with the rule, the vectors it receives from q peers,
+ * and repeats). x: device, n x d fp32 row-major, row v = node v's vector.
+ * peers: device, n x q int32, row v = the q distinct nodes v hears from (each
+ * in [0, n); v itself may be among them). y: device, n x d fp32 (must not
+ * overlap x), row v receives rule(x[peers[v][0]], ..., x[peers[v][q-1]]) with
+ * f Byzantine vectors tolerated among the q: rule = GARFIELD_RULE_KRUM,
+ * _MULTIKRUM, _MULTIKRUM_ITERATED (m as for garfield_multikrum, over q),
+ * _BULYAN, _MEDIAN or _AVERAGE (others: GARFIELD_EINVAL). The rule's
+ * requirement applies to q (e.g. q >= 2f+3 for Krum; GARFIELD_EREQ). Within a
+ * node, ties go to the earlier position in its peer list; a mean adds the
+ * selected rows in ascending row order (Average: in peer-list order).
+ * Distances are computed once for all n rows; selection runs one workgroup
+ * per node and aggregation one launch for all nodes. Repeat with x and y
+ * swapped for several steps. 1 <= q <= n <= GARFIELD_NMAX.
+ */
+garfield_status garfield_contract_step(int rule, const float* x, int n, int64_t d,
+                                       const int32_t* peers, int q, int f, int m, float* y,
+                                       void* stream);
+
+/*
  * Byzantine rows on the device: the attacks Garfield's Byzantine workers and
  * servers implement (Section 3.2, Main objects; Section 6.5 uses random
  * vectors and vectors reversed and amplified by -100). From the h honest

@@ -281,3 +281,35 @@ def delta(rule: str, n: int, f: int) -> float:
     if rule == "median":
         return math.sqrt(n - f) if n >= 2 * f + 1 else math.nan
     return math.nan
+
+
+# --- contraction steps ----------------------------------------------------------
+
+def contract_step(rule: str, x, peers, f: int, m: int | None = None):
+    """Row v = `rule` applied to the rows peers[v] of x, in peer-list order
+    (ties in a selection go to the earlier position in the list): the rule
+    functions above on each node's gathered rows. Average adds the rows in list
+    order in fp64 and rounds once. Returns (y, selections as sorted row
+    indices, or None)."""
+    x = _rows(x)
+    peers = np.asarray(peers, dtype=np.int64)
+    y = np.zeros_like(x)
+    sels = []
+    for v in range(x.shape[0]):
+        xs = np.ascontiguousarray(x[peers[v]])
+        if rule == "average":
+            acc = np.zeros(x.shape[1], dtype=np.float64)
+            for r in range(xs.shape[0]):
+                acc += xs[r].astype(np.float64)
+            y[v] = (acc / xs.shape[0]).astype(np.float32)
+            continue
+        if rule == "median":
+            y[v] = median(xs, f)
+            continue
+        fn = {"krum": lambda a: multikrum(a, f, 1), "multikrum": lambda a: multikrum(a, f, m),
+              "multikrum_iterated": lambda a: multikrum_iterated(a, f, m),
+              "bulyan": lambda a: bulyan(a, f)}[rule]
+        out, sel = fn(xs)[:2]
+        y[v] = out
+        sels.append(sorted(int(peers[v][t]) for t in sel))
+    return y, (sels if sels else None)

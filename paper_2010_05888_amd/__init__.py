@@ -25,7 +25,7 @@ __all__ = [
     "multikrum_median", "gar", "workspace_bytes", "release", "set_direct_max_n",
     "distance_engine", "gram_reference", "set_kernel_timing", "kernel_timing", "RULES",
     "ATTACKS", "attack", "variance_stats", "delta", "variance_condition", "Segmented",
-    "SegmentTable",
+    "SegmentTable", "contract_step", "contract",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -95,6 +95,8 @@ def load():
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = st
+    lib.garfield_contract_step.argtypes = [i32, vp, i32, i64, vp, i32, i32, i32, vp, vp]
+    lib.garfield_contract_step.restype = st
     lib.garfield_attack.argtypes = [i32, vp, i32, i64, ctypes.c_double, ctypes.c_uint64, vp, i32,
                                     vp]
     lib.garfield_attack.restype = st
@@ -269,6 +271,37 @@ def gar(name: str, x: torch.Tensor, f: int, **kw):
     except KeyError:
         raise ValueError(f"unknown rule {name!r}; known: {sorted(RULES)}") from None
     return rule(x, f, **kw)
+
+
+def contract_step(rule: str, x: torch.Tensor, peers: torch.Tensor, f: int, m: int | None = None,
+                  out: torch.Tensor | None = None) -> torch.Tensor:
+    """One contraction step: row v of the result is `rule` applied to the rows
+    peers[v] of x (n nodes, q peers each; peers a device int32 n x q tensor)."""
+    x = _input(x)
+    n, d = x.shape
+    if (not isinstance(peers, torch.Tensor) or peers.dtype != torch.int32 or peers.dim() != 2
+            or peers.shape[0] != n or peers.device != x.device):
+        raise ValueError("peers must be an n x q int32 tensor on x's device")
+    peers = peers.contiguous()
+    if out is None:
+        out = torch.empty_like(x)
+    elif out.shape != x.shape or out.dtype != torch.float32 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous n x d float32 tensor")
+    _check(load().garfield_contract_step(RULE_IDS[rule], _ptr(x), n, d, _ptr(peers),
+                                         peers.shape[1], f, m or 0, _ptr(out), _stream(x)),
+           "garfield_contract_step")
+    return out
+
+
+def contract(rule: str, x: torch.Tensor, peers: torch.Tensor, f: int, steps: int,
+             m: int | None = None) -> torch.Tensor:
+    """`steps` contraction steps from x (x itself is not modified)."""
+    a = _input(x).clone()
+    b = torch.empty_like(a)
+    for _ in range(steps):
+        contract_step(rule, a, peers, f, m, out=b)
+        a, b = b, a
+    return a
 
 
 def attack(kind: str, honest: torch.Tensor | None, nbyz: int, param: float, seed: int = 0,

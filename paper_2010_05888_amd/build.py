@@ -20,7 +20,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libgarfield.so")
 
 SOURCES = ["dist.hip", "select.hip", "aggregate.hip", "byzantine.hip", "segtable.hip",
-           "garfield_api.cpp", "timing.cpp"]
+           "contract.hip", "garfield_api.cpp", "timing.cpp"]
 
 ARCH = "gfx950"
 FLAGS = [

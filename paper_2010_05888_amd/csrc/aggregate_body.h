@@ -3,7 +3,8 @@
 // table of segments (segtable.hip). Each body handles W consecutive
 // coordinates c .. c+W-1 of a segment of length d and writes them to out + c;
 // the rows come from a source (rows.h) and, when `rows` is given, only the
-// listed ones are used.
+// listed ones are used. NT: nontemporal loads (rows read once); kernels whose
+// workgroups share rows read them with ordinary loads, which stay in L2.
 #pragma once
 
 #include "device_common.h"
@@ -33,7 +34,7 @@ __device__ __forceinline__ void store_out(float* __restrict__ out, int64_t c, in
 // ---------------------------------------------------------------------------
 // Mean of k rows: fp64 sum of the rows in the order listed, eight loads in
 // flight at a time, one rounding at the end.
-template <int W, bool FULL, class Src>
+template <int W, bool FULL, bool NT, class Src>
 __device__ __forceinline__ void sum_rows_at(const Src& src, int n, int64_t d,
                                             const int32_t* __restrict__ rows, int k, int64_t c,
                                             double* acc) {
@@ -43,7 +44,7 @@ __device__ __forceinline__ void sum_rows_at(const Src& src, int n, int64_t d,
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const float* p = src.row(row_of(rows, t + u, n)) + c;
-      if constexpr (FULL) load_w<W>(p, v[u]); else load_w_tail<W>(p, d - c, v[u]);
+      if constexpr (FULL) load_w<W, NT>(p, v[u]); else load_w_tail<W>(p, d - c, v[u]);
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u)
@@ -53,13 +54,13 @@ __device__ __forceinline__ void sum_rows_at(const Src& src, int n, int64_t d,
   for (; t < k; ++t) {
     float v[W];
     const float* p = src.row(row_of(rows, t, n)) + c;
-    if constexpr (FULL) load_w<W>(p, v); else load_w_tail<W>(p, d - c, v);
+    if constexpr (FULL) load_w<W, NT>(p, v); else load_w_tail<W>(p, d - c, v);
 #pragma unroll
     for (int e = 0; e < W; ++e) acc[e] += static_cast<double>(v[e]);
   }
 }
 
-template <int W, class Src>
+template <int W, bool NT = true, class Src>
 __device__ __forceinline__ void mean_at(const Src& src, int n, int64_t d,
                                         const int32_t* __restrict__ rows, int k, int64_t c,
                                         float* __restrict__ out) {
@@ -67,8 +68,8 @@ __device__ __forceinline__ void mean_at(const Src& src, int n, int64_t d,
 #pragma unroll
   for (int e = 0; e < W; ++e) acc[e] = 0.0;
   const bool full = c + W <= d;
-  if (full) sum_rows_at<W, true>(src, n, d, rows, k, c, acc);
-  else sum_rows_at<W, false>(src, n, d, rows, k, c, acc);
+  if (full) sum_rows_at<W, true, NT>(src, n, d, rows, k, c, acc);
+  else sum_rows_at<W, false, NT>(src, n, d, rows, k, c, acc);
   const double count = static_cast<double>(k);
   float o[W];
 #pragma unroll
@@ -79,7 +80,7 @@ __device__ __forceinline__ void mean_at(const Src& src, int n, int64_t d,
 // ---------------------------------------------------------------------------
 // Coordinate-wise median of K rows: all K loads back to back, then the
 // selection network per coordinate.
-template <int K, int W, class Src>
+template <int K, int W, bool NT = true, class Src>
 __device__ __forceinline__ void median_at(const Src& src, int n, int64_t d,
                                           const int32_t* __restrict__ rows, int64_t c,
                                           float* __restrict__ out) {
@@ -88,7 +89,7 @@ __device__ __forceinline__ void median_at(const Src& src, int n, int64_t d,
   const bool full = c + W <= d;
   if (full) {
 #pragma unroll
-    for (int t = 0; t < K; ++t) load_w<W>(src.row(row_of(rows, t, n)) + c, v[t]);
+    for (int t = 0; t < K; ++t) load_w<W, NT>(src.row(row_of(rows, t, n)) + c, v[t]);
   } else {
 #pragma unroll
     for (int t = 0; t < K; ++t) load_w_tail<W>(src.row(row_of(rows, t, n)) + c, d - c, v[t]);
@@ -121,7 +122,7 @@ __device__ __forceinline__ void median_at(const Src& src, int n, int64_t d,
 // iff key(L_a) < key(R_{K+1-a}) (a missing R counts as +inf). The number of
 // left values taken is the count of such a. `col` is this thread's column of
 // a T x kBlock LDS array (col[r * kBlock]).
-template <int T, int W, class Src>
+template <int T, int W, bool NT = true, class Src>
 __device__ __forceinline__ void bulyan_at(const Src& src, int n, int64_t d,
                                           const int32_t* __restrict__ sel, int beta, int64_t cc,
                                           float* col, float* __restrict__ out) {
@@ -135,7 +136,7 @@ __device__ __forceinline__ void bulyan_at(const Src& src, int n, int64_t d,
   const bool full = cc + W <= d;
   if (full) {
 #pragma unroll
-    for (int t = 0; t < T; ++t) load_w<W>(src.row(row_of(sel, t, n)) + cc, v[t]);
+    for (int t = 0; t < T; ++t) load_w<W, NT>(src.row(row_of(sel, t, n)) + cc, v[t]);
   } else {
 #pragma unroll
     for (int t = 0; t < T; ++t) load_w_tail<W>(src.row(row_of(sel, t, n)) + cc, d - cc, v[t]);

@@ -305,6 +305,45 @@ double garfield_delta(int rule, int n, int f) {
   }
 }
 
+garfield_status garfield_contract_step(int rule, const float* x, int n, int64_t d,
+                                       const int32_t* peers, int q, int f, int m, float* y,
+                                       void* stream) {
+  garfield_status st = check_common(x, n, f, d);
+  if (st != GARFIELD_OK) return st;
+  if (!peers || q < 1 || q > n) return GARFIELD_EINVAL;
+  if (d > 0 && (!y || reinterpret_cast<uintptr_t>(y) % sizeof(float) != 0)) return GARFIELD_EINVAL;
+  switch (rule) {
+    case GARFIELD_RULE_KRUM:
+    case GARFIELD_RULE_MULTIKRUM:
+    case GARFIELD_RULE_MULTIKRUM_ITERATED:
+    case GARFIELD_RULE_BULYAN:
+    case GARFIELD_RULE_MEDIAN:
+    case GARFIELD_RULE_AVERAGE:
+      break;
+    default:
+      return GARFIELD_EINVAL;
+  }
+  int k = 0;
+  st = rule_shape(rule, q, f, &m, &k);  // the rule's requirements apply to the q peers
+  if (st != GARFIELD_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (rule == GARFIELD_RULE_MEDIAN)
+    return to_status(enqueue_median_nodes(x, n, d, n, peers, q, y, s));
+  if (rule == GARFIELD_RULE_AVERAGE)
+    return to_status(enqueue_mean_nodes(x, n, d, n, peers, q, y, s));
+  DistSums ds;
+  void* scratch = nullptr;
+  st = run_distances(x, n, d, static_cast<size_t>(n) * k * sizeof(int32_t), &ds, &scratch, s);
+  if (st != GARFIELD_OK) return st;
+  int32_t* sel = static_cast<int32_t*>(scratch);
+  const int rounds = rule == GARFIELD_RULE_BULYAN ? q - 2 * f
+                     : rule == GARFIELD_RULE_MULTIKRUM_ITERATED ? m : 0;
+  hipError_t e = enqueue_peer_select(ds, n, peers, q, f, m, rounds, k, sel, s);
+  if (e != hipSuccess) return to_status(e);
+  if (rule == GARFIELD_RULE_BULYAN) return to_status(enqueue_bulyan_nodes(x, n, d, n, q, f, sel, y, s));
+  return to_status(enqueue_mean_nodes(x, n, d, n, sel, k, y, s));
+}
+
 garfield_status garfield_seg_create(int rule, int n, int f, int m, garfield_segmented** out) {
   if (!out) return GARFIELD_EINVAL;
   *out = nullptr;

@@ -90,6 +90,19 @@ hipError_t enqueue_median_table(const float* const* ptrs, int n, const int64_t* 
 hipError_t enqueue_bulyan_table(const float* const* ptrs, int n, int f, const int64_t* dims,
                                 float* const* outs, int K, const int32_t* sel, hipStream_t s);
 
+// Contraction steps (contract.hip, k_peer_select in select.hip): `nodes`
+// nodes, node v aggregating q peers (peers[v*q ..], rows of the n-row x).
+// Selection: sel[v*kout ..] = node v's chosen rows, ascending; rounds > 0 is
+// iterated Krum, else one-shot Multi-Krum with m. Aggregation: row v of y.
+hipError_t enqueue_peer_select(const DistSums& ds, int nodes, const int32_t* peers, int q, int f,
+                               int m, int rounds, int kout, int32_t* sel, hipStream_t s);
+hipError_t enqueue_mean_nodes(const float* x, int n, int64_t d, int nodes, const int32_t* rows,
+                              int k, float* y, hipStream_t s);
+hipError_t enqueue_median_nodes(const float* x, int n, int64_t d, int nodes, const int32_t* rows,
+                                int k, float* y, hipStream_t s);
+hipError_t enqueue_bulyan_nodes(const float* x, int n, int64_t d, int nodes, int q, int f,
+                                const int32_t* sel, float* y, hipStream_t s);
+
 // Byzantine rows from the honest ones (byzantine.hip); kinds as garfield_attack.
 enum AttackKind { kAttackReverse = 0, kAttackRandom = 1, kAttackLittle = 2, kAttackEmpire = 3 };
 hipError_t enqueue_attack(int kind, const float* honest, int h, int64_t d, double param,

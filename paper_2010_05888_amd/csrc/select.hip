@@ -15,13 +15,10 @@ namespace garfield {
 namespace {
 
 // order[i*n + r] = the j != i whose (D[i][j], j) has rank r in row i (and,
-// if pos is given, pos[i*n + j] = r). Scores then walk a row in ascending
-// distance order, which is the order the distances are added in (so identical
-// rows get bit-identical scores).
-__device__ void load_and_rank(const DistSums& ds, double* D, unsigned char* order,
-                              unsigned char* pos = nullptr) {
-  const int n = ds.n;
-  load_dist(ds, D);
+// if pos is given, pos[i*n + j] = r), for an n x n D in LDS. Scores then walk
+// a row in ascending distance order, which is the order the distances are
+// added in (so identical rows get bit-identical scores).
+__device__ void rank_rows(const double* D, int n, unsigned char* order, unsigned char* pos) {
   for (int idx = threadIdx.x; idx < n * n; idx += blockDim.x) {
     const int i = idx / n, j = idx % n;
     if (i == j) continue;
@@ -39,6 +36,12 @@ __device__ void load_and_rank(const DistSums& ds, double* D, unsigned char* orde
   __syncthreads();
 }
 
+__device__ void load_and_rank(const DistSums& ds, double* D, unsigned char* order,
+                              unsigned char* pos = nullptr) {
+  load_dist(ds, D);
+  rank_rows(D, ds.n, order, pos);
+}
+
 // Lowest lane of the calling wave (all 64 lanes active) holding the smallest
 // v, or 64 when every v is +inf; every lane receives it. With lane i owning
 // index i this is the lowest (v, index). The minimum is the device library's
@@ -52,26 +55,29 @@ __device__ __forceinline__ int wave_argmin_lane(double v) {
   return __builtin_ctzll(__ballot(v == m));
 }
 
-// Write the indices i < n with flag[i] set, ascending.
-__device__ void write_flagged(const int* flag, int n, int32_t* __restrict__ sel) {
-  const int i = threadIdx.x;
-  if (i < n && flag[i]) {
-    int pos = 0;
-    for (int j = 0; j < i; ++j) pos += flag[j];
-    sel[pos] = i;
+// Called by the 64 lanes of wave 0: write the selected local indices a < n
+// (bit a of the lane-uniform mask) to sel, as global indices map[a] (a itself
+// when map is null), in ascending order of the global index.
+__device__ void write_selected(uint64_t mask, int n, const int32_t* map,
+                               int32_t* __restrict__ sel) {
+  const int a = threadIdx.x;
+  if (a >= n || !((mask >> a) & 1)) return;
+  int pos;
+  if (!map) {
+    pos = __popcll(mask & ((uint64_t{1} << a) - 1));
+  } else {
+    pos = 0;
+    const int ga = map[a];
+    for (uint64_t rest = mask; rest; rest &= rest - 1) pos += map[__builtin_ctzll(rest)] < ga;
   }
+  sel[pos] = map ? map[a] : a;
 }
 
-// Multi-Krum: score(i) = sum of the k = n-f-2 smallest D[i][j], j != i; the
-// m lowest (score, i) are selected.
-__global__ __launch_bounds__(kBlock) void k_krum_select(DistSums ds, int f, int m,
-                                                        int32_t* __restrict__ sel) {
-  const int n = ds.n;
-  __shared__ double D[kNmax * kNmax];
-  __shared__ unsigned char order[kNmax * kNmax];
-  __shared__ double score[kNmax];
-  __shared__ int flag[kNmax];
-  load_and_rank(ds, D, order);
+// Multi-Krum on an n x n D in LDS: score(i) = sum of the k = n-f-2 smallest
+// D[i][j], j != i (in ascending order); flag[i] = i is among the m lowest
+// (score, i). All threads of the block take part.
+__device__ void krum_flags(const double* D, const unsigned char* order, int n, int f, int m,
+                           double* score, int* flag) {
   const int i = threadIdx.x;
   const int k = n - f - 2;
   if (i < n) {
@@ -87,7 +93,21 @@ __global__ __launch_bounds__(kBlock) void k_krum_select(DistSums ds, int f, int 
     flag[i] = rank < m;
   }
   __syncthreads();
-  write_flagged(flag, n, sel);
+}
+
+// Multi-Krum: the m lowest (score, i) are selected.
+__global__ __launch_bounds__(kBlock) void k_krum_select(DistSums ds, int f, int m,
+                                                        int32_t* __restrict__ sel) {
+  const int n = ds.n;
+  __shared__ double D[kNmax * kNmax];
+  __shared__ unsigned char order[kNmax * kNmax];
+  __shared__ double score[kNmax];
+  __shared__ int flag[kNmax];
+  load_and_rank(ds, D, order);
+  krum_flags(D, order, n, f, m, score, flag);
+  if (threadIdx.x >= 64) return;
+  const uint64_t mask = __ballot(static_cast<int>(threadIdx.x) < n && flag[threadIdx.x]);
+  write_selected(mask, n, nullptr, sel);
 }
 
 // Iterated Krum, Bulyan's selection (theta = n-2f rounds) and the iterated
@@ -98,18 +118,15 @@ __global__ __launch_bounds__(kBlock) void k_krum_select(DistSums ds, int f, int 
 // that a row's score follows the removals: when the pick p leaves and k drops
 // by one, the new score is the old one minus D[i][p] if p was among i's k
 // nearest, else minus the k-th nearest (tracked by its position in the
-// row's ranking, which then steps back to the previous remaining vector).
+// row's ranking, which then steps back to the previous remaining vector); with
+// one neighbour left the score is reset to that distance itself.
 // After the ranking the rounds run in wave 0 alone (n <= 64: lane i owns row
 // i), with the remaining set as a 64-bit mask every lane holds, so a round
 // needs no workgroup barrier.
-__global__ __launch_bounds__(kBlock) void k_bulyan_select(DistSums ds, int f, int rounds,
-                                                          int32_t* __restrict__ sel) {
-  const int n = ds.n;
-  __shared__ double D[kNmax * kNmax];
-  __shared__ unsigned char order[kNmax * kNmax];
-  __shared__ unsigned char pos[kNmax * kNmax];
-  load_and_rank(ds, D, order, pos);
-  if (threadIdx.x >= 64) return;  // no barrier follows; wave 0 stays whole
+// Called by the 64 lanes of wave 0 on a ranked n x n D in LDS; returns the
+// lane-uniform mask of the picked rows.
+__device__ uint64_t krum_rounds_mask(const double* D, const unsigned char* order,
+                                     const unsigned char* pos, int n, int f, int rounds) {
   const int i = threadIdx.x;
   const int k0 = n - f - 2 > 0 ? n - f - 2 : 0;
   double s = 0.0;
@@ -133,14 +150,68 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_select(DistSums ds, int f, in
           --kth;
         } while (kth >= 0 && !((active >> order[i * n + kth]) & 1));
       }
+      // One neighbour: the score is that one distance, exactly (the subtractions
+      // above leave fp64 rounding), so that two mutual nearest neighbours tie
+      // exactly and the lower index decides, as in the definition.
+      if (k == 1) s = D[i * n + order[i * n + kth]];
     }
     p = __builtin_amdgcn_readfirstlane(wave_argmin_lane(mine ? s : __builtin_inf()));
     if (p >= n) break;  // no vector left (rounds <= n - f keeps this from happening)
     active &= ~(uint64_t{1} << p);
     picked |= uint64_t{1} << p;
   }
-  if (i < n && ((picked >> i) & 1))
-    sel[__popcll(picked & ((uint64_t{1} << i) - 1))] = i;
+  return picked;
+}
+
+__global__ __launch_bounds__(kBlock) void k_bulyan_select(DistSums ds, int f, int rounds,
+                                                          int32_t* __restrict__ sel) {
+  const int n = ds.n;
+  __shared__ double D[kNmax * kNmax];
+  __shared__ unsigned char order[kNmax * kNmax];
+  __shared__ unsigned char pos[kNmax * kNmax];
+  load_and_rank(ds, D, order, pos);
+  if (threadIdx.x >= 64) return;  // no barrier follows; wave 0 stays whole
+  write_selected(krum_rounds_mask(D, order, pos, n, f, rounds), n, nullptr, sel);
+}
+
+// Contraction (many nodes, each aggregating its peers): workgroup v gathers the
+// distances among its q peers (peers[v*q .. v*q+q-1], rows of the N-row input
+// whose distance sums are ds) into LDS and selects among them, ties going to
+// the earlier position in the peer list; sel[v*kout ..] receives the chosen
+// rows as input-row indices, ascending. rounds > 0: that many rounds of
+// iterated Krum; else one-shot Multi-Krum with m.
+__global__ __launch_bounds__(kBlock) void k_peer_select(DistSums ds,
+                                                        const int32_t* __restrict__ peers, int q,
+                                                        int f, int m, int rounds, int kout,
+                                                        int32_t* __restrict__ sel) {
+  __shared__ double D[kNmax * kNmax];
+  __shared__ unsigned char order[kNmax * kNmax];
+  __shared__ unsigned char pos[kNmax * kNmax];
+  __shared__ double score[kNmax];
+  __shared__ int flag[kNmax];
+  __shared__ int32_t map[kNmax];
+  const int v = blockIdx.x;
+  if (static_cast<int>(threadIdx.x) < q) {
+    const int r = peers[static_cast<int64_t>(v) * q + threadIdx.x];
+    map[threadIdx.x] = r < 0 ? 0 : (r >= ds.n ? ds.n - 1 : r);
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < q * q; idx += blockDim.x) {
+    const int a = idx / q, b = idx % q;
+    D[idx] = a == b ? 0.0 : dist_entry(ds, map[a], map[b]);
+  }
+  __syncthreads();
+  rank_rows(D, q, order, pos);
+  int32_t* out = sel + static_cast<int64_t>(v) * kout;
+  if (rounds > 0) {
+    if (threadIdx.x >= 64) return;
+    write_selected(krum_rounds_mask(D, order, pos, q, f, rounds), q, map, out);
+  } else {
+    krum_flags(D, order, q, f, m, score, flag);
+    if (threadIdx.x >= 64) return;
+    const uint64_t mask = __ballot(static_cast<int>(threadIdx.x) < q && flag[threadIdx.x]);
+    write_selected(mask, q, map, out);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -305,6 +376,13 @@ hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStr
 hipError_t enqueue_krum_rounds(const DistSums& ds, int f, int rounds, int32_t* sel,
                                hipStream_t s) {
   launch("krum_rounds", k_bulyan_select, dim3(1), dim3(kBlock), 0, s, ds, f, rounds, sel);
+  return hipGetLastError();
+}
+
+hipError_t enqueue_peer_select(const DistSums& ds, int nodes, const int32_t* peers, int q, int f,
+                               int m, int rounds, int kout, int32_t* sel, hipStream_t s) {
+  launch("peer_select", k_peer_select, dim3(nodes), dim3(kBlock), 0, s, ds, peers, q, f, m, rounds,
+         kout, sel);
   return hipGetLastError();
 }
 

@@ -265,6 +265,28 @@ def test_bulyan_shapes(n, f):
     pytest.fail("no pinned seed in 5 tries")
 
 
+@pytest.mark.parametrize("n", [11, 15, 19])
+def test_one_neighbour_rounds_break_ties_by_index(n):
+    # Bulyan with f = 2 ends with rounds of one neighbour, where the two rows of
+    # a mutual-nearest pair always tie (both scores are their one distance):
+    # the lower index must win on every seed, not rounding noise
+    f = 2
+    for seed in range(12):
+        rng = np.random.default_rng(7000 + 31 * n + seed)
+        x = rng.standard_normal((n, 1999)).astype(np.float32)
+        x *= (1.0 + 0.5 * rng.permutation(n) / n).astype(np.float32)[:, None]
+        xt = _to_dev(x)
+        Do = oracle.pairwise_sqdist(x)
+        B, _ = _bounds(x, xt, Do)
+        oo, so, picks, rs = oracle.bulyan(x, f, return_rounds=True)
+        if not parity.bulyan_pinned(picks, rs, Do, B, n, f, parity.identical_rows(Do))[0]:
+            continue
+        out, sel = gf.bulyan(xt, f)
+        assert sel.cpu().numpy().tolist() == so.tolist(), seed
+        _, si = gf.multikrum_iterated(xt, f, n - 2 * f)
+        assert si.cpu().numpy().tolist() == so.tolist(), seed
+
+
 def test_bulyan_small_integer_ties():
     # integer inputs: exact distances on both sides, many exact ties in every
     # round and in the closeness key of the trimmed mean
