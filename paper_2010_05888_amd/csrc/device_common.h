@@ -60,4 +60,26 @@ __device__ __forceinline__ void load_w_tail(const float* __restrict__ p, int64_t
   for (int e = 0; e < W; ++e) v[e] = (e < limit) ? p[e] : 0.0f;
 }
 
+// Lowest lane of the calling wave (all 64 lanes active) holding the smallest
+// v, or 64 when every v is +inf; every lane receives it. With lane i owning
+// index i this is the lowest (v, index). The minimum is the device library's
+// wave reduction (cross-lane DPP moves), then one ballot of the lanes that
+// hold it.
+extern "C" __device__ __attribute__((const)) double __ockl_wfred_min_f64(double);
+
+__device__ __forceinline__ int wave_argmin_lane(double v) {
+  const double m = __ockl_wfred_min_f64(v);
+  if (m == __builtin_inf()) return 64;
+  return __builtin_ctzll(__ballot(v == m));
+}
+
+// Sum of v over the 64 lanes of the calling wave (all active), by an xor
+// butterfly: every lane receives the same bits, and the grouping is fixed, so
+// the result depends only on which lane holds which value.
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+
 }  // namespace garfield

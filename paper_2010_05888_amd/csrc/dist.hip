@@ -50,73 +50,86 @@ __global__ __launch_bounds__(kBlock) void k_dist_direct(const float* __restrict_
 }
 
 // ---------------------------------------------------------------------------
-// Gram engine, step 1: probe. Block i sums (x_i - x_j)^2 for every j over a
-// sample of kProbeRuns runs of kBlock consecutive coordinates spread evenly
-// over d (all coordinates when d is smaller than the sample), and writes row
-// i of the probe matrix (kNmax columns, fp64).
+// Gram engine, step 1: probe. The sample is kProbeRuns runs of kBlock
+// consecutive coordinates spread evenly over d (all of d in one run when d is
+// smaller than the sample). Workgroup (i, r) sums (x_i - x_j)^2 for every j
+// over run r and writes row i of run r's probe matrix (kNmax x kNmax, fp64):
+// one workgroup per row and run keeps the rows' scattered first touches in
+// flight together rather than one run after another.
+int probe_runs(int64_t d) {
+  return d <= static_cast<int64_t>(kProbeRuns) * kBlock ? 1 : kProbeRuns;
+}
+
 __global__ __launch_bounds__(kBlock) void k_probe(const float* __restrict__ x, int n, int64_t d,
                                                   double* __restrict__ probe) {
-  const int i = blockIdx.x;
+  const int i = blockIdx.x, r = blockIdx.y;
   float acc[kNmax];
 #pragma unroll
   for (int j = 0; j < kNmax; ++j) acc[j] = 0.0f;
-  const int64_t sample = static_cast<int64_t>(kProbeRuns) * kBlock;
-  const int64_t runs = (d <= sample) ? 1 : kProbeRuns;
-  const int64_t stride = d / runs;
+  const int64_t runs = gridDim.y;
   const int64_t len = (runs == 1) ? d : kBlock;
-  for (int64_t r = 0; r < runs; ++r) {
-    for (int64_t o = threadIdx.x; o < len; o += kBlock) {
-      const int64_t c = r * stride + o;
-      const float xi = x[static_cast<int64_t>(i) * d + c];
+  const int64_t first = r * (d / runs);
+  for (int64_t o = threadIdx.x; o < len; o += kBlock) {
+    const int64_t c = first + o;
+    const float xi = x[static_cast<int64_t>(i) * d + c];
 #pragma unroll
-      for (int j = 0; j < kNmax; ++j) {
-        if (j < n) {
-          const float t = xi - x[static_cast<int64_t>(j) * d + c];
-          acc[j] = __builtin_fmaf(t, t, acc[j]);
-        }
+    for (int j = 0; j < kNmax; ++j) {
+      if (j < n) {
+        const float t = xi - x[static_cast<int64_t>(j) * d + c];
+        acc[j] = __builtin_fmaf(t, t, acc[j]);
       }
     }
   }
-  block_reduce_pairs<kNmax>(acc, probe + i * kNmax, 1);
+  block_reduce_pairs<kNmax>(acc, probe + (static_cast<int64_t>(r) * kNmax + i) * kNmax, 1);
 }
 
 // Gram engine, step 2: the reference row is the one whose sum of its
 // ceil(n/2) smallest probe distances (self included, which is 0) is lowest:
-// with an honest majority this is a central, honest row.
-__global__ __launch_bounds__(kBlock) void k_pick_ref(const double* __restrict__ probe, int n,
-                                                     int32_t* __restrict__ ref) {
-  __shared__ double P[kNmax * kNmax];
-  __shared__ unsigned char take[kNmax * kNmax];
+// with an honest majority this is a central, honest row. The probe distance
+// of (i, j) is the sum of the runs' partial sums in run order (every thread
+// issues all its loads before the first sum). Wave w of the 16 scores rows
+// w, w + 16, ...: lane j ranks entry (i, j) in row i (ties by index) and the
+// entries ranked below h are summed across the wave; wave 0 then takes the
+// lowest (score, row).
+constexpr int kPickThreads = 1024;
+
+__global__ __launch_bounds__(kPickThreads) void k_pick_ref(const double* __restrict__ probe, int n,
+                                                           int runs, int32_t* __restrict__ ref) {
+  constexpr int kPer = kNmax * kNmax / kPickThreads;
+  __shared__ double P[kNmax * kNmax];  // row stride kNmax; entries beyond n unused
   __shared__ double score[kNmax];
-  for (int idx = threadIdx.x; idx < n * n; idx += kBlock)
-    P[idx] = probe[(idx / n) * kNmax + idx % n];
+  double v[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) v[k] = 0.0;
+  for (int r = 0; r < runs; ++r) {
+    const double* q = probe + static_cast<int64_t>(r) * kNmax * kNmax;
+    double t[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) t[k] = q[threadIdx.x + k * kPickThreads];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) v[k] += t[k];
+  }
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) P[threadIdx.x + k * kPickThreads] = v[k];
   __syncthreads();
   const int h = (n + 1) / 2;
-  // entry (i, j) contributes to row i's score when its rank (ties by index)
-  // among row i is below h
-  for (int idx = threadIdx.x; idx < n * n; idx += kBlock) {
-    const int i = idx / n, j = idx % n;
-    const double v = P[idx];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int i = wave; i < n; i += kPickThreads / 64) {
+    const double* row = P + i * kNmax;
+    const double x = lane < n ? row[lane] : 0.0;
     int rank = 0;
+#pragma unroll 8
     for (int j2 = 0; j2 < n; ++j2) {
-      const double w = P[i * n + j2];
-      rank += (w < v) || (w == v && j2 < j);
+      const double w = row[j2];
+      rank += (w < x) | ((w == x) & (j2 < lane));
     }
-    take[idx] = rank < h;
+    const double s = wave_sum(lane < n && rank < h ? x : 0.0);
+    if (lane == 0) score[i] = s;
   }
   __syncthreads();
-  if (threadIdx.x < n) {
-    double s = 0.0;
-    for (int j = 0; j < n; ++j)
-      if (take[threadIdx.x * n + j]) s += P[threadIdx.x * n + j];
-    score[threadIdx.x] = s;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int best = 0;
-    for (int j = 1; j < n; ++j)
-      if (score[j] < score[best]) best = j;
-    *ref = best;
+  if (wave == 0) {
+    const int best = wave_argmin_lane(lane < n ? score[lane] : __builtin_inf());
+    if (lane == 0) *ref = best;
   }
 }
 
@@ -565,7 +578,7 @@ size_t dist_workspace_bytes(const DistPlan& p) {
     b += align256(static_cast<size_t>(p.entries) * sizeof(double));
   }
   if (p.engine == kEngineGram) {
-    b += align256(static_cast<size_t>(kNmax) * kNmax * sizeof(double));
+    b += align256(static_cast<size_t>(kProbeRuns) * kNmax * kNmax * sizeof(double));
     b += align256(sizeof(int32_t));
   }
   return b;
@@ -582,7 +595,7 @@ DistWorkspace carve_dist_workspace(const DistPlan& p, void* base) {
   }
   if (p.engine == kEngineGram) {
     w.probe = reinterpret_cast<double*>(c);
-    c += align256(static_cast<size_t>(kNmax) * kNmax * sizeof(double));
+    c += align256(static_cast<size_t>(kProbeRuns) * kNmax * kNmax * sizeof(double));
     w.ref = reinterpret_cast<int32_t*>(c);
   }
   return w;
@@ -598,10 +611,11 @@ DistSums dist_sums(const DistPlan& p, const DistWorkspace& ws) {
 
 hipError_t enqueue_reference(const float* x, const DistPlan& p, const DistWorkspace& ws,
                              hipStream_t s) {
-  launch("probe", k_probe, dim3(p.n), dim3(kBlock), 0, s, x, p.n, p.d, ws.probe);
+  const int runs = probe_runs(p.d);
+  launch("probe", k_probe, dim3(p.n, runs), dim3(kBlock), 0, s, x, p.n, p.d, ws.probe);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  launch("pick_ref", k_pick_ref, dim3(1), dim3(kBlock), 0, s, ws.probe, p.n, ws.ref);
+  launch("pick_ref", k_pick_ref, dim3(1), dim3(kPickThreads), 0, s, ws.probe, p.n, runs, ws.ref);
   return hipGetLastError();
 }
 

@@ -43,7 +43,7 @@ int64_t direct_chunk(int64_t d, int width);
 struct DistWorkspace {
   double* partial = nullptr;  // entries x tiles (entry-major)
   double* sums = nullptr;     // entries
-  double* probe = nullptr;    // kNmax x kNmax (Gram engine only)
+  double* probe = nullptr;    // kProbeRuns x kNmax x kNmax (Gram engine only)
   int32_t* ref = nullptr;     // 1 (Gram engine only)
 };
 struct DistSums;

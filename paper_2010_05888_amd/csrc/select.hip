@@ -42,19 +42,6 @@ __device__ void load_and_rank(const DistSums& ds, double* D, unsigned char* orde
   rank_rows(D, ds.n, order, pos);
 }
 
-// Lowest lane of the calling wave (all 64 lanes active) holding the smallest
-// v, or 64 when every v is +inf; every lane receives it. With lane i owning
-// index i this is the lowest (v, index). The minimum is the device library's
-// wave reduction (cross-lane DPP moves), then one ballot of the lanes that
-// hold it.
-extern "C" __device__ __attribute__((const)) double __ockl_wfred_min_f64(double);
-
-__device__ __forceinline__ int wave_argmin_lane(double v) {
-  const double m = __ockl_wfred_min_f64(v);
-  if (m == __builtin_inf()) return 64;
-  return __builtin_ctzll(__ballot(v == m));
-}
-
 // Called by the 64 lanes of wave 0: write the selected local indices a < n
 // (bit a of the lane-uniform mask) to sel, as global indices map[a] (a itself
 // when map is null), in ascending order of the global index.
@@ -74,29 +61,41 @@ __device__ void write_selected(uint64_t mask, int n, const int32_t* map,
 }
 
 // Multi-Krum on an n x n D in LDS: score(i) = sum of the k = n-f-2 smallest
-// D[i][j], j != i (in ascending order); flag[i] = i is among the m lowest
-// (score, i). All threads of the block take part.
+// D[i][j], j != i; flag[i] = i is among the m lowest (score, i). All threads
+// of the block take part. One wave sums a row: lane r holds the row's r-th
+// smallest distance, and the lanes below k are added by the wave's butterfly,
+// so rows with the same distances (in any order) get bit-identical scores.
 __device__ void krum_flags(const double* D, const unsigned char* order, int n, int f, int m,
                            double* score, int* flag) {
-  const int i = threadIdx.x;
-  const int k = n - f - 2;
-  if (i < n) {
-    double s = 0.0;
-    for (int r = 0; r < k; ++r) s += D[i * n + order[i * n + r]];
-    score[i] = s;
+  const int k = n - f - 2;  // 1 .. n-2 (n >= 2f+3)
+  const int lane = threadIdx.x & 63;
+  for (int i = threadIdx.x >> 6; i < n; i += blockDim.x >> 6) {
+    const double v = lane < k ? D[i * n + order[i * n + lane]] : 0.0;
+    const double s = wave_sum(v);
+    if (lane == 0) score[i] = s;
   }
   __syncthreads();
+  const int i = threadIdx.x;
   if (i < n) {
     const double si = score[i];
     int rank = 0;
-    for (int j = 0; j < n; ++j) rank += (score[j] < si) || (score[j] == si && j < i);
+#pragma unroll 8
+    for (int j = 0; j < n; ++j) {
+      const double w = score[j];
+      rank += (w < si) | ((w == si) & (j < i));
+    }
     flag[i] = rank < m;
   }
   __syncthreads();
 }
 
 // Multi-Krum: the m lowest (score, i) are selected.
-__global__ __launch_bounds__(kBlock) void k_krum_select(DistSums ds, int f, int m,
+// The single-workgroup selections run 16 waves: the distance loads and the
+// rankings (independent LDS reads per entry) spread over four times as many
+// lanes as a kBlock workgroup has.
+constexpr int kSelectThreads = 1024;
+
+__global__ __launch_bounds__(kSelectThreads) void k_krum_select(DistSums ds, int f, int m,
                                                         int32_t* __restrict__ sel) {
   const int n = ds.n;
   __shared__ double D[kNmax * kNmax];
@@ -163,7 +162,7 @@ __device__ uint64_t krum_rounds_mask(const double* D, const unsigned char* order
   return picked;
 }
 
-__global__ __launch_bounds__(kBlock) void k_bulyan_select(DistSums ds, int f, int rounds,
+__global__ __launch_bounds__(kSelectThreads) void k_bulyan_select(DistSums ds, int f, int rounds,
                                                           int32_t* __restrict__ sel) {
   const int n = ds.n;
   __shared__ double D[kNmax * kNmax];
@@ -364,18 +363,18 @@ size_t mda_scratch_bytes(int n, int f) {
 }
 
 hipError_t enqueue_krum_select(const DistSums& ds, int f, int m, int32_t* sel, hipStream_t s) {
-  launch("krum_select", k_krum_select, dim3(1), dim3(kBlock), 0, s, ds, f, m, sel);
+  launch("krum_select", k_krum_select, dim3(1), dim3(kSelectThreads), 0, s, ds, f, m, sel);
   return hipGetLastError();
 }
 
 hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStream_t s) {
-  launch("bulyan_select", k_bulyan_select, dim3(1), dim3(kBlock), 0, s, ds, f, ds.n - 2 * f, sel);
+  launch("bulyan_select", k_bulyan_select, dim3(1), dim3(kSelectThreads), 0, s, ds, f, ds.n - 2 * f, sel);
   return hipGetLastError();
 }
 
 hipError_t enqueue_krum_rounds(const DistSums& ds, int f, int rounds, int32_t* sel,
                                hipStream_t s) {
-  launch("krum_rounds", k_bulyan_select, dim3(1), dim3(kBlock), 0, s, ds, f, rounds, sel);
+  launch("krum_rounds", k_bulyan_select, dim3(1), dim3(kSelectThreads), 0, s, ds, f, rounds, sel);
   return hipGetLastError();
 }
 
