@@ -570,7 +570,7 @@ def contract_bench(args):
         device=dev, dtype=torch.int32)
     y = torch.empty_like(x)
     for rule, m, k in (("median", None, q), ("multikrum", q - f, q - f),
-                       ("bulyan", None, q - 2 * f)):
+                       ("bulyan", None, q - 2 * f), ("mda", None, q - f)):
         def call():
             gf.contract_step(rule, x, peers, f, m, out=y)
         for _ in range(args.warmup):
@@ -589,7 +589,8 @@ def contract_bench(args):
         torch.cuda.synchronize()
         kt = gf.kernel_timing()
         gf.set_kernel_timing(False)
-        agg = {"median": "median_nodes", "multikrum": "mean_nodes", "bulyan": "bulyan_nodes"}[rule]
+        agg = {"median": "median_nodes", "multikrum": "mean_nodes", "bulyan": "bulyan_nodes",
+               "mda": "mean_nodes"}[rule]
         agg_bytes = 8.0 * n * d
         rows = {agg: agg_bytes}
         if rule != "median":

@@ -46,6 +46,8 @@ extern "C" {
 #define GARFIELD_NMAX 64
 /* Largest number of candidate subsets C(n, f) MDA will enumerate. */
 #define GARFIELD_MDA_MAX_SUBSETS 2147483647LL
+/* The same per node in a contraction step (C(q, f)). */
+#define GARFIELD_CONTRACT_MDA_MAX_SUBSETS 1048576LL
 
 typedef enum garfield_status {
   GARFIELD_OK = 0,
@@ -156,10 +158,13 @@ garfield_status garfield_average(const float* x, int n, int64_t d, float* out, v
  * overlap x), row v receives rule(x[peers[v][0]], ..., x[peers[v][q-1]]) with
  * f Byzantine vectors tolerated among the q: rule = GARFIELD_RULE_KRUM,
  * _MULTIKRUM, _MULTIKRUM_ITERATED (m as for garfield_multikrum, over q),
- * _BULYAN, _MEDIAN or _AVERAGE (others: GARFIELD_EINVAL). The rule's
- * requirement applies to q (e.g. q >= 2f+3 for Krum; GARFIELD_EREQ). Within a
- * node, ties go to the earlier position in its peer list; a mean adds the
- * selected rows in ascending row order (Average: in peer-list order).
+ * _BULYAN, _MEDIAN, _MDA or _AVERAGE (others: GARFIELD_EINVAL). The rule's
+ * requirement applies to q (e.g. q >= 2f+3 for Krum; GARFIELD_EREQ); MDA
+ * also needs C(q, f) <= GARFIELD_CONTRACT_MDA_MAX_SUBSETS, since one
+ * workgroup searches a node's subsets (GARFIELD_ETOOBIG). Within a node, ties
+ * go to the earlier position in its peer list (for MDA: the first subset of
+ * positions in lexicographic order); a mean adds the selected rows in
+ * ascending row order (Average: in peer-list order).
  * Distances are computed once for all n rows; selection runs one workgroup
  * per node and aggregation one launch for all nodes. Repeat with x and y
  * swapped for several steps. 1 <= q <= n <= GARFIELD_NMAX.

@@ -308,7 +308,7 @@ def contract_step(rule: str, x, peers, f: int, m: int | None = None):
             continue
         fn = {"krum": lambda a: multikrum(a, f, 1), "multikrum": lambda a: multikrum(a, f, m),
               "multikrum_iterated": lambda a: multikrum_iterated(a, f, m),
-              "bulyan": lambda a: bulyan(a, f)}[rule]
+              "bulyan": lambda a: bulyan(a, f), "mda": lambda a: mda(a, f)}[rule]
         out, sel = fn(xs)[:2]
         y[v] = out
         sels.append(sorted(int(peers[v][t]) for t in sel))

@@ -319,6 +319,7 @@ garfield_status garfield_contract_step(int rule, const float* x, int n, int64_t 
     case GARFIELD_RULE_BULYAN:
     case GARFIELD_RULE_MEDIAN:
     case GARFIELD_RULE_AVERAGE:
+    case GARFIELD_RULE_MDA:
       break;
     default:
       return GARFIELD_EINVAL;
@@ -326,6 +327,8 @@ garfield_status garfield_contract_step(int rule, const float* x, int n, int64_t 
   int k = 0;
   st = rule_shape(rule, q, f, &m, &k);  // the rule's requirements apply to the q peers
   if (st != GARFIELD_OK) return st;
+  if (rule == GARFIELD_RULE_MDA && binomial(q, f) > GARFIELD_CONTRACT_MDA_MAX_SUBSETS)
+    return GARFIELD_ETOOBIG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (rule == GARFIELD_RULE_MEDIAN)
     return to_status(enqueue_median_nodes(x, n, d, n, peers, q, y, s));
@@ -338,7 +341,8 @@ garfield_status garfield_contract_step(int rule, const float* x, int n, int64_t 
   int32_t* sel = static_cast<int32_t*>(scratch);
   const int rounds = rule == GARFIELD_RULE_BULYAN ? q - 2 * f
                      : rule == GARFIELD_RULE_MULTIKRUM_ITERATED ? m : 0;
-  hipError_t e = enqueue_peer_select(ds, n, peers, q, f, m, rounds, k, sel, s);
+  hipError_t e = rule == GARFIELD_RULE_MDA ? enqueue_peer_mda(ds, n, peers, q, f, sel, s)
+                 : enqueue_peer_select(ds, n, peers, q, f, m, rounds, k, sel, s);
   if (e != hipSuccess) return to_status(e);
   if (rule == GARFIELD_RULE_BULYAN) return to_status(enqueue_bulyan_nodes(x, n, d, n, q, f, sel, y, s));
   return to_status(enqueue_mean_nodes(x, n, d, n, sel, k, y, s));

@@ -96,6 +96,10 @@ hipError_t enqueue_bulyan_table(const float* const* ptrs, int n, int f, const in
 // iterated Krum, else one-shot Multi-Krum with m. Aggregation: row v of y.
 hipError_t enqueue_peer_select(const DistSums& ds, int nodes, const int32_t* peers, int q, int f,
                                int m, int rounds, int kout, int32_t* sel, hipStream_t s);
+// MDA per node: sel[v*(q-f) ..] = the rows of node v's least-diameter subset
+// of q-f peers (C(q, f) subsets searched by one workgroup), ascending.
+hipError_t enqueue_peer_mda(const DistSums& ds, int nodes, const int32_t* peers, int q, int f,
+                            int32_t* sel, hipStream_t s);
 hipError_t enqueue_mean_nodes(const float* x, int n, int64_t d, int nodes, const int32_t* rows,
                               int k, float* y, hipStream_t s);
 hipError_t enqueue_median_nodes(const float* x, int n, int64_t d, int nodes, const int32_t* rows,

@@ -252,49 +252,41 @@ __device__ void unrank_subset(int64_t rank, int n, int s, Idx idx) {
   }
 }
 
-__global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64_t total,
-                                                       int64_t per, double* __restrict__ bdiam,
-                                                       int64_t* __restrict__ brank) {
-  __shared__ double D[kNmax * kNmax];
-  __shared__ unsigned char idx_all[kNmax * kBlock];  // position a of thread t at a*kBlock + t
-  __shared__ double rd[kBlock];
-  __shared__ int64_t rr[kBlock];
-  const int n = ds.n;
-  load_dist(ds, D);
-  const StridedIdx idx{idx_all + threadIdx.x};
-  const int64_t g = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  const int64_t r0 = g * per;
-  const int64_t r1 = (r0 + per < total) ? r0 + per : total;
-  double best = __builtin_inf();
-  int64_t best_r = INT64_MAX;
-  if (r0 < total) {
-    unrank_subset(r0, n, s, idx);
-    for (int64_t r = r0; r < r1; ++r) {
-      double diam = 0.0;
-      for (int a = 0; a < s; ++a) {
-        const double* row = D + idx[a] * n;
-        for (int b = a + 1; b < s; ++b) {
-          const double v = row[idx[b]];
-          diam = v > diam ? v : diam;
-        }
+// Scan ranks [r0, r1) of the s-subsets of {0..n-1} (D: n x n in LDS), keeping
+// the first strictly smaller diameter: *best, *best_r (unchanged if r0 >= r1).
+__device__ void mda_scan(const double* D, int n, int s, int64_t r0, int64_t r1, StridedIdx idx,
+                         double* best, int64_t* best_r) {
+  if (r0 >= r1) return;
+  unrank_subset(r0, n, s, idx);
+  for (int64_t r = r0; r < r1; ++r) {
+    double diam = 0.0;
+    for (int a = 0; a < s; ++a) {
+      const double* row = D + idx[a] * n;
+      for (int b = a + 1; b < s; ++b) {
+        const double v = row[idx[b]];
+        diam = v > diam ? v : diam;
       }
-      if (diam < best) {
-        best = diam;
-        best_r = r;
-      }
-      // lexicographic successor
-      int t = s - 1;
-      while (t >= 0 && idx[t] == n - s + t) --t;
-      if (t < 0) break;
-      idx[t] = static_cast<unsigned char>(idx[t] + 1);
-      for (int u = t + 1; u < s; ++u) idx[u] = static_cast<unsigned char>(idx[u - 1] + 1);
     }
+    if (diam < *best) {
+      *best = diam;
+      *best_r = r;
+    }
+    // lexicographic successor
+    int t = s - 1;
+    while (t >= 0 && idx[t] == n - s + t) --t;
+    if (t < 0) break;
+    idx[t] = static_cast<unsigned char>(idx[t] + 1);
+    for (int u = t + 1; u < s; ++u) idx[u] = static_cast<unsigned char>(idx[u - 1] + 1);
   }
-  rd[threadIdx.x] = best;
-  rr[threadIdx.x] = best_r;
+}
+
+// Minimum (diameter, rank) over the kBlock threads' candidates by a tree (the
+// minimum of such pairs does not depend on the order of the comparisons);
+// every thread receives it.
+__device__ void block_min_pair(double* rd, int64_t* rr, double* best, int64_t* best_r) {
+  rd[threadIdx.x] = *best;
+  rr[threadIdx.x] = *best_r;
   __syncthreads();
-  // minimum (diameter, rank) of the block by a tree (the minimum of such pairs
-  // does not depend on the order of the comparisons)
   for (int h = kBlock / 2; h > 0; h >>= 1) {
     if (static_cast<int>(threadIdx.x) < h) {
       const int o = threadIdx.x + h;
@@ -305,10 +297,70 @@ __global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64
     }
     __syncthreads();
   }
+  *best = rd[0];
+  *best_r = rr[0];
+}
+
+__global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64_t total,
+                                                       int64_t per, double* __restrict__ bdiam,
+                                                       int64_t* __restrict__ brank) {
+  __shared__ double D[kNmax * kNmax];
+  __shared__ unsigned char idx_all[kNmax * kBlock];  // position a of thread t at a*kBlock + t
+  __shared__ double rd[kBlock];
+  __shared__ int64_t rr[kBlock];
+  const int n = ds.n;
+  load_dist(ds, D);
+  const int64_t g = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int64_t r0 = g * per;
+  const int64_t r1 = (r0 + per < total) ? r0 + per : total;
+  double best = __builtin_inf();
+  int64_t best_r = INT64_MAX;
+  mda_scan(D, n, s, r0, r1, StridedIdx{idx_all + threadIdx.x}, &best, &best_r);
+  block_min_pair(rd, rr, &best, &best_r);
   if (threadIdx.x == 0) {
-    bdiam[blockIdx.x] = rd[0];
-    brank[blockIdx.x] = rr[0];
+    bdiam[blockIdx.x] = best;
+    brank[blockIdx.x] = best_r;
   }
+}
+
+// Contraction with MDA: workgroup v searches the C(q, f) subsets of its q
+// peers (positions in the peer list, distances gathered as k_peer_select
+// gathers them) for the least diameter, ties to the lowest lexicographic rank
+// of positions, and writes the s = q - f chosen rows to sel[v*s ..] as
+// input-row indices, ascending.
+__global__ __launch_bounds__(kBlock) void k_peer_mda(DistSums ds, const int32_t* __restrict__ peers,
+                                                     int q, int f, int64_t total,
+                                                     int32_t* __restrict__ sel) {
+  __shared__ double D[kNmax * kNmax];
+  __shared__ unsigned char idx_all[kNmax * kBlock];
+  __shared__ double rd[kBlock];
+  __shared__ int64_t rr[kBlock];
+  __shared__ int32_t map[kNmax];
+  const int v = blockIdx.x, s = q - f;
+  if (static_cast<int>(threadIdx.x) < q) {
+    const int r = peers[static_cast<int64_t>(v) * q + threadIdx.x];
+    map[threadIdx.x] = r < 0 ? 0 : (r >= ds.n ? ds.n - 1 : r);
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < q * q; idx += blockDim.x) {
+    const int a = idx / q, b = idx % q;
+    D[idx] = a == b ? 0.0 : dist_entry(ds, map[a], map[b]);
+  }
+  __syncthreads();
+  const int64_t per = (total + kBlock - 1) / kBlock;
+  const int64_t r0 = static_cast<int64_t>(threadIdx.x) * per;
+  const int64_t r1 = (r0 + per < total) ? r0 + per : total;
+  double best = __builtin_inf();
+  int64_t best_r = INT64_MAX;
+  mda_scan(D, q, s, r0, r1, StridedIdx{idx_all + threadIdx.x}, &best, &best_r);
+  block_min_pair(rd, rr, &best, &best_r);
+  __shared__ unsigned char win[kNmax];
+  if (threadIdx.x == 0) unrank_subset(best_r, q, s, win);
+  __syncthreads();
+  if (threadIdx.x >= 64) return;  // no barrier follows; wave 0 stays whole
+  uint64_t mask = 0;
+  for (int t = 0; t < s; ++t) mask |= uint64_t{1} << win[t];
+  write_selected(mask, q, map, sel + static_cast<int64_t>(v) * s);
 }
 
 __global__ __launch_bounds__(64) void k_mda_pick(const double* __restrict__ bdiam,
@@ -382,6 +434,14 @@ hipError_t enqueue_peer_select(const DistSums& ds, int nodes, const int32_t* pee
                                int m, int rounds, int kout, int32_t* sel, hipStream_t s) {
   launch("peer_select", k_peer_select, dim3(nodes), dim3(kBlock), 0, s, ds, peers, q, f, m, rounds,
          kout, sel);
+  return hipGetLastError();
+}
+
+hipError_t enqueue_peer_mda(const DistSums& ds, int nodes, const int32_t* peers, int q, int f,
+                            int32_t* sel, hipStream_t s) {
+  const int64_t total = binomial(q, f);
+  if (total < 1) return hipErrorInvalidValue;
+  launch("peer_mda", k_peer_mda, dim3(nodes), dim3(kBlock), 0, s, ds, peers, q, f, total, sel);
   return hipGetLastError();
 }
 

@@ -51,13 +51,16 @@ def _pinned_nodes(rule, x, peers, f, m, B):
             res = (oracle.bulyan(xs, f, return_rounds=True) if rule == "bulyan"
                    else oracle.multikrum_iterated(xs, f, m, return_rounds=True))
             ok.append(parity.bulyan_pinned(res[2], res[3], Ds, Bs, len(p), f, same)[0])
+        elif rule == "mda":
+            _, sel = oracle.mda(xs, f)
+            ok.append(parity.mda_pinned(Ds, Bs, len(p), f, sel)[0])
         else:
             ok.append(True)
     return ok
 
 
 CASES = [("average", 0, None), ("median", 3, None), ("krum", 2, None), ("multikrum", 2, 5),
-         ("multikrum_iterated", 2, 5), ("bulyan", 2, None)]
+         ("multikrum_iterated", 2, 5), ("bulyan", 2, None), ("mda", 2, None)]
 
 
 @pytest.mark.parametrize("n,q,d", [(12, 11, 5003), (20, 15, 4097), (40, 23, 3001)])
@@ -84,7 +87,7 @@ def test_step_matches_the_oracle(rule, f, m, n, q, d):
 
 
 @pytest.mark.parametrize("rule,f", [("multikrum", 2), ("bulyan", 2), ("median", 3), ("krum", 1),
-                                    ("multikrum_iterated", 2), ("average", 0)])
+                                    ("multikrum_iterated", 2), ("average", 0), ("mda", 2)])
 @pytest.mark.parametrize("n", [11, 33])
 def test_all_peers_in_order_equal_the_plain_rule(rule, f, n):
     if rule == "bulyan" and n < 4 * f + 3:
@@ -123,8 +126,29 @@ def test_invalid_arguments_are_rejected():
     assert e.value.code == gf.EINVAL
     p = torch.arange(5, dtype=torch.int32, device=DEV).repeat(6, 1)
     with pytest.raises(gf.GarfieldError) as e:
-        gf.contract_step("mda", x, p, 1)
+        gf.contract_step("dist", x, p, 1)
     assert e.value.code == gf.EINVAL
     with pytest.raises(gf.GarfieldError) as e:
         gf.contract_step("krum", x, p, 2)  # q = 5 < 2f+3
     assert e.value.code == gf.EREQ
+    x = torch.zeros((30, 10), dtype=torch.float32, device=DEV)
+    p = torch.arange(30, dtype=torch.int32, device=DEV).repeat(30, 1)
+    with pytest.raises(gf.GarfieldError) as e:
+        gf.contract_step("mda", x, p, 8)  # C(30, 8) subsets per node, above the per-node cap
+    assert e.value.code == gf.ETOOBIG
+
+
+def test_mda_small_integer_ties():
+    # exact distances: many equal diameters, the first subset of positions wins
+    rng = np.random.default_rng(9)
+    for trial in range(10):
+        n = int(rng.integers(5, 16))
+        q = int(rng.integers(3, n + 1))
+        f = int(rng.integers(0, (q - 1) // 2 + 1))
+        x = rng.integers(-2, 3, size=(n, 33)).astype(np.float32)
+        peers = np.stack([rng.permutation(n)[:q] for _ in range(n)]).astype(np.int32)
+        y = gf.contract_step("mda", torch.from_numpy(x).to(DEV), torch.from_numpy(peers).to(DEV), f)
+        want, want_sel = oracle.contract_step("mda", x, peers, f)
+        got = y.cpu().numpy()
+        for v in range(n):  # exact sums of small integers: equal iff the same rows were taken
+            assert np.array_equal(got[v], want[v]), (trial, n, q, f, v, want_sel[v])

@@ -69,6 +69,7 @@ def test_all_peers_in_order_reduce_to_the_rule():
     x = rng.standard_normal((n, d)).astype(np.float32)
     peers = np.tile(np.arange(n, dtype=np.int32), (n, 1))
     for rule, fn in (("multikrum", lambda: oracle.multikrum(x, f)),
+                     ("mda", lambda: oracle.mda(x, f)),
                      ("bulyan", lambda: oracle.bulyan(np.ascontiguousarray(x[:9]), 1))):
         if rule == "bulyan":
             y, sel = oracle.contract_step(rule, x[:9], peers[:9, :9], 1)
