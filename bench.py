@@ -92,6 +92,41 @@ def calibrate_copy(args):
             "steps": args.steps}
 
 
+def measured_ceiling(steps=20):
+    """What this GPU streams in practice, as a yardstick for the kernels'
+    achieved bandwidth (the roofline fraction stays against the 8 TB/s peak):
+    the library's plain streaming read (garfield_tuning_stream_read) and torch's
+    device copy, each over 1 GiB, timed with events after three warm-up runs."""
+    import torch
+
+    import paper_2010_05888_amd as gf
+
+    nbytes = 1 << 30
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    dst = torch.empty_like(src)
+    sums = torch.empty(gf.STREAM_READ_BLOCKS, dtype=torch.float32, device="cuda:0")
+    out = {}
+    for name, fn, moved in (("read_GBps", lambda: gf.stream_read(src, sums), nbytes),
+                            ("copy_GBps", lambda: dst.copy_(src), 2 * nbytes)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        out[name] = round(moved / (a.elapsed_time(b) / steps * 1e-3) / 1e9, 1)
+    if abs(float(sums.double().sum()) - nbytes / 4) > 1e-3 * nbytes / 4:
+        raise RuntimeError("streaming read returned a wrong sum")
+    out["how"] = ("1 GiB: garfield_tuning_stream_read (16-byte nontemporal loads, 512 "
+                  "workgroups grid-stride); torch copy_ (read + write counted)")
+    del src, dst
+    torch.cuda.empty_cache()
+    return out
+
+
 class Step:
     """One aggregation step of a workload with preallocated outputs."""
 
@@ -322,6 +357,10 @@ def bench_workload(key, args):
         roofline["achieved"] = round(achieved, 2)
         roofline["frac"] = round(achieved / HBM_PEAK_GBS, 4)
 
+    ceiling = measured_ceiling()
+    if roofline["achieved"]:
+        roofline["frac_of_measured_read"] = round(roofline["achieved"] / ceiling["read_GBps"], 4)
+
     base = None
     if args.cpu_seconds > 0:
         print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)
@@ -352,6 +391,7 @@ def bench_workload(key, args):
                    "input_copies": len(copies)},
         "kernels": kernels,
         "roofline": roofline,
+        "measured_ceiling": ceiling,
         "cpu_baseline": base,
     }
     del x, inp, steps, copies

@@ -50,6 +50,18 @@ int garfield_tuning_set_kernel_timing(int on);
  */
 size_t garfield_tuning_kernel_timing(char* buf, size_t len);
 
+/*
+ * Plain streaming read, the yardstick the aggregation kernels' bandwidth is
+ * read against: GARFIELD_TUNING_READ_BLOCKS workgroups of 256 lanes walk the
+ * `count` fp32 values at x (device) grid-stride, each lane with four 16-byte
+ * nontemporal loads in flight, and write each workgroup's fp32 sum to
+ * sums[0 .. GARFIELD_TUNING_READ_BLOCKS-1] (device). x must be 16-byte
+ * aligned and count a multiple of 4 (else GARFIELD_EINVAL and nothing is
+ * enqueued). Asynchronous on `stream`; returns a garfield_status.
+ */
+#define GARFIELD_TUNING_READ_BLOCKS 512
+int garfield_tuning_stream_read(const float* x, long long count, float* sums, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

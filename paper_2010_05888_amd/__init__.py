@@ -23,7 +23,7 @@ __all__ = [
     "pairwise_sqdist", "krum", "multikrum", "multikrum_iterated", "median", "bulyan", "mda",
     "average",
     "multikrum_median", "gar", "workspace_bytes", "release", "set_direct_max_n",
-    "distance_engine", "gram_reference", "set_kernel_timing", "kernel_timing", "RULES",
+    "distance_engine", "gram_reference", "stream_read", "set_kernel_timing", "kernel_timing", "RULES",
     "ATTACKS", "attack", "variance_stats", "delta", "variance_condition", "Segmented",
     "SegmentTable", "contract_step", "contract",
 ]
@@ -118,6 +118,8 @@ def load():
     lib.garfield_tuning_distance_engine.restype = i32
     lib.garfield_tuning_gram_reference.argtypes = [vp, i32, ctypes.c_longlong, vp]
     lib.garfield_tuning_gram_reference.restype = i32
+    lib.garfield_tuning_stream_read.argtypes = [vp, ctypes.c_longlong, vp, vp]
+    lib.garfield_tuning_stream_read.restype = i32
     lib.garfield_tuning_set_kernel_timing.argtypes = [i32]
     lib.garfield_tuning_set_kernel_timing.restype = i32
     lib.garfield_tuning_kernel_timing.argtypes = [ctypes.c_char_p, ctypes.c_size_t]
@@ -532,6 +534,23 @@ def gram_reference(x: torch.Tensor) -> int:
     if ref < 0:
         raise GarfieldError(EHIP, "garfield_tuning_gram_reference", "probe failed")
     return ref
+
+
+STREAM_READ_BLOCKS = 512  # GARFIELD_TUNING_READ_BLOCKS
+
+
+def stream_read(x: torch.Tensor, sums: torch.Tensor | None = None) -> torch.Tensor:
+    """The plain streaming read of garfield_tuning_stream_read over the
+    contiguous fp32 tensor x (16-byte aligned, numel % 4 == 0): returns the
+    STREAM_READ_BLOCKS per-workgroup fp32 sums (a bandwidth yardstick)."""
+    if not isinstance(x, torch.Tensor) or x.dtype != torch.float32 or not x.is_cuda \
+            or not x.is_contiguous():
+        raise ValueError("x must be a contiguous float32 device tensor")
+    if sums is None:
+        sums = torch.empty(STREAM_READ_BLOCKS, dtype=torch.float32, device=x.device)
+    _check(load().garfield_tuning_stream_read(_ptr(x), x.numel(), _ptr(sums), _stream(x)),
+           "garfield_tuning_stream_read")
+    return sums
 
 
 def set_kernel_timing(on: bool) -> bool:

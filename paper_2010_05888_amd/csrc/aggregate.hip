@@ -176,4 +176,44 @@ hipError_t enqueue_bulyan_aggregate(const float* x, int n, int f, int64_t d, con
   return bulyan_dispatch<1>(theta, beta, stream_width(x, out), x, n, d, sel, out, s);
 }
 
+namespace {
+
+// Read-rate probe: workgroup b sums the float4s b*kBlock*4 + t + u*kBlock
+// (u < 4), then the same a grid's worth further on, with nontemporal loads,
+// and writes the workgroup's fp32 total.
+__global__ __launch_bounds__(kBlock) void k_stream_read(const f4* __restrict__ x, int64_t m,
+                                                        float* __restrict__ sums) {
+  constexpr int U = 4;
+  __shared__ float red[kBlock];
+  float acc = 0.0f;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * U;
+  for (int64_t base = static_cast<int64_t>(blockIdx.x) * kBlock * U + threadIdx.x; base < m;
+       base += stride) {
+    f4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + static_cast<int64_t>(u) * kBlock;
+      v[u] = i < m ? __builtin_nontemporal_load(x + i) : f4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc += (v[u].x + v[u].y) + (v[u].z + v[u].w);
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int h = kBlock / 2; h > 0; h >>= 1) {
+    if (static_cast<int>(threadIdx.x) < h) red[threadIdx.x] += red[threadIdx.x + h];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) sums[blockIdx.x] = red[0];
+}
+
+}  // namespace
+
+hipError_t enqueue_stream_read(const float* x, int64_t count, int blocks, float* sums,
+                               hipStream_t s) {
+  launch("stream_read", k_stream_read, dim3(blocks), dim3(kBlock), 0, s,
+         reinterpret_cast<const f4*>(x), count / 4, sums);
+  return hipGetLastError();
+}
+
 }  // namespace garfield

@@ -604,6 +604,14 @@ int garfield_tuning_set_kernel_timing(int on) {
 
 size_t garfield_tuning_kernel_timing(char* buf, size_t len) { return timing_summary(buf, len); }
 
+int garfield_tuning_stream_read(const float* x, long long count, float* sums, void* stream) {
+  if (!x || !sums || count < 0 || count % 4 != 0 || reinterpret_cast<uintptr_t>(x) % 16 != 0 ||
+      reinterpret_cast<uintptr_t>(sums) % sizeof(float) != 0)
+    return GARFIELD_EINVAL;
+  return to_status(enqueue_stream_read(x, count, GARFIELD_TUNING_READ_BLOCKS, sums,
+                                       static_cast<hipStream_t>(stream)));
+}
+
 int garfield_tuning_distance_engine(int n, long long d) {
   if (n < 1 || n > GARFIELD_NMAX || d < 0) return -1;
   const float* aligned = reinterpret_cast<const float*>(uintptr_t{256});

@@ -128,6 +128,10 @@ hipError_t enqueue_mda_select(const DistSums& ds, int f, void* scratch, int32_t*
 // Streaming aggregation kernels over the coordinates.
 // Row lists are device int32 arrays (nullptr = rows 0..k-1); an entry outside
 // [0, n) is clamped into it, so a bad list cannot make a kernel read outside x.
+// Read-rate probe (aggregate.hip): `blocks` workgroups sum the count floats
+// at x (16-byte aligned, count % 4 == 0) grid-stride; sums[b] = workgroup b's.
+hipError_t enqueue_stream_read(const float* x, int64_t count, int blocks, float* sums,
+                               hipStream_t s);
 hipError_t enqueue_mean_rows(const float* x, int n, int64_t d, const int32_t* rows, int k,
                              float* out, hipStream_t s);
 hipError_t enqueue_median(const float* x, int n, int64_t d, const int32_t* rows, int k,

@@ -218,12 +218,24 @@ __global__ __launch_bounds__(kBlock) void k_peer_select(DistSums ds,
 // scans ranks [g*per, (g+1)*per) with a successor step, keeping the first
 // strictly smaller diameter; blocks then take the minimum (diameter, rank).
 
-__device__ int64_t binom_dev(int a, int b) {
-  if (b < 0 || b > a) return 0;
-  if (b > a - b) b = a - b;
-  int64_t c = 1;
-  for (int t = 1; t <= b; ++t) c = c * (a - b + t) / t;
-  return c;
+// C(a, b) for 0 <= b <= a <= kNmax (C(64, 32) < 2^61), Pascal's triangle
+// built at compile time and read from constant memory: unranking takes no
+// 64-bit divisions.
+struct BinomTable {
+  int64_t c[kNmax + 1][kNmax + 1];
+};
+constexpr BinomTable make_binom_table() {
+  BinomTable t{};
+  for (int a = 0; a <= kNmax; ++a) {
+    t.c[a][0] = 1;
+    for (int b = 1; b <= a; ++b) t.c[a][b] = t.c[a - 1][b - 1] + (b < a ? t.c[a - 1][b] : 0);
+  }
+  return t;
+}
+__constant__ BinomTable kBinom = make_binom_table();
+
+__device__ __forceinline__ int64_t binom_dev(int a, int b) {
+  return (b < 0 || b > a) ? 0 : kBinom.c[a][b];
 }
 
 // A thread's subset indices in LDS, position a at a stride of kBlock bytes

@@ -443,3 +443,18 @@ def test_invalid_arguments_are_rejected():
         with pytest.raises(gf.GarfieldError) as e:
             fn()
         assert e.value.code == code
+
+
+def test_stream_read_yardstick():
+    # the bandwidth yardstick bench.py reports beside the roofline: exact sums of
+    # small integers, and its argument checks
+    x = torch.arange(4 * 100003, dtype=torch.float32, device=DEV) % 7
+    sums = gf.stream_read(x)
+    assert sums.shape == (gf.STREAM_READ_BLOCKS,)
+    assert float(sums.double().sum()) == float(x.double().sum())
+    with pytest.raises(gf.GarfieldError) as e:
+        gf.stream_read(x[1:5])  # 4-byte offset
+    assert e.value.code == gf.EINVAL
+    with pytest.raises(gf.GarfieldError) as e:
+        gf.stream_read(x[:6])  # not a multiple of 4
+    assert e.value.code == gf.EINVAL
