@@ -619,8 +619,12 @@ hipError_t enqueue_reference(const float* x, const DistPlan& p, const DistWorksp
   return hipGetLastError();
 }
 
+bool foldable(const DistPlan& p, int max_entries) {
+  return p.engine == kEngineDirect && p.tiles <= kFoldTiles && p.entries <= max_entries;
+}
+
 hipError_t enqueue_distances(const float* x, const DistPlan& p, const DistWorkspace& ws,
-                             hipStream_t s) {
+                             hipStream_t s, bool sum_tiles) {
   hipError_t e = hipSuccess;
   if (p.engine == kEngineNone) return hipSuccess;  // D is all zeros: nothing to compute
   if (p.engine == kEngineDirect) {
@@ -636,7 +640,7 @@ hipError_t enqueue_distances(const float* x, const DistPlan& p, const DistWorksp
       default: return hipErrorInvalidValue;
     }
   }
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || !sum_tiles) return e;
   launch("sum_tiles", k_sum_tiles, dim3(p.entries), dim3(kBlock), 0, s, ws.partial, p.tiles,
     ws.sums);
   return hipGetLastError();

@@ -16,10 +16,16 @@ namespace garfield {
 //    q-th block pair (b1 <= b2) of the upper block triangle, G = Y Y^T;
 //  * no engine (n < 2 or d == 0): D is all zeros;
 //  * matrix: sums is the full n x n fp64 matrix D, row-major.
+// Folded (direct engine with at most kFoldTiles tiles): sums is not formed;
+// partial[entry * tiles + tile] holds the tiles' partial sums, and load_dist
+// adds them exactly as the tile-sum kernel would (only load_dist reads this
+// form).
 struct DistSums {
   const double* sums;
   int engine;
   int n;
+  const double* partial = nullptr;
+  int64_t tiles = 0;
 };
 
 __device__ __forceinline__ int direct_entry(int n, int i, int j) {  // i < j
@@ -50,7 +56,47 @@ __device__ __forceinline__ double dist_entry(const DistSums& ds, int i, int j) {
 // takes one load; D[i][j] is formed exactly as dist_entry forms it.
 __device__ __forceinline__ void load_dist(const DistSums& ds, double* D) {
   const int n = ds.n;
-  if (ds.engine == kEngineGram) {
+  if (ds.partial) {
+    // Entry e is the sum of tiles t = 0 .. tiles-1 in the tile-sum kernel's
+    // order: slot u (< 256) holds tile u, then slots u and u + h are added for
+    // h = 128, 64, ..., 1. Lane l of a wave holds slots l, l+64, l+128, l+192
+    // and adds them as the levels 128 and 64 do; the xor butterfly from 32
+    // down to 1 is the rest of the tree at lane 0 (for l < h, l ^ h = l + h).
+    // A wave takes four entries at a time, all their loads issued first.
+    __shared__ double esum[kDirectMaxNLimit * (kDirectMaxNLimit - 1) / 2];
+    const int P = n * (n - 1) / 2;
+    const int lane = threadIdx.x & 63, waves = blockDim.x >> 6;
+    const int64_t t = ds.tiles;
+    for (int e0 = threadIdx.x >> 6; e0 < P; e0 += 4 * waves) {
+      double v[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = e0 + k * waves;  // wave-uniform
+        if (e < P) {
+          const double* row = ds.partial + static_cast<int64_t>(e) * t;
+          const double s0 = lane < t ? row[lane] : 0.0;
+          const double s1 = lane + 64 < t ? row[lane + 64] : 0.0;
+          const double s2 = lane + 128 < t ? row[lane + 128] : 0.0;
+          const double s3 = lane + 192 < t ? row[lane + 192] : 0.0;
+          v[k] = (s0 + s2) + (s1 + s3);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = e0 + k * waves;
+        if (e < P) {
+#pragma unroll
+          for (int m = 32; m > 0; m >>= 1) v[k] += __shfl_xor(v[k], m, 64);
+          if (lane == 0) esum[e] = v[k];
+        }
+      }
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < n * n; idx += blockDim.x) {
+      const int i = idx / n, j = idx % n;
+      D[idx] = i == j ? 0.0 : esum[direct_entry(n, i < j ? i : j, i < j ? j : i)];
+    }
+  } else if (ds.engine == kEngineGram) {
     __shared__ double diag[kNmax];
     const int nb = (n + 15) / 16;
     if (static_cast<int>(threadIdx.x) < n) diag[threadIdx.x] = ds.sums[gram_entry(nb, threadIdx.x, threadIdx.x)];

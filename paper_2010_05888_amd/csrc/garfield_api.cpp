@@ -72,8 +72,14 @@ garfield_status check_common(const float* x, int n, int f, int64_t d) {
 // Distance step into the workspace. *ds receives the entry sums (valid once
 // the stream reaches the end of the step). `extra` bytes of scratch follow
 // the distance workspace and are returned in *extra_ptr.
+// fold_entries > 0: the consumer is a selection kernel of fold_entries / 4
+// waves that reads D through load_dist, so a direct-engine step with few
+// tiles and at most fold_entries entries skips the tile-sum kernel (the
+// selection kernel adds the tiles in the same order).
+constexpr int kFoldSelect = 4 * 16;  // k_krum_select, k_bulyan_select: 16 waves
+constexpr int kFoldMda = 4 * 4;      // k_mda_search: 4 waves
 garfield_status run_distances(const float* x, int n, int64_t d, size_t extra, DistSums* ds,
-                              void** extra_ptr, hipStream_t s) {
+                              void** extra_ptr, hipStream_t s, int fold_entries = 0) {
   const DistPlan plan = plan_distances(n, d, x);
   const size_t dist_bytes = dist_workspace_bytes(plan);
   void* base = nullptr;
@@ -82,7 +88,12 @@ garfield_status run_distances(const float* x, int n, int64_t d, size_t extra, Di
   const DistWorkspace ws = carve_dist_workspace(plan, base);
   *ds = dist_sums(plan, ws);
   if (extra_ptr) *extra_ptr = static_cast<char*>(base) + dist_bytes;
-  return to_status(enqueue_distances(x, plan, ws, s));
+  const bool fold = fold_entries > 0 && foldable(plan, fold_entries);
+  if (fold) {
+    ds->partial = ws.partial;
+    ds->tiles = plan.tiles;
+  }
+  return to_status(enqueue_distances(x, plan, ws, s, !fold));
 }
 
 // Requirements of `rule` (Section 3.1) and the number of indices it selects
@@ -165,7 +176,7 @@ garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int 
   if (m > n - f) return GARFIELD_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   DistSums ds;
-  st = run_distances(x, n, d, 0, &ds, nullptr, s);
+  st = run_distances(x, n, d, 0, &ds, nullptr, s, kFoldSelect);
   if (st != GARFIELD_OK) return st;
   st = to_status(enqueue_krum_select(ds, f, m, sel, s));
   if (st != GARFIELD_OK || !out) return st;
@@ -187,7 +198,7 @@ garfield_status garfield_multikrum_iterated(const float* x, int n, int f, int64_
   if (m > n - f) return GARFIELD_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   DistSums ds;
-  st = run_distances(x, n, d, 0, &ds, nullptr, s);
+  st = run_distances(x, n, d, 0, &ds, nullptr, s, kFoldSelect);
   if (st != GARFIELD_OK) return st;
   st = to_status(enqueue_krum_rounds(ds, f, m, sel, s));
   if (st != GARFIELD_OK || !out) return st;
@@ -216,7 +227,7 @@ garfield_status garfield_bulyan(const float* x, int n, int f, int64_t d, float* 
   if (n < 4 * f + 3) return GARFIELD_EREQ;
   hipStream_t s = static_cast<hipStream_t>(stream);
   DistSums ds;
-  st = run_distances(x, n, d, 0, &ds, nullptr, s);
+  st = run_distances(x, n, d, 0, &ds, nullptr, s, kFoldSelect);
   if (st != GARFIELD_OK) return st;
   st = to_status(enqueue_bulyan_select(ds, f, sel, s));
   if (st != GARFIELD_OK) return st;
@@ -234,7 +245,7 @@ garfield_status garfield_mda(const float* x, int n, int f, int64_t d, float* out
   hipStream_t s = static_cast<hipStream_t>(stream);
   void* scratch = nullptr;
   DistSums ds;
-  st = run_distances(x, n, d, mda_scratch_bytes(n, f), &ds, &scratch, s);
+  st = run_distances(x, n, d, mda_scratch_bytes(n, f), &ds, &scratch, s, kFoldMda);
   if (st != GARFIELD_OK) return st;
   st = to_status(enqueue_mda_select(ds, f, scratch, sel, s));
   if (st != GARFIELD_OK || !out) return st;

@@ -55,9 +55,16 @@ hipError_t enqueue_reference(const float* x, const DistPlan& p, const DistWorksp
                              hipStream_t s);
 
 // Enqueue the distance step; when the stream reaches its end, ws.sums holds
-// one fp64 sum per entry (see dist_layout.h for how they map to D).
+// one fp64 sum per entry (see dist_layout.h for how they map to D). With
+// sum_tiles false only the tiles' partials are written (the folded form).
 hipError_t enqueue_distances(const float* x, const DistPlan& p, const DistWorkspace& ws,
-                             hipStream_t s);
+                             hipStream_t s, bool sum_tiles = true);
+// Direct-engine plans with at most kFoldTiles tiles and max_entries entries
+// may leave the tile sums to the selection kernel (DistSums' folded form):
+// its waves add four entries at a time, so a workgroup of w waves folds up to
+// 4w entries in one round of loads.
+constexpr int64_t kFoldTiles = 256;
+bool foldable(const DistPlan& p, int max_entries);
 DistSums dist_sums(const DistPlan& p, const DistWorkspace& ws);
 // Write D (n x n fp64, device) from the entry sums.
 hipError_t enqueue_write_dist(const DistSums& ds, double* dist, hipStream_t s);
