@@ -296,10 +296,13 @@ garfield_status garfield_seg_destroy(garfield_segmented* seg);
  *   garfield_seg_aggregate_table(seg, ptrs, dims, K, outs, stream)   aggregates
  *       every segment with the session's selection; outs (HOST array of K
  *       DEVICE pointers, each to dims[s] fp32 values, 4-byte aligned).
- * Requires n <= 20 (the direct distance engine's limit; GARFIELD_ETOOBIG
- * otherwise). Results equal those of garfield_seg_accumulate /
- * garfield_seg_aggregate on the same segments held as n x d matrices, except
- * that the distances come from the direct engine for every n <= 20.
+ * Distances: the direct engine for n <= 20, else the Gram engine over the
+ * table (one reference row, probed on the longest segment, for every
+ * segment). Results equal those of garfield_seg_accumulate /
+ * garfield_seg_aggregate on the same segments held as n x d matrices for
+ * n <= 20 (whatever the engine threshold); for n > 20 the distances differ
+ * from the matrix sessions' only by rounding (the Gram engine's bound). A
+ * launch takes at most 2^31 - 1 workgroups or stages (GARFIELD_ETOOBIG).
  */
 garfield_status garfield_seg_accumulate_table(garfield_segmented* seg, const float* const* ptrs,
                                               const int64_t* dims, int K, void* stream);

@@ -34,6 +34,13 @@ int garfield_tuning_distance_engine(int n, long long d);
  * on error. Lets tests bound the Gram engine's cancellation error. */
 int garfield_tuning_gram_reference(const float* x, int n, long long d, void* stream);
 
+/* The same for a segment table of n vectors (ptrs: DEVICE, K*n pointers;
+ * dims: HOST, K lengths, as garfield_seg_accumulate_table takes them) with
+ * n > 20, whose Gram engine probes the longest segment (the first of equal
+ * ones). Returns -1 on error or when every segment is empty. */
+int garfield_tuning_table_gram_reference(const float* const* ptrs, int n, const long long* dims,
+                                         int K, void* stream);
+
 /*
  * Per-kernel timing. While on, every kernel a call launches is launched with
  * a pair of HIP events that the runtime stamps at the start and the end of

@@ -23,7 +23,7 @@ __all__ = [
     "pairwise_sqdist", "krum", "multikrum", "multikrum_iterated", "median", "bulyan", "mda",
     "average",
     "multikrum_median", "gar", "workspace_bytes", "release", "set_direct_max_n",
-    "distance_engine", "gram_reference", "stream_read", "set_kernel_timing", "kernel_timing", "RULES",
+    "distance_engine", "gram_reference", "table_gram_reference", "stream_read", "set_kernel_timing", "kernel_timing", "RULES",
     "ATTACKS", "attack", "variance_stats", "delta", "variance_condition", "Segmented",
     "SegmentTable", "contract_step", "contract",
 ]
@@ -120,6 +120,8 @@ def load():
     lib.garfield_tuning_gram_reference.restype = i32
     lib.garfield_tuning_stream_read.argtypes = [vp, ctypes.c_longlong, vp, vp]
     lib.garfield_tuning_stream_read.restype = i32
+    lib.garfield_tuning_table_gram_reference.argtypes = [vp, i32, vp, i32, vp]
+    lib.garfield_tuning_table_gram_reference.restype = i32
     lib.garfield_tuning_set_kernel_timing.argtypes = [i32]
     lib.garfield_tuning_set_kernel_timing.restype = i32
     lib.garfield_tuning_kernel_timing.argtypes = [ctypes.c_char_p, ctypes.c_size_t]
@@ -551,6 +553,17 @@ def stream_read(x: torch.Tensor, sums: torch.Tensor | None = None) -> torch.Tens
     _check(load().garfield_tuning_stream_read(_ptr(x), x.numel(), _ptr(sums), _stream(x)),
            "garfield_tuning_stream_read")
     return sums
+
+
+def table_gram_reference(table: "SegmentTable") -> int:
+    """Row the Gram engine (n > 20) shifts a segment table by (synchronises the
+    current stream)."""
+    ref = load().garfield_tuning_table_gram_reference(
+        ctypes.c_void_p(table.ptrs.data_ptr()), table.n, table._dims, table.K,
+        ctypes.c_void_p(torch.cuda.current_stream(table.device).cuda_stream))
+    if ref < 0:
+        raise GarfieldError(EHIP, "garfield_tuning_table_gram_reference", "probe failed")
+    return ref
 
 
 def set_kernel_timing(on: bool) -> bool:

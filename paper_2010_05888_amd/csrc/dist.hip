@@ -60,7 +60,8 @@ int probe_runs(int64_t d) {
   return d <= static_cast<int64_t>(kProbeRuns) * kBlock ? 1 : kProbeRuns;
 }
 
-__global__ __launch_bounds__(kBlock) void k_probe(const float* __restrict__ x, int n, int64_t d,
+template <class Src>
+__global__ __launch_bounds__(kBlock) void k_probe(Src src, int n, int64_t d,
                                                   double* __restrict__ probe) {
   const int i = blockIdx.x, r = blockIdx.y;
   float acc[kNmax];
@@ -71,11 +72,11 @@ __global__ __launch_bounds__(kBlock) void k_probe(const float* __restrict__ x, i
   const int64_t first = r * (d / runs);
   for (int64_t o = threadIdx.x; o < len; o += kBlock) {
     const int64_t c = first + o;
-    const float xi = x[static_cast<int64_t>(i) * d + c];
+    const float xi = src.row(i)[c];
 #pragma unroll
     for (int j = 0; j < kNmax; ++j) {
       if (j < n) {
-        const float t = xi - x[static_cast<int64_t>(j) * d + c];
+        const float t = xi - src.row(j)[c];
         acc[j] = __builtin_fmaf(t, t, acc[j]);
       }
     }
@@ -204,14 +205,13 @@ __device__ __forceinline__ void lds_barrier() {
 // Issue the loads of the stage at c0: this wave's rows into v, the reference
 // row into vr (coordinates at or beyond d read as 0 when the stage is the
 // partial last one).
-template <int NB, bool PAD, bool FULL>
-__device__ __forceinline__ void gram_issue(const float* __restrict__ x, int n, int64_t d,
-                                           int ref, int wave, int lane, int64_t c0, f4* v,
-                                           f4& vr) {
+template <int NB, bool PAD, bool FULL, class Src>
+__device__ __forceinline__ void gram_issue(const Src& src, int n, int64_t d, int ref, int wave,
+                                           int lane, int64_t c0, f4* v, f4& vr) {
   using S = GramShape<NB>;
   const int64_t c = c0 + 4 * lane;
   auto load = [&](int row, f4& out) {
-    const float* p = x + static_cast<int64_t>(row) * d + c;
+    const float* p = src.row(row) + c;
     float t[4];
     if constexpr (FULL) {
       load_w<4>(p, t);
@@ -333,7 +333,7 @@ __device__ __forceinline__ void gram_tile(const float* __restrict__ x, int n, in
   f4 v[S::RPW];
   f4 vr;
   if (b == G) {
-    gram_issue<NB, PAD, false>(x, n, d, ref, wave, lane, full * kGramStage, v, vr);
+    gram_issue<NB, PAD, false>(MatrixRows{x, d}, n, d, ref, wave, lane, full * kGramStage, v, vr);
     lds_barrier();
     gram_put<NB, PAD>(buf, n, wave, lane, v, vr);
     lds_barrier();
@@ -341,14 +341,40 @@ __device__ __forceinline__ void gram_tile(const float* __restrict__ x, int n, in
     return;
   }
   const int64_t mine = (full > b) ? (full - b + G - 1) / G : 0;
-  if (mine > 0) gram_issue<NB, PAD, true>(x, n, d, ref, wave, lane, b * kGramStage, v, vr);
+  if (mine > 0)
+    gram_issue<NB, PAD, true>(MatrixRows{x, d}, n, d, ref, wave, lane, b * kGramStage, v, vr);
   for (int64_t k = 0; k < mine; ++k) {
     lds_barrier();                    // every wave is done with the previous stage
     gram_put<NB, PAD>(buf, n, wave, lane, v, vr);
     if (k + 1 < mine)                 // in flight during the multiply below
-      gram_issue<NB, PAD, true>(x, n, d, ref, wave, lane, (b + (k + 1) * G) * kGramStage, v, vr);
+      gram_issue<NB, PAD, true>(MatrixRows{x, d}, n, d, ref, wave, lane,
+                                (b + (k + 1) * G) * kGramStage, v, vr);
     lds_barrier();                    // the whole stage is in LDS
     gram_multiply<NB, PH>(buf, wave & 1, g, r, acc64);
+  }
+}
+
+// Partials of a workgroup: entry q*256 + row*16 + col holds
+// G[16*b1 + row][16*b2 + col] (MFMA output: lane l, component e is row
+// 4*(l/16) + e, column l%16); the two halves of pair q are held by waves
+// 2*(q%2) (h = 0) and 2*(q%2) + 1 and added half 0 first. out[entry * stride].
+template <int NB>
+__device__ __forceinline__ void gram_write_partials(const double (*acc64)[4], float* buf, int wave,
+                                                    int g, int r, double* __restrict__ out,
+                                                    int64_t stride) {
+  using S = GramShape<NB>;
+  __syncthreads();
+  double* red = reinterpret_cast<double*>(buf);  // 2 x 256 doubles (4 KB <= buf)
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int q = 0; q < S::NBP; ++q) {
+    if ((wave >> 1) == (q & 1)) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) red[(wave & 1) * 256 + (4 * g + e) * 16 + r] = acc64[q / 2][e];
+    }
+    __syncthreads();
+    out[(q * 256 + t) * stride] = red[t] + red[256 + t];
+    __syncthreads();
   }
 }
 
@@ -369,25 +395,67 @@ void k_dist_gram(const float* __restrict__ x, int n, int64_t d,
     for (int e = 0; e < 4; ++e) acc64[i][e] = 0.0;
   if (wave < 2) gram_tile<NB, PAD, 0>(x, n, d, ref, wave, buf, acc64);
   else gram_tile<NB, PAD, 1>(x, n, d, ref, wave, buf, acc64);
+  gram_write_partials<NB>(acc64, buf, wave, g, r, partial + blockIdx.x, gridDim.x);
+}
 
-  // Partials: entry q*256 + row*16 + col holds G[16*b1 + row][16*b2 + col]
-  // (MFMA output: lane l, component e is row 4*(l/16) + e, column l%16); the
-  // two halves of pair q are held by waves 2*(q%2) (h = 0) and 2*(q%2) + 1.
-  __syncthreads();
-  double* red = reinterpret_cast<double*>(buf);  // 2 x 256 doubles (4 KB <= buf)
-  double* __restrict__ out = partial + blockIdx.x;
-  const int64_t stride = gridDim.x;
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int q = 0; q < S::NBP; ++q) {
-    if ((wave >> 1) == (q & 1)) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) red[(wave & 1) * 256 + (4 * g + e) * 16 + r] = acc64[q / 2][e];
-    }
-    __syncthreads();
-    out[(q * 256 + t) * stride] = red[t] + red[256 + t];
-    __syncthreads();
+// ---------------------------------------------------------------------------
+// The Gram engine over a table of segments (segment s of vector i at
+// ptrs[s * n + i], dims[s] floats): the stages of all segments of the launch
+// form one list (segment s owns stages tab.first[s] .. tab.first[s+1]-1, the
+// last one partial when 256 does not divide dims[s]), and workgroup b takes
+// stages b, b + G, ... of it, each with its segment's rows. One reference row
+// index serves every segment (D is the same whatever row each coordinate is
+// shifted by). Tile b of the launch writes column tile_base + b of partials
+// with `tiles` columns in all.
+template <int NB, bool PAD, int PH>
+__device__ __forceinline__ void gram_tile_table(const float* const* __restrict__ ptrs,
+                                                const SegTable& tab, int n, int ref, int wave,
+                                                float* __restrict__ buf, double (*acc64)[4]) {
+  using S = GramShape<NB>;
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, r = lane & 15;
+  const int64_t G = gridDim.x;
+  const int64_t total = tab.first[tab.count];
+  auto issue = [&](int64_t stage, f4* v, f4& vr) {
+    const int sg = seg_of(tab, static_cast<int>(stage));
+    const int64_t c0 = (stage - tab.first[sg]) * kGramStage;
+    const int64_t d = tab.dims[sg];
+    const TableRows src{ptrs + static_cast<int64_t>(sg) * n};
+    if (c0 + kGramStage <= d) gram_issue<NB, PAD, true>(src, n, d, ref, wave, lane, c0, v, vr);
+    else gram_issue<NB, PAD, false>(src, n, d, ref, wave, lane, c0, v, vr);
+  };
+  f4 v[S::RPW];
+  f4 vr;
+  int64_t stage = blockIdx.x;
+  if (stage < total) issue(stage, v, vr);
+  for (; stage < total; stage += G) {
+    lds_barrier();  // every wave is done with the previous stage
+    gram_put<NB, PAD>(buf, n, wave, lane, v, vr);
+    if (stage + G < total) issue(stage + G, v, vr);  // in flight during the multiply
+    lds_barrier();  // the whole stage is in LDS
+    gram_multiply<NB, PH>(buf, wave & 1, g, r, acc64);
   }
+}
+
+template <int NB, bool PAD>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2)))
+void k_dist_gram_table(const float* const* __restrict__ ptrs, SegTable tab, int n,
+                       const int32_t* __restrict__ ref_idx, int64_t tile_base, int64_t tiles,
+                       double* __restrict__ partial) {
+  using S = GramShape<NB>;
+  __shared__ __attribute__((aligned(16))) float buf[S::ROWS * kGramPitch];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, r = lane & 15;
+  const int ref = *ref_idx;
+  double acc64[S::PPW][4];
+#pragma unroll
+  for (int i = 0; i < S::PPW; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc64[i][e] = 0.0;
+  if (wave < 2) gram_tile_table<NB, PAD, 0>(ptrs, tab, n, ref, wave, buf, acc64);
+  else gram_tile_table<NB, PAD, 1>(ptrs, tab, n, ref, wave, buf, acc64);
+  gram_write_partials<NB>(acc64, buf, wave, g, r, partial + tile_base + blockIdx.x, tiles);
 }
 
 // ---------------------------------------------------------------------------
@@ -519,9 +587,138 @@ int gram_blocks_per_cu(int nb) {
   return c;
 }
 
+// The same for the table kernel.
+template <int NB>
+int gram_table_blocks_per_cu_nb() {
+  int blocks = 0, blocks_pad = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_dist_gram_table<NB, false>, kBlock,
+                                                   0) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks_pad, k_dist_gram_table<NB, true>,
+                                                   kBlock, 0) != hipSuccess ||
+      blocks <= 0) {
+    (void)hipGetLastError();
+    return 2;
+  }
+  return blocks < blocks_pad ? blocks : blocks_pad;
+}
+
+int gram_table_blocks_per_cu(int nb) {
+  static int cache[kGramBlocks + 1] = {};
+  int& c = cache[nb];
+  if (c == 0) {
+    switch (nb) {
+      case 1: c = gram_table_blocks_per_cu_nb<1>(); break;
+      case 2: c = gram_table_blocks_per_cu_nb<2>(); break;
+      case 3: c = gram_table_blocks_per_cu_nb<3>(); break;
+      default: c = gram_table_blocks_per_cu_nb<4>(); break;
+    }
+  }
+  return c;
+}
+
+// Launches of the table Gram kernel: at most kSegMax segments each; f(first
+// segment, table (first[] in stages), workgroups) for each launch with work.
+template <class F>
+hipError_t for_each_gram_launch(int n, const int64_t* dims, int K, F&& f) {
+  const int nb = (n + 15) / 16;
+  const int64_t slots = static_cast<int64_t>(device_cus()) * gram_table_blocks_per_cu(nb);
+  for (int g0 = 0; g0 < K; g0 += kSegMax) {
+    SegTable tab{};
+    tab.count = K - g0 < kSegMax ? K - g0 : kSegMax;
+    int64_t total = 0;
+    for (int sg = 0; sg < tab.count; ++sg) {
+      tab.first[sg] = static_cast<int32_t>(total);
+      tab.span[sg] = kGramStage;
+      tab.dims[sg] = dims[g0 + sg];
+      tab.outs[sg] = nullptr;
+      total += (dims[g0 + sg] + kGramStage - 1) / kGramStage;
+      if (total > 0x7fffffff) return hipErrorInvalidValue;
+    }
+    tab.first[tab.count] = static_cast<int32_t>(total);
+    if (total == 0) continue;
+    const hipError_t e = f(g0, tab, total < slots ? total : slots);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+template <int NB>
+hipError_t launch_gram_table_nb(const float* const* ptrs, int n, const SegTable& tab,
+                                int64_t groups, const int32_t* ref, int64_t base, int64_t tiles,
+                                double* partial, hipStream_t s) {
+  if (n < 16 * NB)
+    launch("dist_gram_table", k_dist_gram_table<NB, true>, dim3(static_cast<unsigned>(groups)),
+           dim3(kBlock), 0, s, ptrs, tab, n, ref, base, tiles, partial);
+  else
+    launch("dist_gram_table", k_dist_gram_table<NB, false>, dim3(static_cast<unsigned>(groups)),
+           dim3(kBlock), 0, s, ptrs, tab, n, ref, base, tiles, partial);
+  return hipGetLastError();
+}
+
 int g_direct_max_n = 20;
 
 }  // namespace
+
+int64_t table_gram_tiles(const int64_t* dims, int K, int n) {
+  int64_t tiles = 0;
+  const hipError_t e = for_each_gram_launch(n, dims, K, [&](int, const SegTable&, int64_t groups) {
+    tiles += groups;
+    return hipSuccess;
+  });
+  return e == hipSuccess ? tiles : -1;
+}
+
+size_t table_gram_probe_bytes() {
+  return align256(static_cast<size_t>(kProbeRuns) * kNmax * kNmax * sizeof(double)) +
+         align256(sizeof(int32_t));
+}
+
+int32_t* table_reference_slot(void* probe_space) {
+  return reinterpret_cast<int32_t*>(
+      static_cast<char*>(probe_space) +
+      align256(static_cast<size_t>(kProbeRuns) * kNmax * kNmax * sizeof(double)));
+}
+
+hipError_t enqueue_table_reference(const float* const* ptrs, int n, const int64_t* dims, int K,
+                                   void* probe_space, hipStream_t s) {
+  // probed on the longest segment (the first of equal ones)
+  int big = 0;
+  for (int sg = 1; sg < K; ++sg)
+    if (dims[sg] > dims[big]) big = sg;
+  if (K == 0 || dims[big] == 0) return hipErrorInvalidValue;
+  double* probe = static_cast<double*>(probe_space);
+  const int runs = probe_runs(dims[big]);
+  launch("probe", k_probe<TableRows>, dim3(n, runs), dim3(kBlock), 0, s,
+         TableRows{ptrs + static_cast<int64_t>(big) * n}, n, dims[big], probe);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  launch("pick_ref", k_pick_ref, dim3(1), dim3(kPickThreads), 0, s, probe, n, runs,
+         table_reference_slot(probe_space));
+  return hipGetLastError();
+}
+
+hipError_t enqueue_distances_table_gram(const float* const* ptrs, int n, const int64_t* dims,
+                                        int K, double* partial, int64_t tiles, void* probe_space,
+                                        hipStream_t s) {
+  hipError_t e = enqueue_table_reference(ptrs, n, dims, K, probe_space, s);
+  if (e != hipSuccess) return e;
+  const int32_t* ref = table_reference_slot(probe_space);
+  int64_t base = 0;
+  const int nb = (n + 15) / 16;
+  return for_each_gram_launch(n, dims, K, [&](int g0, const SegTable& tab, int64_t groups) {
+    const float* const* p = ptrs + static_cast<int64_t>(g0) * n;
+    hipError_t r;
+    switch (nb) {
+      case 1: r = launch_gram_table_nb<1>(p, n, tab, groups, ref, base, tiles, partial, s); break;
+      case 2: r = launch_gram_table_nb<2>(p, n, tab, groups, ref, base, tiles, partial, s); break;
+      case 3: r = launch_gram_table_nb<3>(p, n, tab, groups, ref, base, tiles, partial, s); break;
+      case 4: r = launch_gram_table_nb<4>(p, n, tab, groups, ref, base, tiles, partial, s); break;
+      default: return hipErrorInvalidValue;
+    }
+    base += groups;
+    return r;
+  });
+}
 
 int direct_max_n() { return __atomic_load_n(&g_direct_max_n, __ATOMIC_RELAXED); }
 void set_direct_max_n(int n) { __atomic_store_n(&g_direct_max_n, n, __ATOMIC_RELAXED); }
@@ -612,7 +809,8 @@ DistSums dist_sums(const DistPlan& p, const DistWorkspace& ws) {
 hipError_t enqueue_reference(const float* x, const DistPlan& p, const DistWorkspace& ws,
                              hipStream_t s) {
   const int runs = probe_runs(p.d);
-  launch("probe", k_probe, dim3(p.n, runs), dim3(kBlock), 0, s, x, p.n, p.d, ws.probe);
+  launch("probe", k_probe<MatrixRows>, dim3(p.n, runs), dim3(kBlock), 0, s, MatrixRows{x, p.d},
+         p.n, p.d, ws.probe);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   launch("pick_ref", k_pick_ref, dim3(1), dim3(kPickThreads), 0, s, ws.probe, p.n, runs, ws.ref);

@@ -8,6 +8,7 @@
 #include <map>
 #include <mutex>
 #include <new>
+#include <vector>
 
 #include "garfield.h"
 #include "garfield_tuning.h"
@@ -465,7 +466,6 @@ garfield_status garfield_seg_aggregate(garfield_segmented* seg, const float* x, 
 static garfield_status check_table(const garfield_segmented* seg, const float* const* ptrs,
                             const int64_t* dims, int K) {
   if (!seg || K < 0 || (K > 0 && (!ptrs || !dims))) return GARFIELD_EINVAL;
-  if (seg->n > GARFIELD_DIRECT_MAX_N_LIMIT) return GARFIELD_ETOOBIG;
   for (int s = 0; s < K; ++s)
     if (dims[s] < 0) return GARFIELD_EINVAL;
   return GARFIELD_OK;
@@ -476,19 +476,28 @@ garfield_status garfield_seg_accumulate_table(garfield_segmented* seg, const flo
   garfield_status st = check_table(seg, ptrs, dims, K);
   if (st != GARFIELD_OK) return st;
   if (seg->k == 0 || seg->n < 2) return GARFIELD_OK;  // no distances (Median, Average, n = 1)
-  const int64_t tiles = table_tiles(dims, K, seg->n);
+  // n <= 20: the direct engine; above, the Gram engine over the table
+  const bool gram = seg->n > GARFIELD_DIRECT_MAX_N_LIMIT;
+  const int64_t tiles = gram ? table_gram_tiles(dims, K, seg->n) : table_tiles(dims, K, seg->n);
+  if (tiles < 0) return GARFIELD_ETOOBIG;
   if (tiles == 0) return GARFIELD_OK;  // every segment is empty: all distances 0
-  const int entries = seg->n * (seg->n - 1) / 2;
+  const int nb = (seg->n + 15) / 16;
+  const int entries = gram ? nb * (nb + 1) / 2 * 256 : seg->n * (seg->n - 1) / 2;
   void* base = nullptr;
   const size_t partial_bytes = align256(static_cast<size_t>(tiles) * entries * sizeof(double));
-  st = workspace(partial_bytes + align256(entries * sizeof(double)), &base);
+  const size_t sums_bytes = align256(entries * sizeof(double));
+  st = workspace(partial_bytes + sums_bytes + (gram ? table_gram_probe_bytes() : 0), &base);
   if (st != GARFIELD_OK) return st;
   double* partial = static_cast<double*>(base);
   double* sums = reinterpret_cast<double*>(static_cast<char*>(base) + partial_bytes);
+  void* probe = static_cast<char*>(base) + partial_bytes + sums_bytes;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = enqueue_distances_table(ptrs, seg->n, dims, K, partial, tiles, s);
+  hipError_t e = gram ? enqueue_distances_table_gram(ptrs, seg->n, dims, K, partial, tiles, probe, s)
+                      : enqueue_distances_table(ptrs, seg->n, dims, K, partial, tiles, s);
   if (e == hipSuccess) e = enqueue_sum_tiles(partial, tiles, entries, sums, s);
-  if (e == hipSuccess) e = enqueue_accumulate_dist(DistSums{sums, kEngineDirect, seg->n}, seg->dacc, s);
+  if (e == hipSuccess)
+    e = enqueue_accumulate_dist(DistSums{sums, gram ? kEngineGram : kEngineDirect, seg->n},
+                                seg->dacc, s);
   return to_status(e);
 }
 
@@ -603,6 +612,24 @@ int garfield_tuning_gram_reference(const float* x, int n, long long d, void* str
   if (enqueue_reference(x, plan, ws, s) != hipSuccess) return -1;
   int32_t ref = -1;
   if (hipMemcpyAsync(&ref, ws.ref, sizeof(ref), hipMemcpyDeviceToHost, s) != hipSuccess) return -1;
+  if (hipStreamSynchronize(s) != hipSuccess) return -1;
+  return ref;
+}
+
+int garfield_tuning_table_gram_reference(const float* const* ptrs, int n, const long long* dims,
+                                         int K, void* stream) {
+  if (!ptrs || !dims || n < 2 || n > GARFIELD_NMAX || K < 1) return -1;
+  for (int k = 0; k < K; ++k)
+    if (dims[k] < 0) return -1;
+  std::vector<int64_t> d64(dims, dims + K);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  void* base = nullptr;
+  if (workspace(table_gram_probe_bytes(), &base) != GARFIELD_OK) return -1;
+  if (enqueue_table_reference(ptrs, n, d64.data(), K, base, s) != hipSuccess) return -1;
+  int32_t ref = -1;
+  if (hipMemcpyAsync(&ref, table_reference_slot(base), sizeof(ref), hipMemcpyDeviceToHost, s) !=
+      hipSuccess)
+    return -1;
   if (hipStreamSynchronize(s) != hipSuccess) return -1;
   return ref;
 }

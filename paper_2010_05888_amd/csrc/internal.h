@@ -88,6 +88,20 @@ hipError_t enqueue_sum_tiles(const double* partial, int64_t tiles, int entries, 
 int64_t table_tiles(const int64_t* dims, int K, int n);
 hipError_t enqueue_distances_table(const float* const* ptrs, int n, const int64_t* dims, int K,
                                    double* partial, int64_t tiles, hipStream_t s);
+// The Gram engine over a table (n > 20): table_gram_tiles = partial columns
+// (-1 if a launch would exceed 2^31 stages); probe_space holds
+// table_gram_probe_bytes() of probe matrices and the reference row; the
+// partials have the Gram layout of dist_layout.h.
+int64_t table_gram_tiles(const int64_t* dims, int K, int n);
+size_t table_gram_probe_bytes();
+hipError_t enqueue_distances_table_gram(const float* const* ptrs, int n, const int64_t* dims,
+                                        int K, double* partial, int64_t tiles, void* probe_space,
+                                        hipStream_t s);
+// Its reference row alone (into table_reference_slot(probe_space)); needs a
+// nonempty segment.
+hipError_t enqueue_table_reference(const float* const* ptrs, int n, const int64_t* dims, int K,
+                                   void* probe_space, hipStream_t s);
+int32_t* table_reference_slot(void* probe_space);
 hipError_t enqueue_mean_rows_table(const float* const* ptrs, int n, const int64_t* dims,
                                    float* const* outs, int K, const int32_t* rows, int k,
                                    hipStream_t s);

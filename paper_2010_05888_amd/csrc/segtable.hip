@@ -37,7 +37,8 @@ __global__ __launch_bounds__(kBlock) void k_dist_direct_seg(const float* const* 
   block_reduce_pairs<P>(acc, partial + tile_base + b, tiles);
 }
 
-// Aggregation: workgroup b covers kBlock * W coordinates of its segment (W = 4).
+// Aggregation: workgroup b covers kBlock * W coordinates of its segment (the
+// mean: W = 4; median and Bulyan: W by the row count, as in the matrix kernels).
 constexpr auto kAggSpan = [](int64_t) { return static_cast<int64_t>(kBlock) * 4; };
 template <int W>
 __device__ __forceinline__ int64_t seg_coord(const SegTable& tab, int s, int b) {
@@ -132,16 +133,20 @@ hipError_t dist_seg_dispatch(int n, const float* const* ptrs, const int64_t* dim
   }
 }
 
+// Widths as the matrix kernels choose them: the K (or T) x W values of a lane
+// within the registers of two waves per SIMD.
 template <int K>
 hipError_t median_seg_dispatch(int k, const float* const* ptrs, int n, const int32_t* rows,
                                const int64_t* dims, float* const* outs, int nseg, hipStream_t s) {
-  if constexpr (K > kDirectMaxNLimit) {
+  if constexpr (K > kNmax) {
     return hipErrorInvalidValue;
   } else {
     if (k != K) return median_seg_dispatch<K + 1>(k, ptrs, n, rows, dims, outs, nseg, s);
-    return for_each_launch(dims, outs, nseg, kAggSpan, [&](int g0, const SegTable& tab,
-                                                            int64_t total) {
-      launch("median_seg", k_median_seg<K, 4>, dim3(static_cast<unsigned>(total)), dim3(kBlock), 0,
+    constexpr int W = K <= 52 ? 4 : 2;
+    auto per = [](int64_t) { return static_cast<int64_t>(kBlock) * W; };
+    return for_each_launch(dims, outs, nseg, per, [&](int g0, const SegTable& tab,
+                                                      int64_t total) {
+      launch("median_seg", k_median_seg<K, W>, dim3(static_cast<unsigned>(total)), dim3(kBlock), 0,
              s, ptrs + static_cast<int64_t>(g0) * n, n, rows, tab);
       return hipGetLastError();
     });
@@ -152,14 +157,16 @@ template <int T>
 hipError_t bulyan_seg_dispatch(int theta, int beta, const float* const* ptrs, int n,
                                const int32_t* sel, const int64_t* dims, float* const* outs,
                                int nseg, hipStream_t s) {
-  if constexpr (T > kDirectMaxNLimit) {
+  if constexpr (T > kNmax) {
     return hipErrorInvalidValue;
   } else {
     if (theta != T)
       return bulyan_seg_dispatch<T + 1>(theta, beta, ptrs, n, sel, dims, outs, nseg, s);
-    return for_each_launch(dims, outs, nseg, kAggSpan, [&](int g0, const SegTable& tab,
-                                                            int64_t total) {
-      launch("bulyan_agg_seg", k_bulyan_agg_seg<T, 4>, dim3(static_cast<unsigned>(total)),
+    constexpr int W = T <= 24 ? 4 : (T <= 48 ? 2 : 1);
+    auto per = [](int64_t) { return static_cast<int64_t>(kBlock) * W; };
+    return for_each_launch(dims, outs, nseg, per, [&](int g0, const SegTable& tab,
+                                                      int64_t total) {
+      launch("bulyan_agg_seg", k_bulyan_agg_seg<T, W>, dim3(static_cast<unsigned>(total)),
              dim3(kBlock), 0, s, ptrs + static_cast<int64_t>(g0) * n, n, sel, beta, tab);
       return hipGetLastError();
     });

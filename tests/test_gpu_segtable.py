@@ -14,7 +14,10 @@ so a batch spans several launches. Checks:
   session's aggregate of the same segment (the same per-coordinate code; only
   the addressing differs);
 * K = 1 (n whole vectors in separate buffers) reproduces the plain rule on
-  the stacked matrix bit for bit: the same tiles, summed in the same order.
+  the stacked matrix bit for bit: the same tiles, summed in the same order;
+* n > 20 (the Gram engine over the table): the selection equals the oracle's
+  when pinned under the Gram bound for the table's own reference row, and the
+  aggregates are within the same tolerance (bit-exact for Krum and Median).
 """
 import numpy as np
 import pytest
@@ -203,15 +206,65 @@ def test_many_tiny_segments():
     assert ok, (at, err)
 
 
-def test_table_validation():
-    x = torch.zeros((21, 8), dtype=torch.float32, device=DEV)
-    seg = gf.Segmented("multikrum", 21, 2)
+GRAM_CASES = [("multikrum", 33, 7, 26), ("krum", 64, 15, 1), ("multikrum_iterated", 33, 7, 9),
+              ("bulyan", 27, 6, None), ("mda", 23, 2, None), ("median", 40, 9, None),
+              ("average", 21, 0, None)]
+
+
+@pytest.mark.parametrize("rule,n,f,m", GRAM_CASES)
+def test_gram_table_matches_the_oracle(rule, n, f, m):
+    # n > 20: the Gram engine over the table (one reference row for every
+    # segment), ragged and misaligned segments over more than one launch
+    d, K = 40009, 110
+    for attempt in range(5):
+        rng = np.random.default_rng(1000 * n + f + 17 * attempt)
+        x = (rng.standard_normal((n, d)) * (1.0 + 0.5 * rng.permutation(n)[:, None] / n)).astype(np.float32)
+        x[:f] *= 8.0
+        sizes = _split(d, K, rng)
+        vectors, keep = _stored_apart(x, sizes, rng)
+        table = gf.SegmentTable(vectors)
+        D = oracle.pairwise_sqdist(x)
+        B = parity.dist_bounds(D, "gram", gf.table_gram_reference(table))
+        if not _pinned(rule, x, f, m, D, B):
+            continue
+        seg = gf.Segmented(rule, n, f, m)
+        try:
+            seg.accumulate_table(table)
+            sel = seg.select()
+            got = torch.cat(seg.aggregate_table(table)).cpu().numpy()
+        finally:
+            seg.close()
+        want, want_sel = _oracle(rule, x, f, m)
+        if want_sel is not None:
+            assert sel.cpu().numpy().tolist() == want_sel.tolist(), (rule, attempt)
+        if rule in ("krum", "median"):
+            assert np.array_equal(got, want), rule
+        else:
+            ok, at, err = parity.agg_close(got, want)
+            assert ok, (rule, at, err)
+        return
+    pytest.fail(f"{rule}: no pinned seed in 5 tries")
+
+
+def test_gram_table_identical_rows_tie_by_index():
+    # identical vectors in different 16-row blocks get identical distance rows
+    n, f, d = 40, 9, 9001
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((n, d)).astype(np.float32)
+    x[37] = x[2]
+    x[38] = x[2]
+    vectors, keep = _stored_apart(x, _split(d, 12, rng), rng)
+    seg = gf.Segmented("multikrum", n, f, 1)
     try:
-        with pytest.raises(gf.GarfieldError) as e:
-            seg.accumulate_table(gf.SegmentTable.rows(list(x)))
-        assert e.value.code == gf.ETOOBIG  # the table path takes n <= 20
+        seg.accumulate_table(gf.SegmentTable(vectors))
+        sel = seg.select().cpu().tolist()
     finally:
         seg.close()
+    want = oracle.multikrum(x, f, 1)[1].tolist()
+    assert sel == want
+
+
+def test_table_validation():
     y = torch.zeros((7, 8), dtype=torch.float32, device=DEV)
     seg = gf.Segmented("multikrum", 7, 1)
     try:
