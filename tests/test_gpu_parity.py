@@ -265,6 +265,42 @@ def test_bulyan_shapes(n, f):
     pytest.fail("no pinned seed in 5 tries")
 
 
+@pytest.mark.parametrize("n,f", [(17, 3), (24, 5), (64, 2), (64, 0)])
+def test_mda_shapes(n, f):
+    # subset counts from 1 to 42,504 (one workgroup to many), both distance
+    # engines, n up to the maximum
+    for attempt in range(5):
+        rng = np.random.default_rng(n * 37 + f + 1000 * attempt)
+        x = rng.standard_normal((n, 2003)).astype(np.float32)
+        x *= (1.0 + 0.5 * rng.permutation(n) / n).astype(np.float32)[:, None]
+        x[:f] += 3.0
+        xt = _to_dev(x)
+        Do = oracle.pairwise_sqdist(x)
+        B, _ = _bounds(x, xt, Do)
+        oo, so = oracle.mda(x, f)
+        if not parity.mda_pinned(Do, B, n, f, so)[0]:
+            continue
+        out, sel = gf.mda(xt, f)
+        assert sel.cpu().numpy().tolist() == so.tolist(), attempt
+        ok, at, err = parity.agg_close(out.cpu().numpy(), oo)
+        assert ok, (attempt, at, err)
+        return
+    pytest.fail("no pinned seed in 5 tries")
+
+
+@pytest.mark.parametrize("n,f", [(27, 6), (30, 6)])
+def test_mda_many_subsets_small_integers(n, f):
+    # 296,010 and 593,775 subsets: every thread scans several ranks with the
+    # successor step; exact distances, so many diameters tie and the first
+    # subset in lexicographic order must win across threads and workgroups
+    rng = np.random.default_rng(n + f)
+    x = rng.integers(-2, 3, size=(n, 33)).astype(np.float32)
+    out, sel = gf.mda(_to_dev(x), f)
+    oo, so = oracle.mda(x, f)
+    assert sel.cpu().numpy().tolist() == so.tolist()
+    assert np.array_equal(out.cpu().numpy(), oo)
+
+
 @pytest.mark.parametrize("n", [11, 15, 19])
 def test_one_neighbour_rounds_break_ties_by_index(n):
     # Bulyan with f = 2 ends with rounds of one neighbour, where the two rows of
