@@ -42,6 +42,8 @@ def _parse():
                     help="target CPU time of the oracle baseline (0 disables it)")
     ap.add_argument("--direct-max-n", type=int, default=None,
                     help="override the direct/Gram distance engine threshold")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture each step's launches in a HIP graph and time its replays")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="time a plain 1 GiB device-to-device copy instead (HBM calibration "
                          "and the reference for the FETCH_SIZE / WRITE_SIZE counters)")
@@ -144,10 +146,10 @@ class Step:
         p = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
         self.px, self.pout, self.pout2, self.psel = p(x), p(self.out), p(self.out2), p(self.sel)
 
-    def __call__(self):
+    def __call__(self, stream=None):
         lib, w = self.lib, self.w
         n, d = self.x.shape
-        f, s = w.f, self.stream
+        f, s = w.f, (stream if stream is not None else self.stream)
         rules = w.rules
         codes = []
         if rules == ("krum", "median"):
@@ -305,6 +307,26 @@ def bench_workload(key, args):
     for k in range(args.warmup):
         step_k(k)
     torch.cuda.synchronize()
+    eager_step_k = step_k
+    if args.graph and args.segments > 1:
+        raise SystemExit("--graph: plain (unsegmented) workloads only")
+    if args.graph:
+        # every step's launches captured once into a HIP graph (after the
+        # warm-up has sized the library's workspace), then replayed
+        graphs = []
+        for st in steps:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                st(stream=ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+            graphs.append(g)
+        torch.cuda.synchronize()
+
+        def step_k(k):
+            graphs[k % len(graphs)].replay()
+
+        for k in range(args.warmup):
+            step_k(k)
+        torch.cuda.synchronize()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     start.record()
@@ -331,10 +353,11 @@ def bench_workload(key, args):
     ms_median = per_step[len(per_step) // 2]
     ms_min = per_step[0]
 
-    # third pass of the same steps with per-kernel HIP events
+    # third pass of the same steps with per-kernel HIP events (launched
+    # directly: the events are stamped by each kernel's own dispatch)
     gf.set_kernel_timing(True)
     for k in range(args.steps):
-        step_k(args.warmup + args.steps + k)
+        eager_step_k(args.warmup + args.steps + k)
     torch.cuda.synchronize()
     kt = gf.kernel_timing()
     gf.set_kernel_timing(False)
@@ -388,6 +411,7 @@ def bench_workload(key, args):
                    "rules": list(w.rules), "n": w.n, "f": w.f, "d": w.d,
                    "m": w.m, "seed": w.seed, "byzantine_rows": inp.byzantine,
                    "distance_engine": gf.distance_engine(w.n, w.d),
+                   "launch": "hip graph replay" if args.graph else "direct",
                    "input_copies": len(copies)},
         "kernels": kernels,
         "roofline": roofline,
