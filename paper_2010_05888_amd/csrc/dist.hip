@@ -469,7 +469,15 @@ __global__ __launch_bounds__(kBlock) void k_sum_tiles(const double* __restrict__
   __shared__ double red[kBlock];
   const double* __restrict__ row = partial + static_cast<int64_t>(blockIdx.x) * tiles;
   double a = 0.0;
-  for (int64_t t = threadIdx.x; t < tiles; t += kBlock) a += row[t];
+  int64_t t = threadIdx.x;
+  for (; t + 7 * kBlock < tiles; t += 8 * kBlock) {  // eight loads in flight, added in order
+    double v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = row[t + u * kBlock];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) a += v[u];
+  }
+  for (; t < tiles; t += kBlock) a += row[t];
   red[threadIdx.x] = a;
   __syncthreads();
   for (int h = kBlock / 2; h > 0; h >>= 1) {

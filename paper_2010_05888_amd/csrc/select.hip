@@ -313,9 +313,12 @@ __device__ void block_min_pair(double* rd, int64_t* rr, double* best, int64_t* b
   *best_r = rr[0];
 }
 
+// With one workgroup (sel non-null) it also writes the winner: the pick
+// kernel is not needed.
 __global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64_t total,
                                                        int64_t per, double* __restrict__ bdiam,
-                                                       int64_t* __restrict__ brank) {
+                                                       int64_t* __restrict__ brank,
+                                                       int32_t* __restrict__ sel) {
   __shared__ double D[kNmax * kNmax];
   __shared__ unsigned char idx_all[kNmax * kBlock];  // position a of thread t at a*kBlock + t
   __shared__ double rd[kBlock];
@@ -329,6 +332,13 @@ __global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64
   int64_t best_r = INT64_MAX;
   mda_scan(D, n, s, r0, r1, StridedIdx{idx_all + threadIdx.x}, &best, &best_r);
   block_min_pair(rd, rr, &best, &best_r);
+  if (sel) {
+    __shared__ unsigned char win[kNmax];
+    if (threadIdx.x == 0) unrank_subset(best_r, n, s, win);
+    __syncthreads();
+    if (static_cast<int>(threadIdx.x) < s) sel[threadIdx.x] = win[threadIdx.x];
+    return;
+  }
   if (threadIdx.x == 0) {
     bdiam[blockIdx.x] = best;
     brank[blockIdx.x] = best_r;
@@ -466,9 +476,9 @@ hipError_t enqueue_mda_select(const DistSums& ds, int f, void* scratch, int32_t*
   double* bdiam = static_cast<double*>(scratch);
   int64_t* brank = reinterpret_cast<int64_t*>(bdiam + blocks);
   launch("mda_search", k_mda_search, dim3(blocks), dim3(kBlock), 0, s, ds, n - f, total, per,
-    bdiam, brank);
+    bdiam, brank, blocks == 1 ? sel : nullptr);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || blocks == 1) return e;
   launch("mda_pick", k_mda_pick, dim3(1), dim3(64), 0, s, bdiam, brank, blocks, n, n - f, sel);
   return hipGetLastError();
 }
