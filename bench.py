@@ -192,19 +192,27 @@ def algorithmic(kernel, w):
 
 
 def source_digest(path):
-    """First 16 hex digits of the SHA-256 of a C/C++/HIP source with its
-    comments and whitespace removed: it changes when the code does, not when a
-    comment does. (String literals holding comment markers are not expected in
-    the kernel sources.)"""
+    """First 16 hex digits of the SHA-256 of a kernel's source file together
+    with every header beside it (the per-coordinate bodies, row sources and
+    generated networks the kernels share), comments and whitespace removed: it
+    changes when the code does, not when a comment does. (String literals
+    holding comment markers are not expected in the kernel sources.)"""
+    import glob
     import hashlib
     import re
 
-    with open(path) as fh:
-        text = fh.read()
-    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
-    text = re.sub(r"//[^\n]*", " ", text)
-    text = re.sub(r"\s+", "", text)
-    return hashlib.sha256(text.encode()).hexdigest()[:16]
+    folder = os.path.dirname(path)
+    files = [path] + sorted(glob.glob(os.path.join(folder, "*.h")) +
+                            glob.glob(os.path.join(folder, "*.inc")))
+    h = hashlib.sha256()
+    for name in files:
+        with open(name) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        text = re.sub(r"\s+", "", text)
+        h.update(os.path.basename(name).encode() + b"\0" + text.encode() + b"\0")
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(kernel, key):

@@ -112,6 +112,44 @@ __device__ __forceinline__ void median_at(const Src& src, int n, int64_t d,
 }
 
 // ---------------------------------------------------------------------------
+// Bulyan with beta = 3 (theta = 2f + 3, the smallest n for f, so T is odd):
+// only the ranks c-2 .. c+2 around the median s[c] can be taken, so a band
+// network (BandNet) leaves them in registers and the rule below -- the same
+// comparisons and the same fp64 sum as bulyan_at's general path -- runs on
+// compile-time registers, without the LDS column.
+template <int T>
+__device__ __forceinline__ float bulyan3_of_band(const float* a) {
+  using B = BandNet<T>;
+  constexpr int c = (T - 1) / 2;  // n_left = n_right = c
+  const double med = static_cast<double>(a[B::reg(c)]);
+  auto take = [&](float lv, float rv) {  // L before R in the merge by (|v - med|, v)
+    const double dl = med - static_cast<double>(lv);
+    const double dr = static_cast<double>(rv) - med;
+    return (dl < dr) || (dl == dr && lv < rv);
+  };
+  double sum = 0.0;
+  if constexpr (T == 3) {  // the whole set
+    sum += static_cast<double>(a[B::reg(0)]);
+    sum += static_cast<double>(a[B::reg(1)]);
+    sum += static_cast<double>(a[B::reg(2)]);
+  } else {
+    // L_1 = s[c-1] against R_2 = s[c+2], then L_2 = s[c-2] against R_1 = s[c+1]
+    int a_taken = 0;
+    if (take(a[B::reg(c - 1)], a[B::reg(c + 2)])) {
+      a_taken = 1;
+      if (take(a[B::reg(c - 2)], a[B::reg(c + 1)])) a_taken = 2;
+    }
+    const float x0 = a_taken == 0 ? a[B::reg(c)] : (a_taken == 1 ? a[B::reg(c - 1)] : a[B::reg(c - 2)]);
+    const float x1 = a_taken == 0 ? a[B::reg(c + 1)] : (a_taken == 1 ? a[B::reg(c)] : a[B::reg(c - 1)]);
+    const float x2 = a_taken == 0 ? a[B::reg(c + 2)] : (a_taken == 1 ? a[B::reg(c + 1)] : a[B::reg(c)]);
+    sum += static_cast<double>(x0);
+    sum += static_cast<double>(x1);
+    sum += static_cast<double>(x2);
+  }
+  return static_cast<float>(sum / 3.0);
+}
+
+// ---------------------------------------------------------------------------
 // Bulyan aggregation for theta = T selected rows, beta = T - 2f closest.
 //
 // With s[0..T-1] sorted: odd T has the median s[c], c = (T-1)/2, always kept,
@@ -142,6 +180,20 @@ __device__ __forceinline__ void bulyan_at(const Src& src, int n, int64_t d,
     for (int t = 0; t < T; ++t) load_w_tail<W>(src.row(row_of(sel, t, n)) + cc, d - cc, v[t]);
   }
   float o[W];
+  if constexpr (kOdd && T >= 3) {
+    if (beta == 3) {  // uniform: the band network and registers only
+#pragma unroll
+      for (int e = 0; e < W; ++e) {
+        float a[T];
+#pragma unroll
+        for (int t = 0; t < T; ++t) a[t] = v[t][e];
+        BandNet<T>::run(a);
+        o[e] = bulyan3_of_band<T>(a);
+      }
+      store_out<W>(out, cc, d, full, o);
+      return;
+    }
+  }
 #pragma unroll
   for (int e = 0; e < W; ++e) {
     float a[T];

@@ -112,13 +112,29 @@ def _cost(ops):
     return sum(2 if op[0] == "ce" else 1 for op in ops)
 
 
+def band3_ranks(k):
+    """The ranks Bulyan's trimmed mean can use when beta = 3 (the smallest
+    theta, n = 4f + 3): odd k, the median c = (k-1)//2 and two on each side;
+    even k (median between c-1 and c, c = k//2), c-3 .. c+2. Clipped to 0..k-1."""
+    if k % 2:
+        c = (k - 1) // 2
+        lo, hi = c - 2, c + 2
+    else:
+        c = k // 2
+        lo, hi = c - 3, c + 2
+    return list(range(max(lo, 0), min(hi, k - 1) + 1))
+
+
 @functools.lru_cache(maxsize=None)
 def network(k, kind):
-    """kind 'median': ranks (k-1)//2 (odd k) or k//2-1, k//2 (even k); 'sort': all ranks."""
+    """kind 'median': ranks (k-1)//2 (odd k) or k//2-1, k//2 (even k); 'sort': all ranks;
+    'band3': band3_ranks(k)."""
     if kind == "median":
         ranks = [(k - 1) // 2] if k % 2 else [k // 2 - 1, k // 2]
     elif kind == "sort":
         ranks = list(range(k))
+    elif kind == "band3":
+        ranks = band3_ranks(k)
     else:
         raise ValueError(kind)
     n = 1
@@ -168,6 +184,7 @@ def emit_header(nmax=NMAX):
         "",
         "template <int K> struct MedianNet;  // run(): median rank(s) land in v[LO], v[HI]",
         "template <int K> struct SortNet;    // run(): v[R[r]] holds rank r",
+        "template <int K> struct BandNet;    // run(): v[reg(r)] holds rank r, FIRST <= r <= LAST",
         "",
     ]
     for k in range(1, nmax + 1):
@@ -189,6 +206,17 @@ def emit_header(nmax=NMAX):
         out.append(f"template <> struct SortNet<{k}> {{")
         out.append(f"  static constexpr int OPS = {_cost(ops)};")
         out.append(f"  __device__ __forceinline__ static int reg(int r) {{ constexpr int R[{k}] = {{{order}}}; return R[r]; }}")
+        out.append("  __device__ __forceinline__ static void run(float* v) {")
+        body = _emit_body(ops)
+        out.append(body if body else "    (void)v;")
+        out.append("  }")
+        out.append("};")
+        ops, reg = network(k, "band3")
+        ranks = band3_ranks(k)
+        order = ", ".join(str(reg[r]) for r in ranks)
+        out.append(f"template <> struct BandNet<{k}> {{")
+        out.append(f"  static constexpr int FIRST = {ranks[0]}, LAST = {ranks[-1]}, OPS = {_cost(ops)};")
+        out.append(f"  __device__ __forceinline__ static constexpr int reg(int r) {{ constexpr int R[{len(ranks)}] = {{{order}}}; return R[r - FIRST]; }}")
         out.append("  __device__ __forceinline__ static void run(float* v) {")
         body = _emit_body(ops)
         out.append(body if body else "    (void)v;")

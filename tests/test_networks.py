@@ -37,13 +37,13 @@ def _check(k, kind, cols):
 
 
 @pytest.mark.parametrize("k", range(1, 19))
-@pytest.mark.parametrize("kind", ["median", "sort"])
+@pytest.mark.parametrize("kind", ["median", "sort", "band3"])
 def test_network_zero_one_exhaustive(k, kind):
     _check(k, kind, _all_binary(k))
 
 
 @pytest.mark.parametrize("k", range(19, gen.NMAX + 1))
-@pytest.mark.parametrize("kind", ["median", "sort"])
+@pytest.mark.parametrize("kind", ["median", "sort", "band3"])
 def test_network_random(k, kind):
     rng = np.random.default_rng(k)
     bins, perms = _random_inputs(k, rng)
@@ -58,6 +58,12 @@ def test_median_ranks_and_register_map():
         assert sorted(reg) == want
         _, reg = gen.network(k, "sort")
         assert sorted(reg) == list(range(k)) and sorted(reg.values()) == list(range(k))
+        # the band holds every rank a beta = 3 trimmed mean can take around the median
+        _, reg = gen.network(k, "band3")
+        c = (k - 1) // 2 if k % 2 else k // 2
+        want = range(max(c - 2, 0), min(c + 2, k - 1) + 1) if k % 2 else \
+            range(max(c - 3, 0), min(c + 2, k - 1) + 1)
+        assert sorted(reg) == list(want)
 
 
 def test_header_generation_is_deterministic(tmp_path):
