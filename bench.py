@@ -433,7 +433,7 @@ def bench_workload(key, args):
 
 FIG3_N = [7, 11, 15, 19, 23, 27, 31, 35, 39, 47, 55, 63]
 FIG3_D = [10**4, 10**5, 10**6, 10**7, 10**8]
-FIG3_MDA_MAX_SUBSETS = 5 * 10**6
+FIG3_MDA_MAX_SUBSETS = 250_000_000  # n = 39 (C(39, 9) = 2.1e8) still runs; n = 47 (1.7e10) does not
 
 
 class SegmentedStep:

@@ -264,31 +264,77 @@ __device__ void unrank_subset(int64_t rank, int n, int s, Idx idx) {
   }
 }
 
+// Largest D among the pairs of positions 0 .. m-1 of idx.
+__device__ double diameter_of(const double* D, int n, StridedIdx idx, int m) {
+  double v = 0.0;
+  for (int a = 0; a < m; ++a) {
+    const double* row = D + idx[a] * n;
+    for (int b = a + 1; b < m; ++b) {
+      const double w = row[idx[b]];
+      v = w > v ? w : v;
+    }
+  }
+  return v;
+}
+
+// Largest D between position p and positions 0 .. p-1 of idx.
+__device__ double column_max(const double* D, int n, StridedIdx idx, int p) {
+  const double* row = D + idx[p] * n;
+  double v = 0.0;
+  for (int a = 0; a < p; ++a) {
+    const double w = row[idx[a]];
+    v = w > v ? w : v;
+  }
+  return v;
+}
+
 // Scan ranks [r0, r1) of the s-subsets of {0..n-1} (D: n x n in LDS), keeping
 // the first strictly smaller diameter: *best, *best_r (unchanged if r0 >= r1).
+// The diameters of the prefixes (positions 0..s-3 and 0..s-2) are kept and
+// updated only when the successor step changes them, so most subsets cost
+// one column of s-1 distances. Subsets that differ only in the last position
+// have consecutive ranks; once the prefix alone reaches the best diameter so
+// far, none of the rest of them can be strictly smaller, and the scan jumps
+// past them (the result is the exhaustive scan's).
 __device__ void mda_scan(const double* D, int n, int s, int64_t r0, int64_t r1, StridedIdx idx,
                          double* best, int64_t* best_r) {
   if (r0 >= r1) return;
   unrank_subset(r0, n, s, idx);
-  for (int64_t r = r0; r < r1; ++r) {
-    double diam = 0.0;
-    for (int a = 0; a < s; ++a) {
-      const double* row = D + idx[a] * n;
-      for (int b = a + 1; b < s; ++b) {
-        const double v = row[idx[b]];
-        diam = v > diam ? v : diam;
+  double pre2 = s >= 3 ? diameter_of(D, n, idx, s - 2) : 0.0;  // positions 0..s-3
+  double pre = 0.0;                                              // positions 0..s-2
+  if (s >= 2) {
+    const double c = column_max(D, n, idx, s - 2);
+    pre = c > pre2 ? c : pre2;
+  }
+  int64_t r = r0;
+  for (;;) {
+    if (pre >= *best) {  // skip to the last subset with this prefix
+      r += (n - 1) - idx[s - 1];
+      idx[s - 1] = static_cast<unsigned char>(n - 1);
+    } else {
+      double diam = 0.0;
+      if (s >= 2) {
+        const double c = column_max(D, n, idx, s - 1);
+        diam = c > pre ? c : pre;
+      }
+      if (diam < *best) {
+        *best = diam;
+        *best_r = r;
       }
     }
-    if (diam < *best) {
-      *best = diam;
-      *best_r = r;
-    }
+    if (r + 1 >= r1) break;
     // lexicographic successor
     int t = s - 1;
     while (t >= 0 && idx[t] == n - s + t) --t;
     if (t < 0) break;
     idx[t] = static_cast<unsigned char>(idx[t] + 1);
     for (int u = t + 1; u < s; ++u) idx[u] = static_cast<unsigned char>(idx[u - 1] + 1);
+    ++r;
+    if (t <= s - 3) pre2 = diameter_of(D, n, idx, s - 2);
+    if (t <= s - 2 && s >= 2) {
+      const double c = column_max(D, n, idx, s - 2);
+      pre = c > pre2 ? c : pre2;
+    }
   }
 }
 
@@ -385,25 +431,40 @@ __global__ __launch_bounds__(kBlock) void k_peer_mda(DistSums ds, const int32_t*
   write_selected(mask, q, map, sel + static_cast<int64_t>(v) * s);
 }
 
-__global__ __launch_bounds__(64) void k_mda_pick(const double* __restrict__ bdiam,
-                                                 const int64_t* __restrict__ brank, int blocks,
-                                                 int n, int s, int32_t* __restrict__ sel) {
-  __shared__ unsigned char idx[kNmax];
-  if (threadIdx.x == 0) {
-    double bd = bdiam[0];
-    int64_t br = brank[0];
-    for (int b = 1; b < blocks; ++b)
-      if (bdiam[b] < bd || (bdiam[b] == bd && brank[b] < br)) {
-        bd = bdiam[b];
-        br = brank[b];
-      }
-    unrank_subset(br, n, s, idx);
-  }
-  __syncthreads();
-  if (threadIdx.x < s) sel[threadIdx.x] = idx[threadIdx.x];
-}
+constexpr int64_t kMdaMaxBlocks = 1024;  // at most this many search workgroups
 
-constexpr int64_t kMdaMaxBlocks = 1024;
+// The minimum (diameter, rank) over the search's per-workgroup results: each
+// thread takes every kBlock-th workgroup (all its loads in flight), then the
+// block's tree; thread 0 unranks the winner.
+__global__ __launch_bounds__(kBlock) void k_mda_pick(const double* __restrict__ bdiam,
+                                                     const int64_t* __restrict__ brank,
+                                                     int blocks, int n, int s,
+                                                     int32_t* __restrict__ sel) {
+  __shared__ double rd[kBlock];
+  __shared__ int64_t rr[kBlock];
+  __shared__ unsigned char idx[kNmax];
+  constexpr int kPer = static_cast<int>(kMdaMaxBlocks / kBlock);
+  double bd[kPer];
+  int64_t br[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int b = threadIdx.x + u * kBlock;
+    bd[u] = b < blocks ? bdiam[b] : __builtin_inf();
+    br[u] = b < blocks ? brank[b] : INT64_MAX;
+  }
+  double best = bd[0];
+  int64_t best_r = br[0];
+#pragma unroll
+  for (int u = 1; u < kPer; ++u)
+    if (bd[u] < best || (bd[u] == best && br[u] < best_r)) {
+      best = bd[u];
+      best_r = br[u];
+    }
+  block_min_pair(rd, rr, &best, &best_r);
+  if (threadIdx.x == 0) unrank_subset(best_r, n, s, idx);
+  __syncthreads();
+  if (static_cast<int>(threadIdx.x) < s) sel[threadIdx.x] = idx[threadIdx.x];
+}
 
 void mda_split(int n, int f, int64_t* total, int64_t* per, int* blocks) {
   *total = binomial(n, f);
@@ -479,7 +540,7 @@ hipError_t enqueue_mda_select(const DistSums& ds, int f, void* scratch, int32_t*
     bdiam, brank, blocks == 1 ? sel : nullptr);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || blocks == 1) return e;
-  launch("mda_pick", k_mda_pick, dim3(1), dim3(64), 0, s, bdiam, brank, blocks, n, n - f, sel);
+  launch("mda_pick", k_mda_pick, dim3(1), dim3(kBlock), 0, s, bdiam, brank, blocks, n, n - f, sel);
   return hipGetLastError();
 }
 
