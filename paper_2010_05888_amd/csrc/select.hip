@@ -238,12 +238,15 @@ __device__ __forceinline__ int64_t binom_dev(int a, int b) {
   return (b < 0 || b > a) ? 0 : kBinom.c[a][b];
 }
 
-// A thread's subset indices in LDS, position a at a stride of kBlock bytes
-// (neighbouring threads read neighbouring bytes: no bank conflicts).
-struct StridedIdx {
-  unsigned char* base;
-  __device__ unsigned char& operator[](int a) const { return base[a * kBlock]; }
+// A thread's per-position values in LDS, position a at a stride of kBlock
+// elements (neighbouring threads read neighbouring elements: no bank
+// conflicts).
+template <typename T>
+struct Strided {
+  T* base;
+  __device__ T& operator[](int a) const { return base[a * kBlock]; }
 };
+using StridedIdx = Strided<unsigned char>;
 
 // The rank-th s-subset of {0..n-1} in lexicographic order (rank < C(n, s)).
 // Every loop is bounded by n, so an out-of-range rank cannot hang a thread;
@@ -264,78 +267,146 @@ __device__ void unrank_subset(int64_t rank, int n, int s, Idx idx) {
   }
 }
 
-// Largest D among the pairs of positions 0 .. m-1 of idx.
-__device__ double diameter_of(const double* D, int n, StridedIdx idx, int m) {
-  double v = 0.0;
-  for (int a = 0; a < m; ++a) {
-    const double* row = D + idx[a] * n;
-    for (int b = a + 1; b < m; ++b) {
-      const double w = row[idx[b]];
-      v = w > v ? w : v;
-    }
-  }
-  return v;
+// Lexicographic rank of positions u+1 .. s-1 of idx among the (s-1-u)-subsets
+// of {idx[u]+1, ..., n-1}.
+__device__ int64_t suffix_rank(int n, int s, StridedIdx idx, int u) {
+  int64_t q = 0;
+  for (int w = u + 1; w < s; ++w)
+    for (int e = idx[w - 1] + 1; e < idx[w]; ++e) q += binom_dev(n - 1 - e, s - 1 - w);
+  return q;
 }
 
-// Largest D between position p and positions 0 .. p-1 of idx.
-__device__ double column_max(const double* D, int n, StridedIdx idx, int p) {
-  const double* row = D + idx[p] * n;
-  double v = 0.0;
-  for (int a = 0; a < p; ++a) {
-    const double w = row[idx[a]];
-    v = w > v ? w : v;
-  }
-  return v;
+// The bound shared by a workgroup's scans: the bits of a non-negative double,
+// which order as the doubles do.
+__device__ __forceinline__ double read_bound(const unsigned long long* bound) {
+  return __longlong_as_double(static_cast<long long>(*static_cast<const volatile unsigned long long*>(bound)));
+}
+__device__ __forceinline__ void lower_bound_to(unsigned long long* bound, double v) {
+  atomicMin(bound, static_cast<unsigned long long>(__double_as_longlong(v)));
 }
 
-// Scan ranks [r0, r1) of the s-subsets of {0..n-1} (D: n x n in LDS), keeping
-// the first strictly smaller diameter: *best, *best_r (unchanged if r0 >= r1).
-// The diameters of the prefixes (positions 0..s-3 and 0..s-2) are kept and
-// updated only when the successor step changes them, so most subsets cost
-// one column of s-1 distances. Subsets that differ only in the last position
-// have consecutive ranks; once the prefix alone reaches the best diameter so
-// far, none of the rest of them can be strictly smaller, and the scan jumps
-// past them (the result is the exhaustive scan's).
+// Scan ranks [r0, r1) of the s-subsets of {0..n-1} (D: n x n in LDS, zero
+// diagonal), keeping the first strictly smaller diameter: *best, *best_r
+// (unchanged if r0 >= r1). Branch and bound over the lexicographic order:
+// pm[u] is the D entry (row * n + column) of the largest distance among
+// positions 0..u (entry 0, the zero diagonal, while there is no pair), and a
+// successor step that changed position t recomputes levels t.. with one
+// column of distances each. No subset extending a prefix 0..u can be the
+// winner once the prefix reaches this thread's best so far (found at a lower
+// rank) or exceeds *bound, the diameter of some subset (the workgroup's
+// seed and every best its threads have found). Those subsets have consecutive
+// ranks, the current one and the C(n-1-idx[u], s-1-u) - 1 - q after it (q,
+// the rank of the current suffix among them, is 0 after a successor step),
+// and the scan jumps past them. The result is the exhaustive scan's.
 __device__ void mda_scan(const double* D, int n, int s, int64_t r0, int64_t r1, StridedIdx idx,
-                         double* best, int64_t* best_r) {
+                         Strided<uint16_t> pm, unsigned long long* bound, double* best,
+                         int64_t* best_r) {
   if (r0 >= r1) return;
   unrank_subset(r0, n, s, idx);
-  double pre2 = s >= 3 ? diameter_of(D, n, idx, s - 2) : 0.0;  // positions 0..s-3
-  double pre = 0.0;                                              // positions 0..s-2
-  if (s >= 2) {
-    const double c = column_max(D, n, idx, s - 2);
-    pre = c > pre2 ? c : pre2;
-  }
   int64_t r = r0;
+  int t = 0;  // first position whose prefix maximum is stale
+  bool first = true;
   for (;;) {
-    if (pre >= *best) {  // skip to the last subset with this prefix
-      r += (n - 1) - idx[s - 1];
-      idx[s - 1] = static_cast<unsigned char>(n - 1);
-    } else {
-      double diam = 0.0;
-      if (s >= 2) {
-        const double c = column_max(D, n, idx, s - 1);
-        diam = c > pre ? c : pre;
+    const double B = read_bound(bound);
+    int e = t > 0 ? pm[t - 1] : 0;
+    double v = D[e];
+    int u = t;
+    for (; u < s; ++u) {
+      const int iu = idx[u];
+      const double* row = D + iu * n;
+      for (int a = 0; a < u; ++a) {
+        const int ia = idx[a];
+        const double w = row[ia];
+        if (w > v) {
+          v = w;
+          e = iu * n + ia;
+        }
       }
-      if (diam < *best) {
-        *best = diam;
-        *best_r = r;
-      }
+      pm[u] = static_cast<uint16_t>(e);
+      if (v > B || v >= *best) break;
     }
+    if (u < s) {  // no subset with the prefix 0..u wins: jump to its last one
+      const int64_t q = first ? suffix_rank(n, s, idx, u) : 0;
+      r += binom_dev(n - 1 - idx[u], s - 1 - u) - 1 - q;
+      for (int w = u + 1; w < s; ++w) idx[w] = static_cast<unsigned char>(n - s + w);
+    } else if (v < *best) {
+      *best = v;
+      *best_r = r;
+      lower_bound_to(bound, v);
+    }
+    first = false;
     if (r + 1 >= r1) break;
     // lexicographic successor
-    int t = s - 1;
+    t = s - 1;
     while (t >= 0 && idx[t] == n - s + t) --t;
     if (t < 0) break;
     idx[t] = static_cast<unsigned char>(idx[t] + 1);
-    for (int u = t + 1; u < s; ++u) idx[u] = static_cast<unsigned char>(idx[u - 1] + 1);
+    for (int w = t + 1; w < s; ++w) idx[w] = static_cast<unsigned char>(idx[w - 1] + 1);
     ++r;
-    if (t <= s - 3) pre2 = diameter_of(D, n, idx, s - 2);
-    if (t <= s - 2 && s >= 2) {
-      const double c = column_max(D, n, idx, s - 2);
-      pre = c > pre2 ? c : pre2;
-    }
   }
+}
+
+// Sets *bound (LDS) to an upper bound on the least diameter, before the scans
+// (all threads take part; ends with a barrier). With seed, every point i is a
+// center: the diameter of its s nearest points (its D row ranked, ties to the
+// lower index) is the diameter of a subset, and the bound is the least of
+// them. A wave takes one center at a time: lane j ranks point j (every lane
+// reads the same row entry), the members form a ballot, and lane a takes the
+// largest distance from member a to the members (down the columns of the
+// symmetric D: consecutive lanes, consecutive banks). Without seed the bound
+// starts at +inf.
+__device__ void init_bound(const double* D, int n, int s, bool seed, unsigned long long* bound) {
+  if (threadIdx.x == 0) *bound = static_cast<unsigned long long>(__double_as_longlong(__builtin_inf()));
+  __syncthreads();
+  if (seed) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, waves = blockDim.x >> 6;
+    double least = __builtin_inf();
+    for (int i = wave; i < n; i += waves) {  // wave-uniform
+      const double* row = D + i * n;
+      bool in = false;
+      if (lane < n) {
+        const double dj = row[lane];
+        int c = 0;
+        for (int k = 0; k < n; ++k) {
+          const double dk = row[k];
+          c += (dk < dj || (dk == dj && k < lane)) ? 1 : 0;
+        }
+        in = c < s;
+      }
+      const uint64_t mem = __ballot(in);
+      double v = 0.0;
+      if (in)
+        for (int b = 0; b < n; ++b) {
+          const double w = ((mem >> b) & 1) ? D[b * n + lane] : 0.0;
+          v = w > v ? w : v;
+        }
+#pragma unroll
+      for (int m = 32; m > 0; m >>= 1) {
+        const double o = __shfl_xor(v, m, 64);
+        v = o > v ? o : v;
+      }
+      least = v < least ? v : least;
+    }
+    if (lane == 0 && least < __builtin_inf()) lower_bound_to(bound, least);
+  }
+  __syncthreads();
+}
+
+// Dynamic LDS of the subset searches: D (n x n fp64), then every thread's
+// prefix maxima (s x kBlock uint16) and indices (s x kBlock bytes).
+size_t scan_lds_bytes(int n, int s) {
+  return static_cast<size_t>(n) * n * sizeof(double) +
+         static_cast<size_t>(s) * kBlock * (sizeof(uint16_t) + 1);
+}
+struct ScanLds {
+  double* D;
+  Strided<uint16_t> pm;
+  StridedIdx idx;
+};
+__device__ __forceinline__ ScanLds carve_scan_lds(double* lds, int n, int s) {
+  uint16_t* pm = reinterpret_cast<uint16_t*>(lds + n * n);
+  unsigned char* idx = reinterpret_cast<unsigned char*>(pm + s * kBlock);
+  return ScanLds{lds, Strided<uint16_t>{pm + threadIdx.x}, StridedIdx{idx + threadIdx.x}};
 }
 
 // Minimum (diameter, rank) over the kBlock threads' candidates by a tree (the
@@ -365,18 +436,20 @@ __global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64
                                                        int64_t per, double* __restrict__ bdiam,
                                                        int64_t* __restrict__ brank,
                                                        int32_t* __restrict__ sel) {
-  __shared__ double D[kNmax * kNmax];
-  __shared__ unsigned char idx_all[kNmax * kBlock];  // position a of thread t at a*kBlock + t
+  extern __shared__ double lds[];
   __shared__ double rd[kBlock];
   __shared__ int64_t rr[kBlock];
   const int n = ds.n;
-  load_dist(ds, D);
+  const ScanLds sl = carve_scan_lds(lds, n, s);
+  load_dist(ds, sl.D);
   const int64_t g = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   const int64_t r0 = g * per;
   const int64_t r1 = (r0 + per < total) ? r0 + per : total;
+  __shared__ unsigned long long bound;
+  init_bound(sl.D, n, s, per > 1, &bound);
   double best = __builtin_inf();
   int64_t best_r = INT64_MAX;
-  mda_scan(D, n, s, r0, r1, StridedIdx{idx_all + threadIdx.x}, &best, &best_r);
+  mda_scan(sl.D, n, s, r0, r1, sl.idx, sl.pm, &bound, &best, &best_r);
   block_min_pair(rd, rr, &best, &best_r);
   if (sel) {
     __shared__ unsigned char win[kNmax];
@@ -399,12 +472,13 @@ __global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64
 __global__ __launch_bounds__(kBlock) void k_peer_mda(DistSums ds, const int32_t* __restrict__ peers,
                                                      int q, int f, int64_t total,
                                                      int32_t* __restrict__ sel) {
-  __shared__ double D[kNmax * kNmax];
-  __shared__ unsigned char idx_all[kNmax * kBlock];
+  extern __shared__ double lds[];
   __shared__ double rd[kBlock];
   __shared__ int64_t rr[kBlock];
   __shared__ int32_t map[kNmax];
   const int v = blockIdx.x, s = q - f;
+  const ScanLds sl = carve_scan_lds(lds, q, s);
+  double* D = sl.D;
   if (static_cast<int>(threadIdx.x) < q) {
     const int r = peers[static_cast<int64_t>(v) * q + threadIdx.x];
     map[threadIdx.x] = r < 0 ? 0 : (r >= ds.n ? ds.n - 1 : r);
@@ -418,9 +492,11 @@ __global__ __launch_bounds__(kBlock) void k_peer_mda(DistSums ds, const int32_t*
   const int64_t per = (total + kBlock - 1) / kBlock;
   const int64_t r0 = static_cast<int64_t>(threadIdx.x) * per;
   const int64_t r1 = (r0 + per < total) ? r0 + per : total;
+  __shared__ unsigned long long bound;
+  init_bound(D, q, s, per > 1, &bound);
   double best = __builtin_inf();
   int64_t best_r = INT64_MAX;
-  mda_scan(D, q, s, r0, r1, StridedIdx{idx_all + threadIdx.x}, &best, &best_r);
+  mda_scan(D, q, s, r0, r1, sl.idx, sl.pm, &bound, &best, &best_r);
   block_min_pair(rd, rr, &best, &best_r);
   __shared__ unsigned char win[kNmax];
   if (threadIdx.x == 0) unrank_subset(best_r, q, s, win);
@@ -431,11 +507,15 @@ __global__ __launch_bounds__(kBlock) void k_peer_mda(DistSums ds, const int32_t*
   write_selected(mask, q, map, sel + static_cast<int64_t>(v) * s);
 }
 
-constexpr int64_t kMdaMaxBlocks = 1024;  // at most this many search workgroups
+// At most this many search workgroups. Short ranges per thread spread over
+// many workgroups beat long ones: the lanes of a wave take different successor
+// steps, so a wave pays for its slowest lane at every step. Of 256 to 65536,
+// 4096 was fastest from 2.6 to 621 million subsets.
+constexpr int64_t kMdaMaxBlocks = 4096;
 
 // The minimum (diameter, rank) over the search's per-workgroup results: each
-// thread takes every kBlock-th workgroup (all its loads in flight), then the
-// block's tree; thread 0 unranks the winner.
+// thread takes every kBlock-th workgroup, eight loads in flight at a time,
+// then the block's tree; thread 0 unranks the winner.
 __global__ __launch_bounds__(kBlock) void k_mda_pick(const double* __restrict__ bdiam,
                                                      const int64_t* __restrict__ brank,
                                                      int blocks, int n, int s,
@@ -443,27 +523,37 @@ __global__ __launch_bounds__(kBlock) void k_mda_pick(const double* __restrict__ 
   __shared__ double rd[kBlock];
   __shared__ int64_t rr[kBlock];
   __shared__ unsigned char idx[kNmax];
-  constexpr int kPer = static_cast<int>(kMdaMaxBlocks / kBlock);
-  double bd[kPer];
-  int64_t br[kPer];
+  constexpr int kInFlight = 8;
+  double best = __builtin_inf();
+  int64_t best_r = INT64_MAX;
+  for (int b0 = threadIdx.x; b0 < blocks; b0 += kInFlight * kBlock) {
+    double bd[kInFlight];
+    int64_t br[kInFlight];
 #pragma unroll
-  for (int u = 0; u < kPer; ++u) {
-    const int b = threadIdx.x + u * kBlock;
-    bd[u] = b < blocks ? bdiam[b] : __builtin_inf();
-    br[u] = b < blocks ? brank[b] : INT64_MAX;
-  }
-  double best = bd[0];
-  int64_t best_r = br[0];
-#pragma unroll
-  for (int u = 1; u < kPer; ++u)
-    if (bd[u] < best || (bd[u] == best && br[u] < best_r)) {
-      best = bd[u];
-      best_r = br[u];
+    for (int u = 0; u < kInFlight; ++u) {
+      const int b = b0 + u * kBlock;
+      bd[u] = b < blocks ? bdiam[b] : __builtin_inf();
+      br[u] = b < blocks ? brank[b] : INT64_MAX;
     }
+#pragma unroll
+    for (int u = 0; u < kInFlight; ++u)
+      if (bd[u] < best || (bd[u] == best && br[u] < best_r)) {
+        best = bd[u];
+        best_r = br[u];
+      }
+  }
   block_min_pair(rd, rr, &best, &best_r);
   if (threadIdx.x == 0) unrank_subset(best_r, n, s, idx);
   __syncthreads();
   if (static_cast<int>(threadIdx.x) < s) sel[threadIdx.x] = idx[threadIdx.x];
+}
+
+// Dynamic LDS above 64 KB (n near 64 with large s) is requested from the
+// runtime first.
+hipError_t allow_lds(const void* kernel, size_t bytes) {
+  if (bytes <= 65536) return hipSuccess;
+  return hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             static_cast<int>(bytes));
 }
 
 void mda_split(int n, int f, int64_t* total, int64_t* per, int* blocks) {
@@ -524,7 +614,11 @@ hipError_t enqueue_peer_mda(const DistSums& ds, int nodes, const int32_t* peers,
                             int32_t* sel, hipStream_t s) {
   const int64_t total = binomial(q, f);
   if (total < 1) return hipErrorInvalidValue;
-  launch("peer_mda", k_peer_mda, dim3(nodes), dim3(kBlock), 0, s, ds, peers, q, f, total, sel);
+  const size_t lds = scan_lds_bytes(q, q - f);
+  hipError_t e = allow_lds(reinterpret_cast<const void*>(k_peer_mda), lds);
+  if (e != hipSuccess) return e;
+  launch("peer_mda", k_peer_mda, dim3(nodes), dim3(kBlock), static_cast<uint32_t>(lds), s, ds,
+         peers, q, f, total, sel);
   return hipGetLastError();
 }
 
@@ -536,9 +630,12 @@ hipError_t enqueue_mda_select(const DistSums& ds, int f, void* scratch, int32_t*
   mda_split(n, f, &total, &per, &blocks);
   double* bdiam = static_cast<double*>(scratch);
   int64_t* brank = reinterpret_cast<int64_t*>(bdiam + blocks);
-  launch("mda_search", k_mda_search, dim3(blocks), dim3(kBlock), 0, s, ds, n - f, total, per,
-    bdiam, brank, blocks == 1 ? sel : nullptr);
-  hipError_t e = hipGetLastError();
+  const size_t lds = scan_lds_bytes(n, n - f);
+  hipError_t e = allow_lds(reinterpret_cast<const void*>(k_mda_search), lds);
+  if (e != hipSuccess) return e;
+  launch("mda_search", k_mda_search, dim3(blocks), dim3(kBlock), static_cast<uint32_t>(lds), s, ds,
+         n - f, total, per, bdiam, brank, blocks == 1 ? sel : nullptr);
+  e = hipGetLastError();
   if (e != hipSuccess || blocks == 1) return e;
   launch("mda_pick", k_mda_pick, dim3(1), dim3(kBlock), 0, s, bdiam, brank, blocks, n, n - f, sel);
   return hipGetLastError();
