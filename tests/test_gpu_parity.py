@@ -8,6 +8,8 @@ is not pinned the test moves to the next seed and records it. Aggregates must
 agree within max(1e-5 |oracle|, 1e-6); Krum's output and odd medians must be
 bit-identical.
 """
+from math import comb
+
 import numpy as np
 import pytest
 import torch
@@ -290,11 +292,29 @@ def test_mda_shapes(n, f):
 
 @pytest.mark.parametrize("n,f", [(27, 6), (30, 6)])
 def test_mda_many_subsets_small_integers(n, f):
-    # 296,010 and 593,775 subsets: every thread scans several ranks with the
-    # successor step; exact distances, so many diameters tie and the first
-    # subset in lexicographic order must win across threads and workgroups
+    # 296,010 and 593,775 subsets over a few thousand workgroups; exact
+    # distances, so many diameters tie and the first subset in lexicographic
+    # order must win across threads and workgroups
     rng = np.random.default_rng(n + f)
     x = rng.integers(-2, 3, size=(n, 33)).astype(np.float32)
+    out, sel = gf.mda(_to_dev(x), f)
+    oo, so = oracle.mda(x, f)
+    assert sel.cpu().numpy().tolist() == so.tolist()
+    assert np.array_equal(out.cpu().numpy(), oo)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("n,f,d,lim", [(31, 7, 33, 2), (34, 7, 3, 20), (40, 6, 2, 50)])
+def test_mda_branch_and_bound(n, f, d, lim):
+    # More than 2^20 subsets, so every thread scans several ranks with the
+    # successor step. Integer rows give exact distances on both engines: in 33
+    # dimensions with values in [-2, 2] many diameters tie; in 2 or 3 dimensions
+    # with a wide range the distances spread, so most prefixes exceed the bound
+    # and are skipped with all their completions, also from a thread's first
+    # subset in the middle of a block.
+    assert comb(n, f) > 4096 * 256
+    rng = np.random.default_rng(n + f + d)
+    x = rng.integers(-lim, lim + 1, size=(n, d)).astype(np.float32)
     out, sel = gf.mda(_to_dev(x), f)
     oo, so = oracle.mda(x, f)
     assert sel.cpu().numpy().tolist() == so.tolist()
