@@ -279,7 +279,8 @@ __device__ int64_t suffix_rank(int n, int s, StridedIdx idx, int u) {
 // The bound shared by a workgroup's scans: the bits of a non-negative double,
 // which order as the doubles do.
 __device__ __forceinline__ double read_bound(const unsigned long long* bound) {
-  return __longlong_as_double(static_cast<long long>(*static_cast<const volatile unsigned long long*>(bound)));
+  const unsigned long long bits = *static_cast<const volatile unsigned long long*>(bound);
+  return __longlong_as_double(static_cast<long long>(bits));
 }
 __device__ __forceinline__ void lower_bound_to(unsigned long long* bound, double v) {
   atomicMin(bound, static_cast<unsigned long long>(__double_as_longlong(v)));
@@ -356,7 +357,8 @@ __device__ void mda_scan(const double* D, int n, int s, int64_t r0, int64_t r1, 
 // symmetric D: consecutive lanes, consecutive banks). Without seed the bound
 // starts at +inf.
 __device__ void init_bound(const double* D, int n, int s, bool seed, unsigned long long* bound) {
-  if (threadIdx.x == 0) *bound = static_cast<unsigned long long>(__double_as_longlong(__builtin_inf()));
+  if (threadIdx.x == 0)
+    *bound = static_cast<unsigned long long>(__double_as_longlong(__builtin_inf()));
   __syncthreads();
   if (seed) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, waves = blockDim.x >> 6;
@@ -593,7 +595,8 @@ hipError_t enqueue_krum_select(const DistSums& ds, int f, int m, int32_t* sel, h
 }
 
 hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStream_t s) {
-  launch("bulyan_select", k_bulyan_select, dim3(1), dim3(kSelectThreads), 0, s, ds, f, ds.n - 2 * f, sel);
+  launch("bulyan_select", k_bulyan_select, dim3(1), dim3(kSelectThreads), 0, s, ds, f,
+         ds.n - 2 * f, sel);
   return hipGetLastError();
 }
 
