@@ -179,6 +179,10 @@ def algorithmic(kernel, w):
     kernel = kernel[:-4] if kernel.endswith("_seg") else kernel  # segment-table forms
     if kernel in ("dist_direct", "dist_gram"):
         return "hbm", 4.0 * n * d
+    if kernel == "dist_direct_sum":  # the rows, and one fp64 column sum written per coordinate
+        return "hbm", 4.0 * n * d + 8.0 * d
+    if kernel == "mean_complement":  # the column sums, the n - m unselected rows, the output
+        return "hbm", 8.0 * d + 4.0 * (n - w.m + 1) * d
     if kernel == "mean_rows":
         k = {"krum": 1, "multikrum": w.m, "multikrum_iterated": w.m,
              "mda": n - f}.get(w.rules[0], n)

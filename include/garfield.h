@@ -89,6 +89,13 @@ garfield_status garfield_pairwise_sqdist(const float* x, int n, int64_t d, doubl
  * out: device, d fp32 = mean of the selected vectors, or NULL to compute the
  *      selection only (e.g. to feed garfield_median through `rows`).
  * sel: device, m int32, the selected indices in ascending order.
+ * The mean is the fp64 sum of the selected vectors in ascending index order,
+ * rounded once to fp32. For n <= 12 with 2m > n + 4 the distance pass also
+ * stores each coordinate's fp64 sum over all n vectors (d doubles of
+ * workspace), and the mean pass subtracts the n - m others from it wherever
+ * every such sum is provably exact (the coordinate's exponents span at most
+ * 23 binades), summing the selected vectors elsewhere: the same bits from
+ * fewer bytes read.
  */
 garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int m, float* out,
                                    int32_t* sel, void* stream);

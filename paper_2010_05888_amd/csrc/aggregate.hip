@@ -38,6 +38,90 @@ __global__ __launch_bounds__(kBlock) void k_mean_rows(const float* __restrict__ 
     mean_at<W>(src, n, d, rows, k, c, out);
 }
 
+// Mean of the k distinct rows of sel from the distance step's column sums
+// (enqueue_mean_complement): thread 0 lists the rows not in sel, ascending, in
+// LDS; every lane subtracts them from its coordinates' column sums where all
+// W of those are exact (not NaN), and otherwise sums the rows of sel as
+// k_mean_rows does. Either way the fp64 value is the exact sum k_mean_rows
+// forms (sums of these values are exact where the column sum is), rounded
+// once.
+template <int W>
+__global__ __launch_bounds__(kBlock) void k_mean_complement(const float* __restrict__ x, int n,
+                                                            int64_t d,
+                                                            const int32_t* __restrict__ sel, int k,
+                                                            const double* __restrict__ colsum,
+                                                            float* __restrict__ out) {
+  __shared__ int32_t rest[kNmax];
+  __shared__ int nrest;
+  if (threadIdx.x == 0) {
+    uint64_t mask = 0;
+    for (int t = 0; t < k; ++t) mask |= uint64_t{1} << row_of(sel, t, n);
+    int q = 0;
+    for (int r = 0; r < n; ++r)
+      if (!((mask >> r) & 1)) rest[q++] = r;
+    nrest = q;
+  }
+  __syncthreads();
+  const int q = nrest;
+  const MatrixRows src{x, d};
+  const double count = static_cast<double>(k);
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * W;
+  for (int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W; c < d;
+       c += stride) {
+    const bool full = c + W <= d;
+    double acc[W];
+    bool loaded = false;
+    if constexpr (W >= 2) {
+      if (full) {  // ordinary 16-byte loads: a line's halves meet in L2
+#pragma unroll
+        for (int e = 0; e < W; e += 2) {
+          const d2 t = *reinterpret_cast<const d2*>(colsum + c + e);
+          acc[e] = t.x;
+          acc[e + 1] = t.y;
+        }
+        loaded = true;
+      }
+    }
+    if (!loaded) {
+#pragma unroll
+      for (int e = 0; e < W; ++e) acc[e] = (c + e < d) ? colsum[c + e] : 0.0;
+    }
+    bool exact = true;
+#pragma unroll
+    for (int e = 0; e < W; ++e) exact = exact && !__builtin_isnan(acc[e]);
+    if (exact) {
+      for (int t = 0; t < q; t += 2) {  // two rows' loads in flight
+        const bool two = t + 1 < q;
+        float v[2][W];
+        const float* p0 = src.row(rest[t]) + c;
+        const float* p1 = src.row(rest[two ? t + 1 : t]) + c;
+        if (full) {
+          load_w<W>(p0, v[0]);
+          load_w<W>(p1, v[1]);
+        } else {
+          load_w_tail<W>(p0, d - c, v[0]);
+          load_w_tail<W>(p1, d - c, v[1]);
+        }
+#pragma unroll
+        for (int e = 0; e < W; ++e) acc[e] -= static_cast<double>(v[0][e]);
+        if (two) {
+#pragma unroll
+          for (int e = 0; e < W; ++e) acc[e] -= static_cast<double>(v[1][e]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < W; ++e) acc[e] = 0.0;
+      if (full) sum_rows_at<W, true, true>(src, n, d, sel, k, c, acc);
+      else sum_rows_at<W, false, true>(src, n, d, sel, k, c, acc);
+    }
+    float o[W];
+#pragma unroll
+    for (int e = 0; e < W; ++e) o[e] = static_cast<float>(acc[e] / count);
+    store_out<W>(out, c, d, full, o);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Every lane loads W consecutive coordinates of each of the K rows: 16-byte
 // loads (W = 4) stream a K-row gather far faster than 8- or 4-byte ones, so
@@ -86,6 +170,14 @@ hipError_t launch_mean(const float* x, int n, int64_t d, const int32_t* rows, in
                        hipStream_t s) {
   launch("mean_rows", k_mean_rows<W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s, x, n,
     d, rows, k, out);
+  return hipGetLastError();
+}
+
+template <int W>
+hipError_t launch_mean_complement(const float* x, int n, int64_t d, const int32_t* sel, int k,
+                                  const double* colsum, float* out, hipStream_t s) {
+  launch("mean_complement", k_mean_complement<W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0,
+         s, x, n, d, sel, k, colsum, out);
   return hipGetLastError();
 }
 
@@ -160,6 +252,15 @@ hipError_t enqueue_mean_rows(const float* x, int n, int64_t d, const int32_t* ro
   if (w == 4) return launch_mean<4>(x, n, d, rows, k, out, s);
   if (w == 2) return launch_mean<2>(x, n, d, rows, k, out, s);
   return launch_mean<1>(x, n, d, rows, k, out, s);
+}
+
+hipError_t enqueue_mean_complement(const float* x, int n, int64_t d, const int32_t* sel, int k,
+                                   const double* colsum, float* out, hipStream_t s) {
+  if (d == 0) return hipSuccess;
+  if (n < 1 || n > kNmax || k < 1 || !sel || !colsum) return hipErrorInvalidValue;
+  const int w = stream_width(x, out);
+  if (w == 4) return launch_mean_complement<4>(x, n, d, sel, k, colsum, out, s);
+  return launch_mean_complement<1>(x, n, d, sel, k, colsum, out, s);
 }
 
 hipError_t enqueue_median(const float* x, int n, int64_t d, const int32_t* rows, int k,

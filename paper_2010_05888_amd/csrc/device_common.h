@@ -15,6 +15,8 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 // aligned only when d % 4 == 0).
 typedef float f2u __attribute__((ext_vector_type(2), aligned(4)));
 typedef float f4u __attribute__((ext_vector_type(4), aligned(4)));
+// Two doubles (16-byte aligned).
+typedef double d2 __attribute__((ext_vector_type(2)));
 
 // min / max on finite values (inputs are finite by contract).
 __device__ __forceinline__ float fmin_(float a, float b) { return __builtin_fminf(a, b); }

@@ -44,12 +44,40 @@ __device__ __forceinline__ void block_reduce_pairs(const float* acc, double* __r
   }
 }
 
+// Column sums for the mean of a large selection (dist.hip's column-sum
+// variant): colsum[c] is the fp64 sum of the N rows at coordinate c, in row
+// order, when that sum and every sum of a subset of the rows is exact, else
+// NaN. Exactness is decided from the exponents: finite fp32 values whose
+// exponent fields lie in [emin, emax] (subnormals counted as 1) are integer
+// multiples of 2^(emin - 150) below 2^(emax - 126) in magnitude, so any sum of
+// at most 64 of them is such a multiple below 2^(emax - 120), which takes at
+// most emax - emin + 30 bits: exact in fp64 when emax - emin <= 23. hi is the
+// largest |bits| seen, lo1 the smallest |bits| - 1 (zeros wrap to 2^32 - 1
+// and drop out).
+struct ColSum {
+  double s = 0.0;
+  uint32_t hi = 0, lo1 = 0xffffffffu;
+  __device__ __forceinline__ void add(float v) {
+    const uint32_t b = __float_as_uint(v) & 0x7fffffffu;
+    hi = b > hi ? b : hi;
+    lo1 = (b - 1u) < lo1 ? (b - 1u) : lo1;
+    s += static_cast<double>(v);
+  }
+  __device__ __forceinline__ double value() const {
+    const int emax = static_cast<int>(hi >> 23);
+    int emin = lo1 == 0xffffffffu ? emax : static_cast<int>((lo1 + 1u) >> 23);
+    emin = emin < 1 ? 1 : emin;
+    return (emax < 255 && emax - emin <= 23) ? s : __builtin_nan("");
+  }
+};
+
 // Lane t takes W consecutive coordinates every kBlock * W in [start, end) of
 // rows 0..N-1 of `src`, adding (x_i - x_j)^2 for every pair into acc (pairs
-// in row-major order over i < j).
-template <int N, int W, class Src>
+// in row-major order over i < j). With SUM, it also writes the column sums
+// (ColSum) of its coordinates to colsum.
+template <int N, int W, bool SUM = false, class Src>
 __device__ __forceinline__ void direct_accumulate(const Src& src, int64_t start, int64_t end,
-                                                  float* acc) {
+                                                  float* acc, double* __restrict__ colsum = nullptr) {
   for (int64_t c = start + static_cast<int64_t>(threadIdx.x) * W; c < end; c += kBlock * W) {
     float v[N][W];
     if (c + W <= end) {
@@ -71,6 +99,33 @@ __device__ __forceinline__ void direct_accumulate(const Src& src, int64_t start,
           ++p;
         }
       }
+    }
+    if constexpr (SUM) {
+      double o[W];
+#pragma unroll
+      for (int e = 0; e < W; ++e) {
+        ColSum cs;
+#pragma unroll
+        for (int i = 0; i < N; ++i) cs.add(v[i][e]);
+        o[e] = cs.value();
+      }
+      // ordinary (L2-allocating) stores, two doubles at a time: the lanes'
+      // halves of each cache line meet in L2 before it goes to HBM
+      if constexpr (W >= 2) {
+        if (c + W <= end) {
+#pragma unroll
+          for (int e = 0; e < W; e += 2) {
+            d2 t;
+            t.x = o[e];
+            t.y = o[e + 1];
+            *reinterpret_cast<d2*>(colsum + c + e) = t;
+          }
+          continue;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < W; ++e)
+        if (c + e < end) colsum[c + e] = o[e];
     }
   }
 }

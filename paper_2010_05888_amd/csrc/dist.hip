@@ -49,6 +49,23 @@ __global__ __launch_bounds__(kBlock) void k_dist_direct(const float* __restrict_
   block_reduce_pairs<P>(acc, partial + blockIdx.x, gridDim.x);
 }
 
+// The same step, also writing the exact column sums of the n rows (ColSum in
+// direct_body.h) for the mean of a large selection.
+template <int N, int W>
+__global__ __launch_bounds__(kBlock) void k_dist_direct_sum(const float* __restrict__ x, int64_t d,
+                                                             int64_t chunk,
+                                                             double* __restrict__ partial,
+                                                             double* __restrict__ colsum) {
+  constexpr int P = N * (N - 1) / 2;
+  float acc[P];
+#pragma unroll
+  for (int p = 0; p < P; ++p) acc[p] = 0.0f;
+  const int64_t start = static_cast<int64_t>(blockIdx.x) * chunk;
+  const int64_t end = (start + chunk < d) ? start + chunk : d;
+  direct_accumulate<N, W, true>(MatrixRows{x, d}, start, end, acc, colsum);
+  block_reduce_pairs<P>(acc, partial + blockIdx.x, gridDim.x);
+}
+
 // ---------------------------------------------------------------------------
 // Gram engine, step 1: probe. The sample is kProbeRuns runs of kBlock
 // consecutive coordinates spread evenly over d (all of d in one run when d is
@@ -506,7 +523,16 @@ __global__ __launch_bounds__(kBlock) void k_zero_f64(double* __restrict__ p, int
 
 // ---------------------------------------------------------------------------
 template <int N, int W>
-hipError_t launch_direct_nw(const float* x, const DistPlan& p, double* partial, hipStream_t s) {
+hipError_t launch_direct_nw(const float* x, const DistPlan& p, double* partial, double* colsum,
+                            hipStream_t s) {
+  if constexpr (N <= kColSumMaxN) {
+    if (colsum) {
+      launch("dist_direct_sum", k_dist_direct_sum<N, W>, dim3(static_cast<unsigned>(p.tiles)),
+             dim3(kBlock), 0, s, x, p.d, p.chunk, partial, colsum);
+      return hipGetLastError();
+    }
+  }
+  if (colsum) return hipErrorInvalidValue;
   launch("dist_direct", k_dist_direct<N, W>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock), 0,
     s, x, p.d, p.chunk, partial);
   return hipGetLastError();
@@ -518,24 +544,25 @@ hipError_t launch_direct_nw(const float* x, const DistPlan& p, double* partial, 
 int direct_width_cap(int n) { return n <= 12 ? 4 : (n <= 19 ? 2 : 1); }
 
 template <int N>
-hipError_t launch_direct_n(const float* x, const DistPlan& p, double* partial, hipStream_t s) {
+hipError_t launch_direct_n(const float* x, const DistPlan& p, double* partial, double* colsum,
+                           hipStream_t s) {
   if constexpr (N <= 12) {
-    if (p.width == 4) return launch_direct_nw<N, 4>(x, p, partial, s);
+    if (p.width == 4) return launch_direct_nw<N, 4>(x, p, partial, colsum, s);
   }
   if constexpr (N <= 19) {
-    if (p.width >= 2) return launch_direct_nw<N, 2>(x, p, partial, s);
+    if (p.width >= 2) return launch_direct_nw<N, 2>(x, p, partial, colsum, s);
   }
-  return launch_direct_nw<N, 1>(x, p, partial, s);
+  return launch_direct_nw<N, 1>(x, p, partial, colsum, s);
 }
 
 template <int N>
 hipError_t launch_direct_dispatch(int n, const float* x, const DistPlan& p, double* partial,
-                                  hipStream_t s) {
+                                  double* colsum, hipStream_t s) {
   if constexpr (N > kDirectMaxNLimit) {
     return hipErrorInvalidValue;
   } else {
-    if (n == N) return launch_direct_n<N>(x, p, partial, s);
-    return launch_direct_dispatch<N + 1>(n, x, p, partial, s);
+    if (n == N) return launch_direct_n<N>(x, p, partial, colsum, s);
+    return launch_direct_dispatch<N + 1>(n, x, p, partial, colsum, s);
   }
 }
 
@@ -830,11 +857,12 @@ bool foldable(const DistPlan& p, int max_entries) {
 }
 
 hipError_t enqueue_distances(const float* x, const DistPlan& p, const DistWorkspace& ws,
-                             hipStream_t s, bool sum_tiles) {
+                             hipStream_t s, bool sum_tiles, double* colsum) {
   hipError_t e = hipSuccess;
+  if (colsum && (p.engine != kEngineDirect || p.n > kColSumMaxN)) return hipErrorInvalidValue;
   if (p.engine == kEngineNone) return hipSuccess;  // D is all zeros: nothing to compute
   if (p.engine == kEngineDirect) {
-    e = launch_direct_dispatch<2>(p.n, x, p, ws.partial, s);
+    e = launch_direct_dispatch<2>(p.n, x, p, ws.partial, colsum, s);
   } else {
     if ((e = enqueue_reference(x, p, ws, s)) != hipSuccess) return e;
     const int nb = (p.n + 15) / 16;

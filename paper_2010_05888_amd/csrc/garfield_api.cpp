@@ -79,8 +79,11 @@ garfield_status check_common(const float* x, int n, int f, int64_t d) {
 // selection kernel adds the tiles in the same order).
 constexpr int kFoldSelect = 4 * 16;  // k_krum_select, k_bulyan_select: 16 waves
 constexpr int kFoldMda = 4 * 4;      // k_mda_search: 4 waves
+// colsum: the scratch begins with d doubles that receive the column sums
+// (enqueue_distances' colsum).
 garfield_status run_distances(const float* x, int n, int64_t d, size_t extra, DistSums* ds,
-                              void** extra_ptr, hipStream_t s, int fold_entries = 0) {
+                              void** extra_ptr, hipStream_t s, int fold_entries = 0,
+                              bool colsum = false) {
   const DistPlan plan = plan_distances(n, d, x);
   const size_t dist_bytes = dist_workspace_bytes(plan);
   void* base = nullptr;
@@ -94,7 +97,20 @@ garfield_status run_distances(const float* x, int n, int64_t d, size_t extra, Di
     ds->partial = ws.partial;
     ds->tiles = plan.tiles;
   }
-  return to_status(enqueue_distances(x, plan, ws, s, !fold));
+  double* cs = colsum ? static_cast<double*>(*extra_ptr) : nullptr;
+  return to_status(enqueue_distances(x, plan, ws, s, !fold, cs));
+}
+
+// The mean of m of the n rows reads m rows. With the column sums of the
+// distance step (d doubles written there, read here) it reads those and the
+// n - m other rows instead: fewer bytes when 2m > n + 4. Direct engine with
+// n <= kColSumMaxN only.
+bool use_colsum(const float* x, int n, int64_t d, int m) {
+  if (d == 0 || n > kColSumMaxN || 2 * m <= n + 4) return false;
+  return plan_distances(n, d, x).engine == kEngineDirect;
+}
+size_t colsum_bytes(bool cs, int64_t d) {
+  return cs ? static_cast<size_t>(d) * sizeof(double) : 0;
 }
 
 // Requirements of `rule` (Section 3.1) and the number of indices it selects
@@ -177,10 +193,14 @@ garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int 
   if (m > n - f) return GARFIELD_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   DistSums ds;
-  st = run_distances(x, n, d, 0, &ds, nullptr, s, kFoldSelect);
+  const bool cs = out && use_colsum(x, n, d, m);
+  void* colsum = nullptr;
+  st = run_distances(x, n, d, colsum_bytes(cs, d), &ds, &colsum, s, kFoldSelect, cs);
   if (st != GARFIELD_OK) return st;
   st = to_status(enqueue_krum_select(ds, f, m, sel, s));
   if (st != GARFIELD_OK || !out) return st;
+  if (cs)
+    return to_status(enqueue_mean_complement(x, n, d, sel, m, static_cast<double*>(colsum), out, s));
   return to_status(enqueue_mean_rows(x, n, d, sel, m, out, s));
 }
 
@@ -199,10 +219,14 @@ garfield_status garfield_multikrum_iterated(const float* x, int n, int f, int64_
   if (m > n - f) return GARFIELD_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   DistSums ds;
-  st = run_distances(x, n, d, 0, &ds, nullptr, s, kFoldSelect);
+  const bool cs = out && use_colsum(x, n, d, m);
+  void* colsum = nullptr;
+  st = run_distances(x, n, d, colsum_bytes(cs, d), &ds, &colsum, s, kFoldSelect, cs);
   if (st != GARFIELD_OK) return st;
   st = to_status(enqueue_krum_rounds(ds, f, m, sel, s));
   if (st != GARFIELD_OK || !out) return st;
+  if (cs)
+    return to_status(enqueue_mean_complement(x, n, d, sel, m, static_cast<double*>(colsum), out, s));
   return to_status(enqueue_mean_rows(x, n, d, sel, m, out, s));
 }
 
@@ -542,16 +566,19 @@ garfield_status garfield_seg_destroy(garfield_segmented* seg) {
 }
 
 size_t garfield_workspace_bytes(int rule, int n, int f, int64_t d, int m) {
-  (void)m;
   if (n < 1 || n > GARFIELD_NMAX || f < 0 || d < 0) return 0;
   // Plan for 4-byte-aligned rows: the narrowest loads give the most tiles, so
   // this bounds every alignment of x.
   const float* narrow = reinterpret_cast<const float*>(uintptr_t{4});
   switch (rule) {
+    case GARFIELD_RULE_MULTIKRUM:
+    case GARFIELD_RULE_MULTIKRUM_ITERATED: {
+      const int mm = m <= 0 ? n - f : m;
+      return dist_workspace_bytes(plan_distances(n, d, narrow)) +
+             align256(colsum_bytes(use_colsum(narrow, n, d, mm), d));
+    }
     case GARFIELD_RULE_DIST:
     case GARFIELD_RULE_KRUM:
-    case GARFIELD_RULE_MULTIKRUM:
-    case GARFIELD_RULE_MULTIKRUM_ITERATED:
     case GARFIELD_RULE_BULYAN:
       return dist_workspace_bytes(plan_distances(n, d, narrow));
     case GARFIELD_RULE_MDA: {

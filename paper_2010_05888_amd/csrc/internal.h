@@ -57,8 +57,13 @@ hipError_t enqueue_reference(const float* x, const DistPlan& p, const DistWorksp
 // Enqueue the distance step; when the stream reaches its end, ws.sums holds
 // one fp64 sum per entry (see dist_layout.h for how they map to D). With
 // sum_tiles false only the tiles' partials are written (the folded form).
+// colsum (d doubles; direct engine with n <= kColSumMaxN only): the step also
+// writes every coordinate's exact column sum of the n rows, or NaN where that
+// sum or a sum of some of the rows might not be exact (ColSum in
+// direct_body.h).
+constexpr int kColSumMaxN = 12;
 hipError_t enqueue_distances(const float* x, const DistPlan& p, const DistWorkspace& ws,
-                             hipStream_t s, bool sum_tiles = true);
+                             hipStream_t s, bool sum_tiles = true, double* colsum = nullptr);
 // Direct-engine plans with at most kFoldTiles tiles and max_entries entries
 // may leave the tile sums to the selection kernel (DistSums' folded form):
 // its waves add four entries at a time, so a workgroup of w waves folds up to
@@ -155,6 +160,13 @@ hipError_t enqueue_stream_read(const float* x, int64_t count, int blocks, float*
                                hipStream_t s);
 hipError_t enqueue_mean_rows(const float* x, int n, int64_t d, const int32_t* rows, int k,
                              float* out, hipStream_t s);
+// The same mean for a selection of k distinct rows (sel, as a selection kernel
+// writes it), from the column sums the distance step wrote: the sum of the
+// rows not in sel taken from colsum, where colsum is not NaN (the same exact
+// value as the rows' sum in listed order), else the rows of sel summed as
+// enqueue_mean_rows sums them.
+hipError_t enqueue_mean_complement(const float* x, int n, int64_t d, const int32_t* sel, int k,
+                                   const double* colsum, float* out, hipStream_t s);
 hipError_t enqueue_median(const float* x, int n, int64_t d, const int32_t* rows, int k,
                           float* out, hipStream_t s);
 hipError_t enqueue_bulyan_aggregate(const float* x, int n, int f, int64_t d, const int32_t* sel,

@@ -124,7 +124,12 @@ def test_workspace_bytes(lib):
     assert gf.workspace_bytes("krum", 0, 0, 10) == 0
     small = gf.workspace_bytes("multikrum", 11, 2, 11_173_962)
     big = gf.workspace_bytes("multikrum", 64, 15, 138_357_544)
-    assert 0 < small < 64 << 20 and 0 < big < 256 << 20
+    # n = 11, m = 9: the distance partials plus 8 bytes of column sum per
+    # coordinate; m = 7 (2m <= n + 4) has no column sums
+    sums = 8 * 11_173_962
+    small_m7 = gf.workspace_bytes("multikrum", 11, 2, 11_173_962, 7)
+    assert 0 < small_m7 < 4 << 20 and small == small_m7 + (sums + 255) // 256 * 256
+    assert 0 < big < 256 << 20
     assert gf.workspace_bytes("mda", 10, 3, 25_557_032) > 0
     assert gf.workspace_bytes("multikrum_iterated", 11, 2, 11_173_962) == small
     assert gf.workspace_bytes("mda", 64, 31, 10) == 0
