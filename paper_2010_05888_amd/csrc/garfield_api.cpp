@@ -270,10 +270,16 @@ garfield_status garfield_mda(const float* x, int n, int f, int64_t d, float* out
   hipStream_t s = static_cast<hipStream_t>(stream);
   void* scratch = nullptr;
   DistSums ds;
-  st = run_distances(x, n, d, mda_scratch_bytes(n, f), &ds, &scratch, s, kFoldMda);
+  // scratch: the column sums (if used), then the search's per-block results
+  const bool cs = out && use_colsum(x, n, d, n - f);
+  const size_t cs_bytes = align256(colsum_bytes(cs, d));
+  st = run_distances(x, n, d, cs_bytes + mda_scratch_bytes(n, f), &ds, &scratch, s, kFoldMda, cs);
   if (st != GARFIELD_OK) return st;
-  st = to_status(enqueue_mda_select(ds, f, scratch, sel, s));
+  st = to_status(enqueue_mda_select(ds, f, static_cast<char*>(scratch) + cs_bytes, sel, s));
   if (st != GARFIELD_OK || !out) return st;
+  if (cs)
+    return to_status(
+        enqueue_mean_complement(x, n, d, sel, n - f, static_cast<double*>(scratch), out, s));
   return to_status(enqueue_mean_rows(x, n, d, sel, n - f, out, s));
 }
 
@@ -585,6 +591,7 @@ size_t garfield_workspace_bytes(int rule, int n, int f, int64_t d, int m) {
       const int64_t subsets = binomial(n, f);
       if (n < 2 * f + 1 || subsets < 0 || subsets > GARFIELD_MDA_MAX_SUBSETS) return 0;
       return dist_workspace_bytes(plan_distances(n, d, narrow)) +
+             align256(colsum_bytes(use_colsum(narrow, n, d, n - f), d)) +
              align256(mda_scratch_bytes(n, f));
     }
     case GARFIELD_RULE_MEDIAN:

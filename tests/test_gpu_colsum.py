@@ -33,6 +33,9 @@ def _check(x, f, m, rule="multikrum"):
     if rule == "multikrum":
         out, sel = gf.multikrum(xt, f, m)
         oo, so = oracle.multikrum(x, f, m)
+    elif rule == "mda":
+        out, sel = gf.mda(xt, f)
+        oo, so = oracle.mda(x, f)
     else:
         out, sel = gf.multikrum_iterated(xt, f, m)
         oo, so = oracle.multikrum_iterated(x, f, m)
@@ -53,7 +56,7 @@ def test_exact_path_matches_the_oracle(n, f, m, d):
     _check(x, f, m)
 
 
-@pytest.mark.parametrize("rule", ["multikrum", "multikrum_iterated"])
+@pytest.mark.parametrize("rule", ["multikrum", "multikrum_iterated", "mda"])
 def test_inexact_coordinates_take_the_row_sum(rule):
     n, f, m, d = 11, 2, 9, 20011
     x, rng = _rows(n, d, 77)
