@@ -81,3 +81,21 @@ def test_workspace_includes_the_column_sums():
     with_sums = gf.workspace_bytes("multikrum", 11, 2, d, 9)
     without = gf.workspace_bytes("multikrum", 11, 2, d, 7)  # 2m <= n + 4
     assert with_sums - without >= 8 * d
+
+
+@pytest.mark.parametrize("d", [4099, 4100])
+def test_rows_at_an_odd_float_offset(d):
+    # rows starting one float past 16-byte alignment: both kernels take their
+    # one-float loads and stores
+    n, f, m = 11, 2, 9
+    x, rng = _rows(n, d, 5 + d)
+    x += rng.standard_normal((n, d)).astype(np.float32)
+    x[0, ::7] = 1.0e20
+    buf = torch.empty(n * d + 1, dtype=torch.float32, device=DEV)
+    xt = buf[1:].view(n, d)
+    xt.copy_(torch.from_numpy(x))
+    out, sel = gf.multikrum(xt, f, m)
+    oo, so = oracle.multikrum(x, f, m)
+    torch.cuda.synchronize()
+    assert sel.cpu().numpy().tolist() == so.tolist()
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), oo.view(np.uint32))
