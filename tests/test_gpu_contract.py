@@ -103,6 +103,18 @@ def test_all_peers_in_order_equal_the_plain_rule(rule, f, n):
     assert all(torch.equal(y[v], want) for v in range(n))
 
 
+def test_mda_with_64_peers():
+    # 64 peers per node: the subset search's dynamic LDS (D, prefix maxima and
+    # indices) exceeds 64 KB and is requested from the runtime
+    n, f = 64, 2
+    _, x = _inputs(n, 3001, 64)
+    xt = torch.from_numpy(x).to(DEV)
+    peers = torch.arange(n, dtype=torch.int32, device=DEV).repeat(n, 1)
+    y = gf.contract_step("mda", xt, peers, f)
+    want = gf.gar("mda", xt, f)[0]
+    assert all(torch.equal(y[v], want) for v in range(n))
+
+
 def test_several_steps():
     n, q, d, f = 16, 9, 2049, 2
     rng, x = _inputs(n, d, 5)
