@@ -277,13 +277,14 @@ __device__ int64_t suffix_rank(int n, int s, StridedIdx idx, int u) {
 }
 
 // The bound shared by a workgroup's scans: the bits of a non-negative double,
-// which order as the doubles do.
+// which order as the doubles do; none (+inf) when bound is null.
 __device__ __forceinline__ double read_bound(const unsigned long long* bound) {
+  if (!bound) return __builtin_inf();
   const unsigned long long bits = *static_cast<const volatile unsigned long long*>(bound);
   return __longlong_as_double(static_cast<long long>(bits));
 }
 __device__ __forceinline__ void lower_bound_to(unsigned long long* bound, double v) {
-  atomicMin(bound, static_cast<unsigned long long>(__double_as_longlong(v)));
+  if (bound) atomicMin(bound, static_cast<unsigned long long>(__double_as_longlong(v)));
 }
 
 // Scan ranks [r0, r1) of the s-subsets of {0..n-1} (D: n x n in LDS, zero
@@ -447,11 +448,13 @@ __global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64
   const int64_t g = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   const int64_t r0 = g * per;
   const int64_t r1 = (r0 + per < total) ? r0 + per : total;
+  // one subset per thread: nothing to prune, no shared bound
   __shared__ unsigned long long bound;
-  init_bound(sl.D, n, s, per > 1, &bound);
+  unsigned long long* bp = per > 1 ? &bound : nullptr;
+  if (bp) init_bound(sl.D, n, s, true, bp);
   double best = __builtin_inf();
   int64_t best_r = INT64_MAX;
-  mda_scan(sl.D, n, s, r0, r1, sl.idx, sl.pm, &bound, &best, &best_r);
+  mda_scan(sl.D, n, s, r0, r1, sl.idx, sl.pm, bp, &best, &best_r);
   block_min_pair(rd, rr, &best, &best_r);
   if (sel) {
     __shared__ unsigned char win[kNmax];
@@ -495,10 +498,11 @@ __global__ __launch_bounds__(kBlock) void k_peer_mda(DistSums ds, const int32_t*
   const int64_t r0 = static_cast<int64_t>(threadIdx.x) * per;
   const int64_t r1 = (r0 + per < total) ? r0 + per : total;
   __shared__ unsigned long long bound;
-  init_bound(D, q, s, per > 1, &bound);
+  unsigned long long* bp = per > 1 ? &bound : nullptr;
+  if (bp) init_bound(D, q, s, true, bp);
   double best = __builtin_inf();
   int64_t best_r = INT64_MAX;
-  mda_scan(D, q, s, r0, r1, sl.idx, sl.pm, &bound, &best, &best_r);
+  mda_scan(D, q, s, r0, r1, sl.idx, sl.pm, bp, &best, &best_r);
   block_min_pair(rd, rr, &best, &best_r);
   __shared__ unsigned char win[kNmax];
   if (threadIdx.x == 0) unrank_subset(best_r, q, s, win);
