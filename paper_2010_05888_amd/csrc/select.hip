@@ -469,6 +469,8 @@ __global__ __launch_bounds__(kBlock) void k_mda_search(DistSums ds, int s, int64
   }
 }
 
+constexpr int64_t kPeerBoundMinPer = 4;
+
 // Contraction with MDA: workgroup v searches the C(q, f) subsets of its q
 // peers (positions in the peer list, distances gathered as k_peer_select
 // gathers them) for the least diameter, ties to the lowest lexicographic rank
@@ -497,8 +499,10 @@ __global__ __launch_bounds__(kBlock) void k_peer_mda(DistSums ds, const int32_t*
   const int64_t per = (total + kBlock - 1) / kBlock;
   const int64_t r0 = static_cast<int64_t>(threadIdx.x) * per;
   const int64_t r1 = (r0 + per < total) ? r0 + per : total;
+  // one workgroup per node: with a few subsets per thread the seed and the
+  // shared bound cost more than they prune
   __shared__ unsigned long long bound;
-  unsigned long long* bp = per > 1 ? &bound : nullptr;
+  unsigned long long* bp = per > kPeerBoundMinPer ? &bound : nullptr;
   if (bp) init_bound(D, q, s, true, bp);
   double best = __builtin_inf();
   int64_t best_r = INT64_MAX;
