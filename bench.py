@@ -5,15 +5,24 @@ Metric: GAR input GB/s = n * d * 4 B / (time of one whole step), with the n x d
 input already resident in HBM, plus that rate as a fraction of the 8 TB/s HBM
 peak. A step is one full pass of the rule(s) the workload names (distances,
 selection and aggregation, all in libgarfield's HIP kernels), launched on
-torch's current stream. The default workload is the ResNet-18-sized
-Multi-Krum set (n = 11, f = 2, m = 9, d = 11,173,962).
+torch's current stream. The default workload is the largest one that fits
+one GPU: Multi-Krum (m = 49) and then the Median over its selection, n = 64,
+f = 15, d = 138,357,544 (VGG-16-sized vectors, 35.4 GB resident).
 
 Alongside the metric the line carries:
   * roofline: the kernel that took the most time, its algorithmic bytes per
-    launch divided by its average duration (HIP events recorded around each
-    launch by the library, over a second pass of the same timed steps);
+    launch (the rows the rule itself must read and the output it must write)
+    divided by its average duration (HIP events stamped by each launch's own
+    dispatch, over a separate pass of the same steps); bytes that the design
+    adds on top (e.g. column sums written for a later pass) are reported apart
+    as design_bytes_per_launch;
+  * rooflines: the same figure for every kernel that has an algorithmic byte
+    count, and for the Gram distance kernel also its useful matrix-core rate
+    (n (n + 1) d flops of the upper-triangle Gram matrix per launch) against the
+    fp32 MFMA peak;
   * cpu_baseline: the CPU oracle timed on this host's cores on a bounded
-    sample of the same input.
+    sample of the same input, with the host's CPU model, its processor count
+    and the OpenMP team the oracle ran with.
 """
 from __future__ import annotations
 
@@ -34,7 +43,7 @@ def _parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=21)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6],
+    ap.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5, 6],
                     help="1-5: the paper's workload shapes; 6: supplementary, the iterated "
                          "Multi-Krum variant on workload 2's shape")
     ap.add_argument("--all", action="store_true", help="one line per workload (1..6)")
@@ -174,25 +183,38 @@ class Step:
 
 
 def algorithmic(kernel, w):
-    """(bound, algorithmic bytes or flops per launch, unit) of a kernel of workload w."""
+    """(bound, algorithmic bytes per launch, design bytes per launch) of a kernel
+    of workload w. Algorithmic bytes are what the rule itself must move: every
+    row the step reads once, the output written once. Design bytes are what
+    this kernel actually moves by design when that differs (None otherwise):
+    the column sums that the distance pass writes for the complement mean, and
+    the complement mean's own reads."""
     n, f, d = w.n, w.f, w.d
     kernel = kernel[:-4] if kernel.endswith("_seg") else kernel  # segment-table forms
     if kernel in ("dist_direct", "dist_gram"):
-        return "hbm", 4.0 * n * d
-    if kernel == "dist_direct_sum":  # the rows, and one fp64 column sum written per coordinate
-        return "hbm", 4.0 * n * d + 8.0 * d
-    if kernel == "mean_complement":  # the column sums, the n - m unselected rows, the output
-        return "hbm", 8.0 * d + 4.0 * (n - w.m + 1) * d
+        return "hbm", 4.0 * n * d, None
+    if kernel == "dist_direct_sum":  # the rows; the design also writes one fp64 sum per coordinate
+        return "hbm", 4.0 * n * d, 4.0 * n * d + 8.0 * d
+    if kernel == "mean_complement":
+        # the rule's mean reads the m selected rows and writes the output; this
+        # kernel reads the column sums and the n - m unselected rows instead
+        return "hbm", 4.0 * (w.m + 1) * d, 8.0 * d + 4.0 * (n - w.m + 1) * d
     if kernel == "mean_rows":
         k = {"krum": 1, "multikrum": w.m, "multikrum_iterated": w.m,
              "mda": n - f}.get(w.rules[0], n)
-        return "hbm", 4.0 * (k + 1) * d
+        return "hbm", 4.0 * (k + 1) * d, None
     if kernel == "median":
         k = w.m if w.rules == ("multikrum-median",) else n
-        return "hbm", 4.0 * (k + 1) * d
+        return "hbm", 4.0 * (k + 1) * d, None
     if kernel == "bulyan_agg":
-        return "hbm", 4.0 * (n - 2 * f + 1) * d
-    return None, None
+        return "hbm", 4.0 * (n - 2 * f + 1) * d, None
+    return None, None, None
+
+
+def gram_useful_flops(w):
+    """Useful flops of one Gram distance launch: the upper triangle of
+    G = Y Y^T with its diagonal, n (n + 1) / 2 dot products of length d."""
+    return float(w.n * (w.n + 1)) * w.d
 
 
 def source_digest(path):
@@ -232,6 +254,18 @@ def measured_traffic(kernel, key):
         return entry["bytes_per_launch"] if digest == entry["source_sha256"] else None
     except (OSError, KeyError, ValueError):
         return None
+
+
+def cpu_model():
+    """The host CPU's model name, from /proc/cpuinfo."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def cpu_baseline(w, x_dev, seconds):
@@ -276,11 +310,15 @@ def cpu_baseline(w, x_dev, seconds):
         total += run(xs)
         reps += 1
     t = total / reps
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    team = oracle.omp_team_size()
     sample = (f"first {d_s} of {d} coordinates" if d_s < d else "the full input") + \
              f", {reps} run(s), mean time {t:.3f} s"
-    return {"value": round(n * d_s * 4 / t / 1e9, 4), "unit": "GB/s", "cores": threads,
-            "kind": "oracle", "sample": sample}
+    return {"value": round(n * d_s * 4 / t / 1e9, 4), "unit": "GB/s", "cores": team,
+            "kind": "oracle", "sample": sample, "omp_team": team,
+            "nproc": len(os.sched_getaffinity(0)), "cpu_count": os.cpu_count(),
+            "cpu_model": cpu_model(),
+            "scheme": "C++/OpenMP fp64 oracle: the distance pairs split over the team, "
+                      "per-coordinate rules over contiguous coordinate shares"}
 
 
 def bench_workload(key, args):
@@ -378,23 +416,38 @@ def bench_workload(key, args):
     # algorithmic byte count; in latency-bound workloads they can take as long)
     priced = [k for k in kt if algorithmic(k, w)[1]]
     dominant = max(priced or kt, key=lambda k: kt[k][1])
-    bound, per_launch = algorithmic(dominant, w)
-    if per_launch and args.segments > 1:
-        # per-segment calls: one launch per (equal) segment; a segment table: one
-        # launch per 96 segments
-        per_launch /= -(-args.segments // 96) if args.table else args.segments
-    avg_ms = kt[dominant][1] / kt[dominant][0]
-    roofline = {"kernel": dominant, "bound": bound, "achieved": None, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": None, "traffic": measured_traffic(dominant, key),
-                "avg_ms": round(avg_ms, 6), "bytes_per_launch": per_launch}
-    if per_launch:
-        achieved = per_launch / (avg_ms * 1e-3) / 1e9
-        roofline["achieved"] = round(achieved, 2)
-        roofline["frac"] = round(achieved / HBM_PEAK_GBS, 4)
-
     ceiling = measured_ceiling()
-    if roofline["achieved"]:
-        roofline["frac_of_measured_read"] = round(roofline["achieved"] / ceiling["read_GBps"], 4)
+
+    def kernel_roofline(kern):
+        bound, per_launch, design = algorithmic(kern, w)
+        if per_launch and args.segments > 1:
+            # per-segment calls: one launch per (equal) segment; a segment table: one
+            # launch per 96 segments
+            per_seg = -(-args.segments // 96) if args.table else args.segments
+            per_launch /= per_seg
+            design = design / per_seg if design else None
+        avg_ms = kt[kern][1] / kt[kern][0]
+        r = {"kernel": kern, "bound": bound, "achieved": None, "peak": HBM_PEAK_GBS,
+             "unit": "GB/s", "frac": None, "traffic": measured_traffic(kern, key),
+             "avg_ms": round(avg_ms, 6), "bytes_per_launch": per_launch}
+        if per_launch:
+            achieved = per_launch / (avg_ms * 1e-3) / 1e9
+            r["achieved"] = round(achieved, 2)
+            r["frac"] = round(achieved / HBM_PEAK_GBS, 4)
+            r["frac_of_measured_read"] = round(achieved / ceiling["read_GBps"], 4)
+        if design:
+            r["design_bytes_per_launch"] = design
+            r["design_GBps"] = round(design / (avg_ms * 1e-3) / 1e9, 2)
+        if kern.startswith("dist_gram") and args.segments == 1:
+            flops = gram_useful_flops(w)
+            tf = flops / (avg_ms * 1e-3) / 1e12
+            r["mfma"] = {"useful_flops_per_launch": flops, "achieved": round(tf, 2),
+                         "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tf / FP32_MFMA_PEAK_TFLOPS, 4)}
+        return r
+
+    roofline = kernel_roofline(dominant)
+    rooflines = [kernel_roofline(k) for k in sorted(priced, key=lambda k: -kt[k][1])]
 
     base = None
     if args.cpu_seconds > 0:
@@ -427,6 +480,7 @@ def bench_workload(key, args):
                    "input_copies": len(copies)},
         "kernels": kernels,
         "roofline": roofline,
+        "rooflines": rooflines,
         "measured_ceiling": ceiling,
         "cpu_baseline": base,
     }

@@ -66,8 +66,15 @@ def _load():
                    lib.oracle_median, lib.oracle_bulyan, lib.oracle_mda,
                    lib.oracle_multikrum_iterated, lib.oracle_attack, lib.oracle_variance_stats):
             fn.restype = ctypes.c_int
+        lib.oracle_omp_team_size.argtypes = []
+        lib.oracle_omp_team_size.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def omp_team_size() -> int:
+    """Threads in the OpenMP team the oracle's parallel loops use on this host."""
+    return int(_load().oracle_omp_team_size())
 
 
 class OracleError(ValueError):

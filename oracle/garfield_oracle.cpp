@@ -47,6 +47,8 @@
 // Status codes match the library's: 0 ok, 1 invalid argument, 2 n too small
 // for the rule's requirement in f.
 
+#include <omp.h>
+
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
@@ -437,6 +439,18 @@ int oracle_variance_stats(const float* g, int h, int64_t d, const float* grad, d
   stats[0] = dev / (h - 1);
   stats[1] = norm;
   return kOk;
+}
+
+// Threads of the OpenMP team that the parallel loops above run with (the
+// size of a default parallel region on this host), for reporting.
+int oracle_omp_team_size() {
+  int team = 0;
+#pragma omp parallel
+  {
+#pragma omp single
+    team = omp_get_num_threads();
+  }
+  return team;
 }
 
 }  // extern "C"

@@ -15,6 +15,18 @@ rounding inside a tile (everything across tiles is fp64). Per entry:
   |dG_ij| <= (P/2) u (N_i + N_j) + u (N_i + N_j) and |dN_i| <= P u N_i + 2u N_i,
   so |dD_ij| <= (2P + 4) u (N_i + N_j).
 
+Gram reference row. The Gram engine shifts every row by one input row, chosen
+by a probe over a sample of the coordinates: 4 runs of 256 consecutive
+coordinates starting at r * (d // 4), r = 0..3 (all of d when d <= 1024). The
+probe distance of (i, j) is the squared distance over the sample; a row's
+score is the sum of its ceil(n/2) smallest probe distances (itself included,
+at 0), and the reference is the lowest (score, index). The library sums each
+coordinate's square in fp32 (at most 4 per lane, after one rounded
+subtraction) before fp64, a relative error of at most (4 + 2) u per probe
+distance. gram_reference_rule() evaluates the rule from the oracle's fp64
+distances on the same sample, so the tests check the library's pick against
+it instead of trusting it.
+
 Decisions. A selection is "pinned" when every decision it makes is separated
 by more than the summed error bounds of the two quantities compared, so any
 D within those bounds makes the same decision; identical input rows are
@@ -31,6 +43,59 @@ DIRECT_LANE_COORDS = 16
 EPS_DIRECT = (DIRECT_LANE_COORDS + 2) * U
 GRAM_PRODUCTS = 32
 EPS_GRAM = (2 * GRAM_PRODUCTS + 4) * U
+
+
+PROBE_RUNS = 4
+PROBE_RUN = 256
+EPS_PROBE = 6 * U + 1e-12
+
+
+def probe_columns(d):
+    """Coordinates the Gram engine's probe reads."""
+    if d <= PROBE_RUNS * PROBE_RUN:
+        return [np.arange(d)]
+    return [np.arange(r * (d // PROBE_RUNS), r * (d // PROBE_RUNS) + PROBE_RUN)
+            for r in range(PROBE_RUNS)]
+
+
+def gram_reference_rule(x):
+    """(best, candidates): the reference row the probe rule picks on the oracle's
+    exact probe distances, and every row whose score interval, under the
+    library's probe error, reaches the best one's (the library's pick must be
+    among them; when that set is {best} the pick is pinned)."""
+    import oracle
+
+    x = np.asarray(x, dtype=np.float32)
+    n, d = x.shape
+    xs = np.ascontiguousarray(x[:, np.concatenate(probe_columns(d))]) if d else x
+    P = np.zeros((n, n))
+    for cols in probe_columns(d):
+        P += oracle.pairwise_sqdist(np.ascontiguousarray(x[:, cols]))
+    h = (n + 1) // 2
+    score = np.array([np.sort(P[i])[:h].sum() for i in range(n)])
+    lo = np.array([np.sort(P[i] * (1 - EPS_PROBE))[:h].sum() for i in range(n)])
+    hi = np.array([np.sort(P[i])[:h].sum() * (1 + EPS_PROBE) for i in range(n)])
+    best = int(min(range(n), key=lambda i: (score[i], i)))
+    # rows equal on the sample have bit-identical probe rows: an exact tie,
+    # which goes to the lower index
+    same = [i for i in range(n) if np.array_equal(xs[i], xs[best])]
+    cands = sorted(i for i in range(n) if lo[i] <= hi[best] and i not in same[1:])
+    if best not in cands:
+        cands = sorted(cands + [best])
+    return best, cands
+
+
+def checked_reference(x, ref, byzantine=()):
+    """Assert that the library's reference row `ref` follows the probe rule on x
+    (equal to the rule's pick when that is pinned, else one of the rows the
+    error bound cannot separate from it; identical rows tie to the lower
+    index) and is not a Byzantine row; return it."""
+    best, cands = gram_reference_rule(x)
+    assert ref in cands, ("Gram reference row", ref, "rule", best, "candidates", cands)
+    if cands == [best]:
+        assert ref == best, ("Gram reference row", ref, "rule", best)
+    assert ref not in set(int(b) for b in byzantine), ("Byzantine reference row", ref, byzantine)
+    return ref
 
 
 def agg_close(got, want):

@@ -68,6 +68,8 @@ def test_full_size_workload(key):
         ref = gf.gram_reference(xt) if eng == "gram" else None
         torch.cuda.synchronize()
         x = xt.cpu().numpy()
+        if ref is not None:  # the library's pick, checked against the probe rule
+            parity.checked_reference(x, ref, inp.byzantine)
         del xt, inp
         torch.cuda.empty_cache()
         _log(f"copied to host; oracle ({eng} engine bounds)")

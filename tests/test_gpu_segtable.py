@@ -224,7 +224,13 @@ def test_gram_table_matches_the_oracle(rule, n, f, m):
         vectors, keep = _stored_apart(x, sizes, rng)
         table = gf.SegmentTable(vectors)
         D = oracle.pairwise_sqdist(x)
-        B = parity.dist_bounds(D, "gram", gf.table_gram_reference(table))
+        # the table's reference row is probed on its longest segment (the first
+        # of equal ones); checked against the probe rule on that segment
+        big = int(np.argmax(sizes))
+        off = int(sum(sizes[:big]))
+        ref = parity.checked_reference(np.ascontiguousarray(x[:, off:off + sizes[big]]),
+                                       gf.table_gram_reference(table))
+        B = parity.dist_bounds(D, "gram", ref)
         if not _pinned(rule, x, f, m, D, B):
             continue
         seg = gf.Segmented(rule, n, f, m)
