@@ -100,6 +100,27 @@ garfield_status garfield_pairwise_sqdist(const float* x, int n, int64_t d, doubl
 garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int m, float* out,
                                    int32_t* sel, void* stream);
 
+/*
+ * garfield_multikrum for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc. Same arguments, validation, selection and output as
+ * garfield_multikrum (the mean always sums the selected vectors; the result is
+ * the same bits). Its scratch is a fixed array of
+ * GARFIELD_NOALLOC_SCRATCH_BYTES in each device's memory, reserved when the
+ * library is loaded and held until the process ends; the call itself
+ * allocates and frees nothing (when the opt-in per-kernel timing of
+ * garfield_tuning.h is on, its events are created as for every call).
+ * Returns GARFIELD_ETOOBIG when the distance step of (n, d) needs more
+ * scratch than that: up to about 1.7e8 coordinates at n = 20 and any d that
+ * fits in memory for n > 20. Every call on one device uses that device's one
+ * array and leaves it holding its own intermediate values: calls that overlap
+ * in time on one device (other streams, other threads) race and give wrong
+ * results; each call writes every scratch byte it reads before reading it.
+ */
+#define GARFIELD_NOALLOC_SCRATCH_BYTES (64u << 20)
+garfield_status garfield_multikrum_noalloc(const float* x, int n, int f, int64_t d, int m,
+                                           float* out, int32_t* sel, void* stream);
+
 /* Krum (Section 3.1 item 2): Multi-Krum with m = 1; out is a copy of vector
  * sel[0]. out may be NULL. */
 garfield_status garfield_krum(const float* x, int n, int f, int64_t d, float* out, int32_t* sel,

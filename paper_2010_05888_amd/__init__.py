@@ -70,6 +70,7 @@ def load():
         "garfield_pairwise_sqdist": [vp, i32, i64, vp, vp],
         "garfield_krum": [vp, i32, i32, i64, vp, vp, vp],
         "garfield_multikrum": [vp, i32, i32, i64, i32, vp, vp, vp],
+        "garfield_multikrum_noalloc": [vp, i32, i32, i64, i32, vp, vp, vp],
         "garfield_multikrum_iterated": [vp, i32, i32, i64, i32, vp, vp, vp],
         "garfield_median": [vp, i32, i32, i64, vp, i32, vp, vp],
         "garfield_bulyan": [vp, i32, i32, i64, vp, vp, vp],

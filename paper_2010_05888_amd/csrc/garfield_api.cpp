@@ -16,6 +16,14 @@
 #include "internal.h"
 #include "timing.h"
 
+// Scratch of garfield_multikrum_noalloc: a fixed array in every device's
+// memory, held from the library's load until the process ends. Host code
+// never uses the name itself (on the host it is only a stand-in for the
+// symbol): the device address comes from hipGetSymbolAddress, once per
+// device (static_scratch below), and every kernel argument and carve uses
+// that address.
+static __device__ __align__(256) unsigned char scratch[GARFIELD_NOALLOC_SCRATCH_BYTES];
+
 namespace garfield {
 namespace {
 
@@ -81,6 +89,12 @@ constexpr int kFoldSelect = 4 * 16;  // k_krum_select, k_bulyan_select: 16 waves
 constexpr int kFoldMda = 4 * 4;      // k_mda_search: 4 waves
 // colsum: the scratch begins with d doubles that receive the column sums
 // (enqueue_distances' colsum).
+// The steps of run_distances on scratch the caller provides (`base`, at least
+// dist_workspace_bytes(plan) + align256(extra) bytes).
+garfield_status run_distances_on(const DistPlan& plan, void* base, const float* x, size_t extra,
+                                 DistSums* ds, void** extra_ptr, hipStream_t s,
+                                 int fold_entries, bool colsum);
+
 garfield_status run_distances(const float* x, int n, int64_t d, size_t extra, DistSums* ds,
                               void** extra_ptr, hipStream_t s, int fold_entries = 0,
                               bool colsum = false) {
@@ -89,6 +103,14 @@ garfield_status run_distances(const float* x, int n, int64_t d, size_t extra, Di
   void* base = nullptr;
   garfield_status st = workspace(dist_bytes + align256(extra), &base);
   if (st != GARFIELD_OK) return st;
+  return run_distances_on(plan, base, x, extra, ds, extra_ptr, s, fold_entries, colsum);
+}
+
+garfield_status run_distances_on(const DistPlan& plan, void* base, const float* x, size_t extra,
+                                 DistSums* ds, void** extra_ptr, hipStream_t s,
+                                 int fold_entries, bool colsum) {
+  (void)extra;
+  const size_t dist_bytes = dist_workspace_bytes(plan);
   const DistWorkspace ws = carve_dist_workspace(plan, base);
   *ds = dist_sums(plan, ws);
   if (extra_ptr) *extra_ptr = static_cast<char*>(base) + dist_bytes;
@@ -151,6 +173,24 @@ garfield_status rule_shape(int rule, int n, int f, int* m, int* k) {
   }
 }
 
+std::mutex g_scratch_mutex;
+std::map<int, void*> g_scratch_ptr;  // device -> address of `scratch` there
+
+garfield_status static_scratch(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return to_status(hipErrorInvalidDevice);
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  auto it = g_scratch_ptr.find(dev);
+  if (it == g_scratch_ptr.end()) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return to_status(e != hipSuccess ? e : hipErrorUnknown);
+    it = g_scratch_ptr.emplace(dev, p).first;
+  }
+  *out = it->second;
+  return GARFIELD_OK;
+}
+
 static_assert(GARFIELD_NMAX == kNmax, "kernel limit and public limit differ");
 static_assert(GARFIELD_DIRECT_MAX_N_LIMIT == kDirectMaxNLimit, "direct engine limit differs");
 
@@ -201,6 +241,31 @@ garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int 
   if (st != GARFIELD_OK || !out) return st;
   if (cs)
     return to_status(enqueue_mean_complement(x, n, d, sel, m, static_cast<double*>(colsum), out, s));
+  return to_status(enqueue_mean_rows(x, n, d, sel, m, out, s));
+}
+
+garfield_status garfield_multikrum_noalloc(const float* x, int n, int f, int64_t d, int m,
+                                           float* out, int32_t* sel, void* stream) {
+  garfield_status st = check_common(x, n, f, d);
+  if (st != GARFIELD_OK) return st;
+  if (!sel) return GARFIELD_EINVAL;
+  if (n < 2 * f + 3) return GARFIELD_EREQ;
+  if (m <= 0) m = n - f;
+  if (m > n - f) return GARFIELD_EINVAL;
+  const DistPlan plan = plan_distances(n, d, x);
+  if (dist_workspace_bytes(plan) > GARFIELD_NOALLOC_SCRATCH_BYTES) return GARFIELD_ETOOBIG;
+  void* base = nullptr;
+  st = static_scratch(&base);
+  if (st != GARFIELD_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  DistSums ds;
+  // every scratch byte a kernel reads here is written earlier in the same call
+  // (tile partials, entry sums, probe matrices, reference row), so nothing
+  // needs clearing; the mean reads the selected rows (no column sums)
+  st = run_distances_on(plan, base, x, 0, &ds, nullptr, s, kFoldSelect, false);
+  if (st != GARFIELD_OK) return st;
+  st = to_status(enqueue_krum_select(ds, f, m, sel, s));
+  if (st != GARFIELD_OK || !out) return st;
   return to_status(enqueue_mean_rows(x, n, d, sel, m, out, s));
 }
 

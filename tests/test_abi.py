@@ -76,6 +76,15 @@ def test_validation_codes(lib):
     # a float pointer that is not 4-byte aligned
     assert lib.garfield_krum(ctypes.c_void_p(0x1002), 7, 1, 10, FAKE, FAKE, NULL) == gf.EINVAL
     assert lib.garfield_median(ctypes.c_void_p(0x1001), 7, 1, 10, NULL, 0, FAKE, NULL) == gf.EINVAL
+    # the no-allocation Multi-Krum: the same checks, and sizes whose distance
+    # step needs more than its fixed scratch (20 x 2e8: about 74 MB of tile
+    # partials) are refused before any HIP call
+    assert lib.garfield_multikrum_noalloc(FAKE, 7, 1, 10, 7, FAKE, FAKE, NULL) == gf.EINVAL
+    assert lib.garfield_multikrum_noalloc(FAKE, 6, 2, 10, 0, FAKE, FAKE, NULL) == gf.EREQ
+    assert lib.garfield_multikrum_noalloc(FAKE, 65, 2, 10, 0, FAKE, FAKE, NULL) == gf.ETOOBIG
+    assert lib.garfield_multikrum_noalloc(FAKE, 7, 1, 10, 0, FAKE, NULL, NULL) == gf.EINVAL
+    assert lib.garfield_multikrum_noalloc(FAKE, 20, 2, 200_000_000, 0, FAKE, FAKE, NULL) == \
+        gf.ETOOBIG
     # distances / average
     assert lib.garfield_pairwise_sqdist(FAKE, 5, 10, NULL, NULL) == gf.EINVAL
     assert lib.garfield_average(FAKE, 0, 10, FAKE, NULL) == gf.EINVAL
