@@ -15,12 +15,14 @@
 //    n(n-1)/2 pairs in fp32 registers over its coordinates. No cancellation,
 //    and identical rows give bit-identical rows of D.
 //  * Gram (larger n): G = Y Y^T with Y = X - x_ref (a per-coordinate shift by
-//    one input row, chosen robustly by a small probe), on fp32 MFMA
-//    (v_mfma_f32_16x16x4_f32, 16-row blocks, upper block triangle only), then
-//    D_ij = G_ii + G_jj - 2 G_ij in fp64. Shifting by a central row keeps the
-//    cancellation in that difference to a small factor. Identical rows give
-//    identical products in the same order, hence identical G and D rows and
-//    an exact 0 between them.
+//    one input row, chosen robustly by a small probe), each row of Y rounded
+//    per 256-coordinate stage to 22-bit integers and multiplied exactly on
+//    integer MFMA (v_mfma_i32_16x16x64_i8 on three int8 digits, 16-row
+//    blocks, upper block triangle only), then D_ij = G_ii + G_jj - 2 G_ij in
+//    fp64. Shifting by a central row keeps the rounding steps, and the
+//    cancellation in that difference, small. The products are exact, so
+//    identical rows give identical G and D rows and an exact 0 between them,
+//    whatever blocks they sit in.
 
 #include "device_common.h"
 #include "direct_body.h"
@@ -152,44 +154,69 @@ __global__ __launch_bounds__(kPickThreads) void k_pick_ref(const double* __restr
 }
 
 // ---------------------------------------------------------------------------
-// Gram engine, step 3: partial sums of G = Y Y^T, Y = X - x_ref, on fp32 MFMA
-// (v_mfma_f32_16x16x4_f32), upper block triangle only.
+// Gram engine, step 3: partial sums of G = Y Y^T, Y = X - x_ref, computed
+// exactly on integer MFMA (v_mfma_i32_16x16x64_i8), upper block triangle only.
 //
-// Streaming. A stage is the 16*NB rows (rows at or beyond n are not loaded;
-// their Y rows are 0) times kGramStage = 256
-// consecutive coordinates: 1 KB of every row, the shortest run that streams
-// well from rows whose starts are not cache-line aligned (row i starts at
-// i * d floats). Wave w loads rows w*4NB .. w*4NB + 4NB - 1 with one 16-byte
-// load per lane per row (lane l: coordinates 4l .. 4l+3, so one instruction
-// reads 1 KB of one row), writes them to the stage buffer in LDS, and issues
-// the next stage's loads into the same registers before the stage is
-// multiplied: a stage is in flight while the previous one is computed.
+// Streaming and roles. A stage is the 16*NB rows (rows at or beyond n are
+// not loaded; their Y rows are 0) times kGramStage = 256 consecutive
+// coordinates: 1 KB of every row, the shortest run that streams well from
+// rows whose starts are not cache-line aligned (row i starts at i * d
+// floats). A workgroup is eight waves in two roles. Waves 0-3 produce: wave
+// w loads rows w*4NB .. w*4NB + 4NB - 1 with one 16-byte load per lane per
+// row (lane l: coordinates 4l .. 4l+3, so one instruction reads 1 KB of one
+// row), quantizes them into one of two LDS stage buffers, and keeps the next
+// two stages' loads in flight in two register sets (each row's next load is
+// issued as soon as the row is written). Waves 4-7 consume: they multiply
+// the stage in the other buffer. One barrier per stage hands the buffers
+// over, so quantizing (VALU) and multiplying (matrix cores) overlap on every
+// SIMD, which holds one wave of each role.
 //
-// Multiplying. The stage buffer holds Y (the reference row is subtracted as
-// the stage is written). Wave w takes half h = w % 2 of the stage's
-// coordinates (128) for the block pairs (b1 <= b2) of parity w / 2 (pairs q
-// with q % 2 == w / 2; five each when NB = 4, so every wave issues the same
-// number of MFMAs): per 16-coordinate group, lane (g = l/16, r = l%16) reads
-// the 16-byte fragment of row 16b + r at coordinates 4g .. 4g+3 of each block
-// b once (the A and B operands of four consecutive MFMA k-steps). Each pair's
-// MFMAs over two groups start from zero and their fp32 result (32 products)
-// is added into fp64, so every fp32 accumulation spans 32 products whatever d
-// is. (The conversions and fp64 additions do not overlap the MFMAs on this
-// hardware: one addition per 32 products instead of per 16 saves about a
-// fifth of the multiply time.)
+// Quantizing. y = fl(x - x_ref) in fp32 (one rounding). Per row and stage,
+// with E the exponent of the largest |y| (-126 for a zero or subnormal
+// maximum) and k = min(21 - E, 127), every y becomes the integer
+// q = RNE(y * 2^k), |q| <= 2^22: an error of at most 2^-k / 2, i.e. about
+// 2^-23 of the row's largest value in the stage. q is written as three signed
+// base-256 digits, q = 65536 a + 256 b + c with c, b in [-128, 127] and a in
+// [-64, 64], one int8 plane per digit in LDS (c is q's low byte, b the second
+// byte of q + 128, a the third byte of q + 32896), with k per row.
 //
-// Partials. The two halves' fp64 sums of each pair are added (half 0 first)
-// and written as this workgroup's partials; workgroup b takes stages b, b + G, ... (G = grid
-// size), so at any time the grid streams one compact window of every row.
-constexpr int kGramStage = 256;               // coordinates per stage
-constexpr int kGramPitch = kGramStage + 4;    // floats per LDS row (bank spread)
+// Multiplying. The nine digit products of a block pair go into five int32
+// accumulators by weight (aa': 2^32; ab' + ba': 2^24; ac' + bb' + ca': 2^16;
+// bc' + cb': 2^8; cc': 1), each product of int8 digits exact and every sum
+// exact in int32 (at most 2^23 over a stage). Per stage the five are combined
+// in fp64 (a Horner sum in 256, exact: the total is below 2^52) and scaled by
+// 2^-(k_i + k_j) (exact), so the stage's G_ij is the exact dot product of the
+// two quantized rows; it is then added into an fp64 accumulator. Exactness
+// makes the order of the products irrelevant: identical rows give identical
+// G rows wherever they sit in the blocks, and an exact 0 between them.
+// Consumer wave c takes the block pairs q = c, c + 4, ... over the whole
+// stage (K chunks of 64 coordinates: lane (g = l/16, r = l%16) supplies
+// coordinates 16g .. 16g+15 of the chunk for row r of the block, in A and in
+// B alike).
+//
+// Partials. Each consumer wave writes the fp64 sums of its pairs as this
+// workgroup's partials; workgroup b takes stages b, b + G, ... (G = grid
+// size, one workgroup per CU), so at any time the grid streams one compact
+// window of every row.
+constexpr int kGramStage = 256;                  // coordinates per stage
+// Bytes per LDS row of a digit plane: with 288 the 16-byte fragment reads of
+// the multiply (16 rows x 4 column groups per instruction) hit no bank twice
+// on gfx950 (measured: 272, 304, 336 and 400 do).
+constexpr int kPlanePitch = kGramStage + 32;
+constexpr int kGramThreads = 512;                // 4 producer + 4 consumer waves
+constexpr float kRoundMagic = 12582912.0f;       // 1.5 * 2^23
+
+typedef int i4 __attribute__((ext_vector_type(4)));
 
 template <int NB>
 struct GramShape {
   static constexpr int ROWS = 16 * NB;
   static constexpr int NBP = NB * (NB + 1) / 2;   // block pairs b1 <= b2
   static constexpr int RPW = ROWS / 4;            // rows loaded per wave
-  static constexpr int PPW = (NBP + 1) / 2;       // pairs per wave (one parity)
+  static constexpr int PPW = (NBP + 3) / 4;       // pairs per wave (q = w, w + 4, ...)
+  static constexpr int PLANE = ROWS * kPlanePitch;  // bytes per digit plane
+  static constexpr int BUF = 3 * PLANE + 4 * ROWS;  // three planes, then k per row
+  static constexpr int LDS = 2 * BUF;               // two stage buffers
 };
 
 __host__ __device__ constexpr int pair_b1(int nb, int q) {
@@ -219,260 +246,483 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Issue the loads of the stage at c0: this wave's rows into v, the reference
-// row into vr (coordinates at or beyond d read as 0 when the stage is the
-// partial last one).
-template <int NB, bool PAD, bool FULL, class Src>
-__device__ __forceinline__ void gram_issue(const Src& src, int n, int64_t d, int ref, int wave,
-                                           int lane, int64_t c0, f4* v, f4& vr) {
+// One 16-byte load of row `row` at coordinate c (lane l of the wave reads
+// c = c0 + 4l .. c0 + 4l + 3), coordinates at or beyond d reading as 0 unless
+// the stage is known to be whole.
+template <bool FULL, class Src>
+__device__ __forceinline__ f4 gram_load(const Src& src, int row, int64_t c, int64_t d) {
+  const float* p = src.row(row) + c;
+  float t[4];
+  if constexpr (FULL) {
+    load_w<4>(p, t);
+  } else {
+    if (c + 4 <= d) load_w<4>(p, t); else load_w_tail<4>(p, d - c, t);
+  }
+  return f4{t[0], t[1], t[2], t[3]};
+}
+
+// One stage: its rows, its first coordinate and the length of its segment;
+// `full` when all 256 coordinates lie in the segment (wave-uniform).
+template <class Src>
+struct StageRef {
+  Src src;
+  int64_t c0;
+  int64_t d;
+  bool full;
+};
+
+// Load row `row` of stage st into out (this lane's 4 coordinates), guarded
+// when the stage is partial.
+template <class Src>
+__device__ __forceinline__ void stage_load(const StageRef<Src>& st, int row, int lane, f4& out) {
+  const int64_t c = st.c0 + 4 * lane;
+  if (st.full) out = gram_load<true>(st.src, row, c, st.d);
+  else out = gram_load<false>(st.src, row, c, st.d);
+}
+
+// The row a producer lane loads for row `row` of a whole stage: a padding
+// row (at or beyond n) loads the reference row again (an L2 hit; its values
+// are replaced by 0), so that every load is issued unconditionally and the
+// compiler can count the loads in flight.
+template <bool PAD>
+__device__ __forceinline__ int load_row(int row, int n, int ref) {
+  return (PAD && row >= n) ? ref : row;
+}
+
+// Issue the loads of stage st: producer wave pw's rows into v, the reference
+// row into vr. WHOLE: st is a full stage, every load unconditional.
+template <int NB, bool PAD, bool WHOLE, class Src>
+__device__ __forceinline__ void gram_issue(const StageRef<Src>& st, int n, int ref, int pw,
+                                           int lane, f4* v, f4& vr) {
   using S = GramShape<NB>;
-  const int64_t c = c0 + 4 * lane;
-  auto load = [&](int row, f4& out) {
-    const float* p = src.row(row) + c;
-    float t[4];
-    if constexpr (FULL) {
-      load_w<4>(p, t);
+  const int64_t c = st.c0 + 4 * lane;
+#pragma unroll
+  for (int i = 0; i < S::RPW; ++i) {
+    const int row = pw * S::RPW + i;  // wave-uniform
+    if constexpr (WHOLE) v[i] = gram_load<true>(st.src, load_row<PAD>(row, n, ref), c, st.d);
+    else if (!PAD || row < n) stage_load(st, row, lane, v[i]);
+  }
+  if constexpr (WHOLE) vr = gram_load<true>(st.src, ref, c, st.d);
+  else stage_load(st, ref, lane, vr);
+}
+
+// Per-row maxima of P values per lane (P a power of two, at most 16) over the
+// whole wave, transposed: each step pairs a lane with one whose lane bit s
+// differs (xor 1, xor 2 by quad permutes, then rotations by 4 and 8 within a
+// row of 16 lanes, which also pair opposite bits), and every lane keeps the
+// half of its values that its bit s selects, so the count halves per step.
+// Then the four rows of 16 lanes are combined by the cross-row swaps. Lane l
+// ends with the maximum of value rho(l) over all 64 lanes, where rho(l) is
+// the bit reversal of l mod P over log2(P) bits.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return static_cast<uint32_t>(
+      __builtin_amdgcn_update_dpp(0, static_cast<int>(x), CTRL, 0xF, 0xF, false));
+}
+
+template <int CTRL, int H>
+__device__ __forceinline__ void transpose_step(uint32_t* m, bool hi) {
+#pragma unroll
+  for (int j = 0; j < H; ++j) {
+    const uint32_t keep = hi ? m[j + H] : m[j];
+    const uint32_t send = hi ? m[j] : m[j + H];
+    const uint32_t got = dpp_u32<CTRL>(send);
+    m[j] = keep > got ? keep : got;
+  }
+}
+
+__device__ __forceinline__ uint32_t max_u32(uint32_t a, uint32_t b) { return a > b ? a : b; }
+
+template <int P>
+__device__ __forceinline__ uint32_t transpose_max(uint32_t* m, int lane) {
+  static_assert(P == 4 || P == 8 || P == 16, "4, 8 or 16 values per lane");
+  transpose_step<0xB1, P / 2>(m, lane & 1);           // quad_perm [1, 0, 3, 2]
+  transpose_step<0x4E, P / 4>(m, (lane >> 1) & 1);    // quad_perm [2, 3, 0, 1]
+  uint32_t u;
+  if constexpr (P >= 8) {
+    transpose_step<0x124, P / 8>(m, (lane >> 2) & 1); // row_ror 4
+    if constexpr (P == 16) {
+      transpose_step<0x128, 1>(m, (lane >> 3) & 1);   // row_ror 8
+      u = m[0];
     } else {
-      if (c + 4 <= d) load_w<4>(p, t); else load_w_tail<4>(p, d - c, t);
+      u = m[0];
+      u = max_u32(u, dpp_u32<0x128>(u));
     }
-    out = f4{t[0], t[1], t[2], t[3]};
-  };
+  } else {
+    u = m[0];
+    u = max_u32(u, dpp_u32<0x124>(u));
+    u = max_u32(u, dpp_u32<0x128>(u));
+  }
+  const auto s16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);  // rows 0 <-> 1, 2 <-> 3
+  u = max_u32(s16[0], s16[1]);
+  const auto s32 = __builtin_amdgcn_permlane32_swap(u, u, false, false);  // halves
+  return max_u32(s32[0], s32[1]);
+}
+
+__host__ __device__ constexpr int bit_reverse(int x, int bits) {
+  int r = 0;
+  for (int b = 0; b < bits; ++b) r |= ((x >> b) & 1) << (bits - 1 - b);
+  return r;
+}
+
+// Bytes `byte` of four 32-bit words, packed low to high.
+__device__ __forceinline__ uint32_t pack_bytes(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
+                                               uint32_t byte) {
+  const uint32_t sel = 0x0c0c0400u | (byte * 0x0101u);  // [s1.byte, s0.byte, 0, 0]
+  const uint32_t lo = __builtin_amdgcn_perm(w1, w0, sel);
+  const uint32_t hi = __builtin_amdgcn_perm(w3, w2, sel);
+  return __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+}
+
+// Y = X - x_ref for producer wave pw's rows (rows at or beyond n are 0),
+// quantized per row into the three digit planes of the stage buffer `lds`
+// and the row's k (see above); with NEXT, as each row is written the load of
+// that row for the full stage `next` is issued into its registers, and the
+// reference row's last.
+template <int NB, bool PAD, bool NEXT, class Src>
+__device__ __forceinline__ void gram_put(uint8_t* __restrict__ lds, int n, int pw, int lane,
+                                         f4* v, f4& vr, int ref, const StageRef<Src>& next) {
+  const int wave = pw;
+  const int64_t cn = next.c0 + 4 * lane;
+  using S = GramShape<NB>;
+  constexpr int P = S::RPW <= 4 ? 4 : (S::RPW <= 8 ? 8 : 16);
+  constexpr int LB = P == 4 ? 2 : (P == 8 ? 3 : 4);
+  int* kexp = reinterpret_cast<int*>(lds + 3 * S::PLANE);
+  uint32_t m[P];
+#pragma unroll
+  for (int i = 0; i < P; ++i) m[i] = 0u;
 #pragma unroll
   for (int i = 0; i < S::RPW; ++i) {
     const int row = wave * S::RPW + i;  // wave-uniform
-    if (!PAD || row < n) load(row, v[i]);
+    v[i] = v[i] - vr;
+    if (PAD && row >= n) v[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    const float a = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(v[i].x), __builtin_fabsf(v[i].y)),
+                                    __builtin_fmaxf(__builtin_fabsf(v[i].z), __builtin_fabsf(v[i].w)));
+    m[i] = __builtin_bit_cast(uint32_t, a);
   }
-  load(ref, vr);
-}
-
-// Y = X - x_ref for this wave's rows into the stage buffer (rows at or beyond
-// n are 0).
-template <int NB, bool PAD>
-__device__ __forceinline__ void gram_put(float* __restrict__ buf, int n, int wave, int lane,
-                                         const f4* v, const f4& vr) {
-  using S = GramShape<NB>;
+  // lane l: the largest |y| of row rho(l) of this wave; its exponent field e8
+  // gives k = min(21 - E, 127) = 148 - max(e8, 21), E = max(e8, 1) - 127
+  const uint32_t mx = transpose_max<P>(m, lane);
+  const int e8 = static_cast<int>(mx >> 23);
+  const int kl = 148 - (e8 > 21 ? e8 : 21);
+  const int mine = bit_reverse(lane & (P - 1), LB);
+  if (lane < P && mine < S::RPW) kexp[wave * S::RPW + mine] = kl;
 #pragma unroll
   for (int i = 0; i < S::RPW; ++i) {
-    const int row = wave * S::RPW + i;  // wave-uniform
-    f4 t = v[i] - vr;
-    if (PAD && row >= n) t = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    *reinterpret_cast<f4*>(buf + row * kGramPitch + 4 * lane) = t;
+    const int row = wave * S::RPW + i;
+    const int k = __builtin_amdgcn_readlane(kl, bit_reverse(i, LB));
+    const float scale = __builtin_bit_cast(float, static_cast<uint32_t>(k + 127) << 23);
+    uint32_t w[4];
+    w[0] = __builtin_bit_cast(uint32_t, __builtin_fmaf(v[i].x, scale, kRoundMagic));
+    w[1] = __builtin_bit_cast(uint32_t, __builtin_fmaf(v[i].y, scale, kRoundMagic));
+    w[2] = __builtin_bit_cast(uint32_t, __builtin_fmaf(v[i].z, scale, kRoundMagic));
+    w[3] = __builtin_bit_cast(uint32_t, __builtin_fmaf(v[i].w, scale, kRoundMagic));
+    // the low 22 bits of w are those of q (w = bits(1.5 * 2^23 + q)); the
+    // constant's bit 22 is taken out where the third byte is read
+    const uint32_t pc = pack_bytes(w[0], w[1], w[2], w[3], 0);
+    const uint32_t pb = pack_bytes(w[0] + 128u, w[1] + 128u, w[2] + 128u, w[3] + 128u, 1);
+    constexpr uint32_t kA = 32896u - 4194304u;  // + 32896, minus the constant's 2^22
+    const uint32_t pa = pack_bytes(w[0] + kA, w[1] + kA, w[2] + kA, w[3] + kA, 2);
+    const int off = row * kPlanePitch + 4 * lane;
+    *reinterpret_cast<uint32_t*>(lds + off) = pa;
+    *reinterpret_cast<uint32_t*>(lds + S::PLANE + off) = pb;
+    *reinterpret_cast<uint32_t*>(lds + 2 * S::PLANE + off) = pc;
+    if constexpr (NEXT) v[i] = gram_load<true>(next.src, load_row<PAD>(row, n, ref), cn, next.d);
   }
+  if constexpr (NEXT) vr = gram_load<true>(next.src, ref, cn, next.d);
 }
 
-// Pairs I, I + 1, ... of this wave (pair q = 2I + PH) over two consecutive
-// 16-coordinate groups (fragments y0, y1): per pair a chain of eight MFMAs (32
-// products) from zero, then one addition into fp64. Two pairs at a time, their
-// chains interleaved, so that no MFMA waits on the one issued just before it.
-// A template recursion, so that every pair's blocks are compile-time
-// constants (the fragments stay in fixed registers).
-template <int NB, int Q>
-__device__ __forceinline__ void gram_flush(const f4& acc, double* acc64) {
-  (void)Q;
-  acc64[0] += static_cast<double>(acc.x);
-  acc64[1] += static_cast<double>(acc.y);
-  acc64[2] += static_cast<double>(acc.z);
-  acc64[3] += static_cast<double>(acc.w);
+__device__ __forceinline__ i4 mfma_i8(const i4& a, const i4& b, const i4& c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
 }
 
-template <int NB, int PH, int I>
-__device__ __forceinline__ void gram_pairs(const f4* y0, const f4* y1, double (*acc64)[4]) {
+// The nine digit products of block pair q = CV + 4P of consumer wave CV
+// (and of its later pairs, by recursion: every pair's blocks, and with them
+// its fragment registers, are compile-time constants).
+template <int NB, int CV, int P>
+__device__ __forceinline__ void gram_pair_mfma(const i4* fa, const i4* fb, const i4* fc,
+                                               i4 (*acc)[5]) {
   using S = GramShape<NB>;
-  constexpr int q = 2 * I + PH;
-  constexpr int q2 = 2 * (I + 1) + PH;
-  const f4 zero = f4{0.0f, 0.0f, 0.0f, 0.0f};
-  if constexpr (I + 1 < S::PPW && q2 < S::NBP) {
-    constexpr int a1 = pair_b1(NB, q), a2 = pair_b2(NB, q);
-    constexpr int c1 = pair_b1(NB, q2), c2 = pair_b2(NB, q2);
-    f4 u = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[a1].x, y0[a2].x, zero, 0, 0, 0);
-    f4 w = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[c1].x, y0[c2].x, zero, 0, 0, 0);
-    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[a1].y, y0[a2].y, u, 0, 0, 0);
-    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[c1].y, y0[c2].y, w, 0, 0, 0);
-    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[a1].z, y0[a2].z, u, 0, 0, 0);
-    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[c1].z, y0[c2].z, w, 0, 0, 0);
-    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[a1].w, y0[a2].w, u, 0, 0, 0);
-    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[c1].w, y0[c2].w, w, 0, 0, 0);
-    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[a1].x, y1[a2].x, u, 0, 0, 0);
-    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[c1].x, y1[c2].x, w, 0, 0, 0);
-    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[a1].y, y1[a2].y, u, 0, 0, 0);
-    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[c1].y, y1[c2].y, w, 0, 0, 0);
-    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[a1].z, y1[a2].z, u, 0, 0, 0);
-    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[c1].z, y1[c2].z, w, 0, 0, 0);
-    u = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[a1].w, y1[a2].w, u, 0, 0, 0);
-    w = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[c1].w, y1[c2].w, w, 0, 0, 0);
-    gram_flush<NB, q>(u, acc64[I]);
-    gram_flush<NB, q2>(w, acc64[I + 1]);
-    gram_pairs<NB, PH, I + 2>(y0, y1, acc64);
-  } else if constexpr (I < S::PPW && q < S::NBP) {
+  constexpr int q = CV + 4 * P;
+  if constexpr (P < S::PPW && q < S::NBP) {
     constexpr int b1 = pair_b1(NB, q), b2 = pair_b2(NB, q);
-    f4 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[b1].x, y0[b2].x, zero, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[b1].y, y0[b2].y, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[b1].z, y0[b2].z, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y0[b1].w, y0[b2].w, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[b1].x, y1[b2].x, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[b1].y, y1[b2].y, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[b1].z, y1[b2].z, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(y1[b1].w, y1[b2].w, acc, 0, 0, 0);
-    gram_flush<NB, q>(acc, acc64[I]);
+    i4* A = acc[P];
+    A[0] = mfma_i8(fa[b1], fa[b2], A[0]);
+    A[1] = mfma_i8(fa[b1], fb[b2], A[1]);
+    A[2] = mfma_i8(fa[b1], fc[b2], A[2]);
+    A[1] = mfma_i8(fb[b1], fa[b2], A[1]);
+    A[2] = mfma_i8(fb[b1], fb[b2], A[2]);
+    A[3] = mfma_i8(fb[b1], fc[b2], A[3]);
+    A[2] = mfma_i8(fc[b1], fa[b2], A[2]);
+    A[3] = mfma_i8(fc[b1], fb[b2], A[3]);
+    A[4] = mfma_i8(fc[b1], fc[b2], A[4]);
+    gram_pair_mfma<NB, CV, P + 1>(fa, fb, fc, acc);
   }
 }
 
-// This wave's half h of the stage in `buf`, block pairs of parity PH.
-template <int NB, int PH>
-__device__ __forceinline__ void gram_multiply(const float* __restrict__ buf, int h, int g, int r,
-                                              double (*acc64)[4]) {
+// The exact stage value of each G entry of pair q = CV + 4P (and later
+// pairs) added into acc64 (lane l, component e: row 16*b1 + 4*(l/16) + e,
+// column 16*b2 + l%16).
+template <int NB, int CV, int P>
+__device__ __forceinline__ void gram_pair_flush(const int* kexp, int g, int r,
+                                                const i4 (*acc)[5], double (*acc64)[4]) {
+  using S = GramShape<NB>;
+  constexpr int q = CV + 4 * P;
+  if constexpr (P < S::PPW && q < S::NBP) {
+    constexpr int b1 = pair_b1(NB, q), b2 = pair_b2(NB, q);
+    const i4 kr = *reinterpret_cast<const i4*>(kexp + 16 * b1 + 4 * g);
+    const int kc = kexp[16 * b2 + r];
+    const i4* A = acc[P];
 #pragma unroll
-  for (int grp = 0; grp < 8; grp += 2) {
-    const int col = 128 * h + 16 * grp + 4 * g;
-    f4 y0[NB], y1[NB];
+    for (int e = 0; e < 4; ++e) {
+      double t = static_cast<double>(A[0][e]);
+      t = __builtin_fma(t, 256.0, static_cast<double>(A[1][e]));
+      t = __builtin_fma(t, 256.0, static_cast<double>(A[2][e]));
+      t = __builtin_fma(t, 256.0, static_cast<double>(A[3][e]));
+      t = __builtin_fma(t, 256.0, static_cast<double>(A[4][e]));
+      acc64[P][e] += __builtin_ldexp(t, -(kr[e] + kc));
+    }
+    gram_pair_flush<NB, CV, P + 1>(kexp, g, r, acc, acc64);
+  }
+}
+
+// Consumer wave CV's block pairs over the stage in the buffer `lds`: the
+// nine digit products of each pair into its five weight accumulators, chunk
+// by chunk, then the stage's exact G entries added into acc64.
+template <int NB, int CV>
+__device__ __forceinline__ void gram_multiply(const uint8_t* __restrict__ lds, int g, int r,
+                                              double (*acc64)[4]) {
+  using S = GramShape<NB>;
+  const int* kexp = reinterpret_cast<const int*>(lds + 3 * S::PLANE);
+  i4 acc[S::PPW][5];
+  const i4 zero = i4{0, 0, 0, 0};
+#pragma unroll
+  for (int p = 0; p < S::PPW; ++p)
+#pragma unroll
+    for (int t = 0; t < 5; ++t) acc[p][t] = zero;
+#pragma unroll
+  for (int ch = 0; ch < kGramStage / 64; ++ch) {
+    i4 fa[NB], fb[NB], fc[NB];  // digit fragments a, b, c of every block
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      y0[b] = *reinterpret_cast<const f4*>(buf + (16 * b + r) * kGramPitch + col);
-      y1[b] = *reinterpret_cast<const f4*>(buf + (16 * b + r) * kGramPitch + col + 16);
+      const int off = (16 * b + r) * kPlanePitch + 64 * ch + 16 * g;
+      fa[b] = *reinterpret_cast<const i4*>(lds + off);
+      fb[b] = *reinterpret_cast<const i4*>(lds + S::PLANE + off);
+      fc[b] = *reinterpret_cast<const i4*>(lds + 2 * S::PLANE + off);
     }
-    gram_pairs<NB, PH, 0>(y0, y1, acc64);
+    gram_pair_mfma<NB, CV, 0>(fa, fb, fc, acc);
   }
-}
-
-// The stages of this workgroup: load, stage in LDS, multiply. Workgroups
-// 0 .. G-1 take the full stages b, b + G, ...; when kGramStage does not divide
-// d, one more workgroup (b = G) takes the partial last stage alone, so that the
-// loop over full stages carries no tail handling.
-template <int NB, bool PAD, int PH>
-__device__ __forceinline__ void gram_tile(const float* __restrict__ x, int n, int64_t d, int ref,
-                                          int wave, float* __restrict__ buf, double (*acc64)[4]) {
-  using S = GramShape<NB>;
-  const int lane = threadIdx.x & 63;
-  const int g = lane >> 4, r = lane & 15;
-  const int64_t full = d / kGramStage;  // full stages
-  const int64_t b = blockIdx.x;
-  const int64_t G = gridDim.x - (full * kGramStage < d ? 1 : 0);
-  f4 v[S::RPW];
-  f4 vr;
-  if (b == G) {
-    gram_issue<NB, PAD, false>(MatrixRows{x, d}, n, d, ref, wave, lane, full * kGramStage, v, vr);
-    lds_barrier();
-    gram_put<NB, PAD>(buf, n, wave, lane, v, vr);
-    lds_barrier();
-    gram_multiply<NB, PH>(buf, wave & 1, g, r, acc64);
-    return;
-  }
-  const int64_t mine = (full > b) ? (full - b + G - 1) / G : 0;
-  if (mine > 0)
-    gram_issue<NB, PAD, true>(MatrixRows{x, d}, n, d, ref, wave, lane, b * kGramStage, v, vr);
-  for (int64_t k = 0; k < mine; ++k) {
-    lds_barrier();                    // every wave is done with the previous stage
-    gram_put<NB, PAD>(buf, n, wave, lane, v, vr);
-    if (k + 1 < mine)                 // in flight during the multiply below
-      gram_issue<NB, PAD, true>(MatrixRows{x, d}, n, d, ref, wave, lane,
-                                (b + (k + 1) * G) * kGramStage, v, vr);
-    lds_barrier();                    // the whole stage is in LDS
-    gram_multiply<NB, PH>(buf, wave & 1, g, r, acc64);
-  }
+  gram_pair_flush<NB, CV, 0>(kexp, g, r, acc, acc64);
 }
 
 // Partials of a workgroup: entry q*256 + row*16 + col holds
-// G[16*b1 + row][16*b2 + col] (MFMA output: lane l, component e is row
-// 4*(l/16) + e, column l%16); the two halves of pair q are held by waves
-// 2*(q%2) (h = 0) and 2*(q%2) + 1 and added half 0 first. out[entry * stride].
-template <int NB>
-__device__ __forceinline__ void gram_write_partials(const double (*acc64)[4], float* buf, int wave,
-                                                    int g, int r, double* __restrict__ out,
-                                                    int64_t stride) {
+// G[16*b1 + row][16*b2 + col]; consumer wave c holds pairs q = c, c + 4, ...
+// (MFMA output: lane l, component e is row 4*(l/16) + e, column l%16).
+// out[entry * stride].
+template <int NB, int CV>
+__device__ __forceinline__ void gram_write_partials(const double (*acc64)[4], int g, int r,
+                                                    double* __restrict__ out, int64_t stride) {
   using S = GramShape<NB>;
-  __syncthreads();
-  double* red = reinterpret_cast<double*>(buf);  // 2 x 256 doubles (4 KB <= buf)
-  const int t = threadIdx.x;
 #pragma unroll
-  for (int q = 0; q < S::NBP; ++q) {
-    if ((wave >> 1) == (q & 1)) {
+  for (int p = 0; p < S::PPW; ++p) {
+    const int q = CV + 4 * p;  // entries only: no register choice depends on q
+    if (q < S::NBP) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) red[(wave & 1) * 256 + (4 * g + e) * 16 + r] = acc64[q / 2][e];
+      for (int e = 0; e < 4; ++e) out[(q * 256 + (4 * g + e) * 16 + r) * stride] = acc64[p][e];
     }
-    __syncthreads();
-    out[(q * 256 + t) * stride] = red[t] + red[256 + t];
-    __syncthreads();
   }
 }
 
-template <int NB, bool PAD>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2)))
-void k_dist_gram(const float* __restrict__ x, int n, int64_t d,
-                 const int32_t* __restrict__ ref_idx, double* __restrict__ partial) {
+// A batch of segments for one Gram table launch (by value in the kernel
+// arguments): ffirst[s] = full stages before segment s (ffirst[count] = all
+// of them), pfirst[s] = partial stages before segment s (pfirst[count] = all
+// of them), and each segment's length.
+struct GramSegs {
+  int count;
+  int32_t ffirst[kSegMax + 1];
+  int32_t pfirst[kSegMax + 1];
+  int64_t dims[kSegMax];
+};
+
+// The schedule of a workgroup. Its stages are entries b, b + G, ... of a list
+// that holds every full stage first and then the partial ones (G = grid
+// size, one workgroup per CU), `cnt` entries of which the first `nf` are
+// full. In iteration i the producers quantize entry i into buffer i % 2 and
+// the consumers multiply entry i - 1 from buffer (i - 1) % 2; a barrier
+// ends every iteration. Iterations run two at a time while both entries are
+// full stages, with every load unconditional (so the compiler keeps the
+// next stages' loads in flight across the quantizing); the rest (the last
+// full stage when nf is odd, the partial stages and the final multiply) go
+// one at a time with guarded loads.
+
+// Consumer wave CV, then its partials.
+template <int NB, int CV>
+__device__ __forceinline__ void gram_consume(const uint8_t* __restrict__ lds, int64_t cnt,
+                                             int64_t nf, double* __restrict__ out,
+                                             int64_t stride) {
   using S = GramShape<NB>;
-  __shared__ __attribute__((aligned(16))) float buf[S::ROWS * kGramPitch];
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, r = lane & 15;
-  const int ref = *ref_idx;
   double acc64[S::PPW][4];
 #pragma unroll
   for (int i = 0; i < S::PPW; ++i)
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc64[i][e] = 0.0;
-  if (wave < 2) gram_tile<NB, PAD, 0>(x, n, d, ref, wave, buf, acc64);
-  else gram_tile<NB, PAD, 1>(x, n, d, ref, wave, buf, acc64);
-  gram_write_partials<NB>(acc64, buf, wave, g, r, partial + blockIdx.x, gridDim.x);
+  int64_t t = 0;
+  if (nf >= 2) {
+    for (; t + 1 < nf; t += 2) {
+      if (t >= 1) gram_multiply<NB, CV>(lds + S::BUF, g, r, acc64);  // entry t - 1
+      lds_barrier();
+      gram_multiply<NB, CV>(lds, g, r, acc64);                       // entry t
+      lds_barrier();
+    }
+  }
+  for (int64_t i = t; i <= cnt; ++i) {
+    if (i >= 1) gram_multiply<NB, CV>(lds + ((i - 1) & 1) * S::BUF, g, r, acc64);
+    lds_barrier();
+  }
+  gram_write_partials<NB, CV>(acc64, g, r, out, stride);
+}
+
+// Producer wave pw. `list.entry(i)` is this workgroup's i-th stage.
+template <int NB, bool PAD, class List>
+__device__ __forceinline__ void gram_produce(uint8_t* __restrict__ lds, int64_t cnt, int64_t nf,
+                                             int n, int ref, int pw, const List& list) {
+  using S = GramShape<NB>;
+  const int lane = threadIdx.x & 63;
+  f4 va[S::RPW], vb[S::RPW];
+  f4 ra, rb;
+  int64_t t = 0;
+  if (nf >= 2) {
+    // entries past the last full one load that one again (not used)
+    auto whole = [&](int64_t i) { return list.entry(i < nf ? i : nf - 1); };
+    gram_issue<NB, PAD, true>(whole(0), n, ref, pw, lane, va, ra);
+    gram_issue<NB, PAD, true>(whole(1), n, ref, pw, lane, vb, rb);
+    for (; t + 1 < nf; t += 2) {
+      gram_put<NB, PAD, true>(lds, n, pw, lane, va, ra, ref, whole(t + 2));
+      lds_barrier();
+      gram_put<NB, PAD, true>(lds + S::BUF, n, pw, lane, vb, rb, ref, whole(t + 3));
+      lds_barrier();
+    }
+  }
+  for (int64_t i = t; i <= cnt; ++i) {
+    if (i < cnt) {
+      const auto st = list.entry(i);
+      gram_issue<NB, PAD, false>(st, n, ref, pw, lane, va, ra);
+      gram_put<NB, PAD, false>(lds + (i & 1) * S::BUF, n, pw, lane, va, ra, ref, st);
+    }
+    lds_barrier();
+  }
+}
+
+template <int NB, bool PAD, class List>
+__device__ __forceinline__ void gram_run(uint8_t* __restrict__ lds, int64_t cnt, int64_t nf,
+                                         int n, int ref, const List& list,
+                                         double* __restrict__ out, int64_t stride) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  // the roles are compile-time per wave, so that every consumer's block
+  // pairs, and with them its fragment registers, are constants
+  switch (wave) {
+    case 4: gram_consume<NB, 0>(lds, cnt, nf, out, stride); break;
+    case 5: gram_consume<NB, 1>(lds, cnt, nf, out, stride); break;
+    case 6: gram_consume<NB, 2>(lds, cnt, nf, out, stride); break;
+    case 7: gram_consume<NB, 3>(lds, cnt, nf, out, stride); break;
+    default: gram_produce<NB, PAD>(lds, cnt, nf, n, ref, wave, list); break;
+  }
+}
+
+// Entries of workgroup b among `total` list entries of which the first
+// `nfull` are full stages: (count, full count).
+__device__ __forceinline__ void gram_share(int64_t total, int64_t nfull, int64_t* cnt,
+                                           int64_t* nf) {
+  const int64_t b = blockIdx.x, G = gridDim.x;
+  *cnt = total > b ? (total - b + G - 1) / G : 0;
+  *nf = nfull > b ? (nfull - b + G - 1) / G : 0;
+}
+
+// The stages of an n x d matrix: full stage s at coordinate 256 s, then the
+// partial last one (when 256 does not divide d).
+struct MatrixStages {
+  const float* x;
+  int64_t d;
+  int64_t nfull;
+  __device__ __forceinline__ StageRef<MatrixRows> entry(int64_t i) const {
+    const int64_t li = blockIdx.x + i * gridDim.x;  // list index (the partial stage is last)
+    return StageRef<MatrixRows>{MatrixRows{x, d}, li * kGramStage, d, li < nfull};
+  }
+};
+
+template <int NB, bool PAD>
+__global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void k_dist_gram(const float* __restrict__ x, int n, int64_t d,
+                 const int32_t* __restrict__ ref_idx, double* __restrict__ partial) {
+  using S = GramShape<NB>;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[S::LDS];
+  const int ref = *ref_idx;
+  const int64_t nfull = d / kGramStage;
+  const int64_t total = (d + kGramStage - 1) / kGramStage;
+  int64_t cnt, nf;
+  gram_share(total, nfull, &cnt, &nf);
+  gram_run<NB, PAD>(lds, cnt, nf, n, ref, MatrixStages{x, d, nfull}, partial + blockIdx.x,
+                    gridDim.x);
 }
 
 // ---------------------------------------------------------------------------
 // The Gram engine over a table of segments (segment s of vector i at
-// ptrs[s * n + i], dims[s] floats): the stages of all segments of the launch
-// form one list (segment s owns stages tab.first[s] .. tab.first[s+1]-1, the
-// last one partial when 256 does not divide dims[s]), and workgroup b takes
-// stages b, b + G, ... of it, each with its segment's rows. One reference row
-// index serves every segment (D is the same whatever row each coordinate is
-// shifted by). Tile b of the launch writes column tile_base + b of partials
-// with `tiles` columns in all.
-template <int NB, bool PAD, int PH>
-__device__ __forceinline__ void gram_tile_table(const float* const* __restrict__ ptrs,
-                                                const SegTable& tab, int n, int ref, int wave,
-                                                float* __restrict__ buf, double (*acc64)[4]) {
-  using S = GramShape<NB>;
-  const int lane = threadIdx.x & 63;
-  const int g = lane >> 4, r = lane & 15;
-  const int64_t G = gridDim.x;
-  const int64_t total = tab.first[tab.count];
-  auto issue = [&](int64_t stage, f4* v, f4& vr) {
-    const int sg = seg_of(tab, static_cast<int>(stage));
-    const int64_t c0 = (stage - tab.first[sg]) * kGramStage;
-    const int64_t d = tab.dims[sg];
-    const TableRows src{ptrs + static_cast<int64_t>(sg) * n};
-    if (c0 + kGramStage <= d) gram_issue<NB, PAD, true>(src, n, d, ref, wave, lane, c0, v, vr);
-    else gram_issue<NB, PAD, false>(src, n, d, ref, wave, lane, c0, v, vr);
-  };
-  f4 v[S::RPW];
-  f4 vr;
-  int64_t stage = blockIdx.x;
-  if (stage < total) issue(stage, v, vr);
-  for (; stage < total; stage += G) {
-    lds_barrier();  // every wave is done with the previous stage
-    gram_put<NB, PAD>(buf, n, wave, lane, v, vr);
-    if (stage + G < total) issue(stage + G, v, vr);  // in flight during the multiply
-    lds_barrier();  // the whole stage is in LDS
-    gram_multiply<NB, PH>(buf, wave & 1, g, r, acc64);
+// ptrs[s * n + i], dims[s] floats). The list of a launch holds the full
+// stages of all its segments in segment order (segment s owns list entries
+// ffirst[s] .. ffirst[s+1]-1), then the partial last stage of every segment
+// whose length 256 does not divide (entries nfull + pfirst[s] for those),
+// and workgroup b takes entries b, b + G, ..., each with its segment's rows.
+// One reference row index serves every segment (D is the same whatever row
+// each coordinate is shifted by). Tile b of the launch writes column
+// tile_base + b of partials with `tiles` columns in all.
+__device__ __forceinline__ int last_le(const int32_t* first, int count, int64_t v) {
+  int lo = 0, hi = count - 1;  // the last s with first[s] <= v
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (first[mid] <= v) lo = mid;
+    else hi = mid - 1;
   }
+  return lo;
 }
 
+struct TableStages {
+  const float* const* ptrs;
+  int n;
+  const GramSegs* segs;
+  __device__ __forceinline__ StageRef<TableRows> entry(int64_t i) const {
+    const GramSegs& t = *segs;
+    const int64_t li = blockIdx.x + i * gridDim.x;
+    const int64_t nfull = t.ffirst[t.count];
+    if (li < nfull) {
+      const int sg = last_le(t.ffirst, t.count, li);
+      return StageRef<TableRows>{TableRows{ptrs + static_cast<int64_t>(sg) * n},
+                                 (li - t.ffirst[sg]) * kGramStage, t.dims[sg], true};
+    }
+    // the partial stages: segment sg is the last with pfirst[sg] <= j (and
+    // has one, since pfirst grows exactly at the segments that have one)
+    const int sg = last_le(t.pfirst, t.count, li - nfull);
+    const int64_t c0 = (t.dims[sg] / kGramStage) * kGramStage;
+    return StageRef<TableRows>{TableRows{ptrs + static_cast<int64_t>(sg) * n}, c0, t.dims[sg],
+                               false};
+  }
+};
+
 template <int NB, bool PAD>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2)))
-void k_dist_gram_table(const float* const* __restrict__ ptrs, SegTable tab, int n,
+__global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void k_dist_gram_table(const float* const* __restrict__ ptrs, GramSegs segs, int n,
                        const int32_t* __restrict__ ref_idx, int64_t tile_base, int64_t tiles,
                        double* __restrict__ partial) {
   using S = GramShape<NB>;
-  __shared__ __attribute__((aligned(16))) float buf[S::ROWS * kGramPitch];
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  const int g = lane >> 4, r = lane & 15;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[S::LDS];
   const int ref = *ref_idx;
-  double acc64[S::PPW][4];
-#pragma unroll
-  for (int i = 0; i < S::PPW; ++i)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) acc64[i][e] = 0.0;
-  if (wave < 2) gram_tile_table<NB, PAD, 0>(ptrs, tab, n, ref, wave, buf, acc64);
-  else gram_tile_table<NB, PAD, 1>(ptrs, tab, n, ref, wave, buf, acc64);
-  gram_write_partials<NB>(acc64, buf, wave, g, r, partial + tile_base + blockIdx.x, tiles);
+  const int64_t nfull = segs.ffirst[segs.count];
+  const int64_t total = nfull + segs.pfirst[segs.count];
+  int64_t cnt, nf;
+  gram_share(total, nfull, &cnt, &nf);
+  gram_run<NB, PAD>(lds, cnt, nf, n, ref, TableStages{ptrs, n, &segs},
+                    partial + tile_base + blockIdx.x, tiles);
 }
 
 // ---------------------------------------------------------------------------
@@ -570,10 +820,10 @@ template <int NB>
 hipError_t launch_gram_nb(const float* x, const DistPlan& p, const int32_t* ref, double* partial,
                           hipStream_t s) {
   if (p.n < 16 * NB)
-    launch("dist_gram", k_dist_gram<NB, true>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock),
+    launch("dist_gram", k_dist_gram<NB, true>, dim3(static_cast<unsigned>(p.tiles)), dim3(kGramThreads),
            0, s, x, p.n, p.d, ref, partial);
   else
-    launch("dist_gram", k_dist_gram<NB, false>, dim3(static_cast<unsigned>(p.tiles)), dim3(kBlock),
+    launch("dist_gram", k_dist_gram<NB, false>, dim3(static_cast<unsigned>(p.tiles)), dim3(kGramThreads),
            0, s, x, p.n, p.d, ref, partial);
   return hipGetLastError();
 }
@@ -596,13 +846,13 @@ int device_cus() {
 template <int NB>
 int gram_blocks_per_cu_nb() {
   int blocks = 0, blocks_pad = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_dist_gram<NB, false>, kBlock, 0) !=
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_dist_gram<NB, false>, kGramThreads, 0) !=
           hipSuccess ||
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks_pad, k_dist_gram<NB, true>, kBlock,
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks_pad, k_dist_gram<NB, true>, kGramThreads,
                                                    0) != hipSuccess ||
       blocks <= 0) {
     (void)hipGetLastError();
-    return 2;
+    return 1;
   }
   return blocks < blocks_pad ? blocks : blocks_pad;  // the grid fits either variant
 }
@@ -626,13 +876,13 @@ int gram_blocks_per_cu(int nb) {
 template <int NB>
 int gram_table_blocks_per_cu_nb() {
   int blocks = 0, blocks_pad = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_dist_gram_table<NB, false>, kBlock,
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_dist_gram_table<NB, false>, kGramThreads,
                                                    0) != hipSuccess ||
       hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks_pad, k_dist_gram_table<NB, true>,
-                                                   kBlock, 0) != hipSuccess ||
+                                                   kGramThreads, 0) != hipSuccess ||
       blocks <= 0) {
     (void)hipGetLastError();
-    return 2;
+    return 1;
   }
   return blocks < blocks_pad ? blocks : blocks_pad;
 }
@@ -658,18 +908,20 @@ hipError_t for_each_gram_launch(int n, const int64_t* dims, int K, F&& f) {
   const int nb = (n + 15) / 16;
   const int64_t slots = static_cast<int64_t>(device_cus()) * gram_table_blocks_per_cu(nb);
   for (int g0 = 0; g0 < K; g0 += kSegMax) {
-    SegTable tab{};
+    GramSegs tab{};
     tab.count = K - g0 < kSegMax ? K - g0 : kSegMax;
-    int64_t total = 0;
+    int64_t full = 0, part = 0;
     for (int sg = 0; sg < tab.count; ++sg) {
-      tab.first[sg] = static_cast<int32_t>(total);
-      tab.span[sg] = kGramStage;
+      tab.ffirst[sg] = static_cast<int32_t>(full);
+      tab.pfirst[sg] = static_cast<int32_t>(part);
       tab.dims[sg] = dims[g0 + sg];
-      tab.outs[sg] = nullptr;
-      total += (dims[g0 + sg] + kGramStage - 1) / kGramStage;
-      if (total > 0x7fffffff) return hipErrorInvalidValue;
+      full += dims[g0 + sg] / kGramStage;
+      part += dims[g0 + sg] % kGramStage != 0 ? 1 : 0;
+      if (full + part > 0x7fffffff) return hipErrorInvalidValue;
     }
-    tab.first[tab.count] = static_cast<int32_t>(total);
+    tab.ffirst[tab.count] = static_cast<int32_t>(full);
+    tab.pfirst[tab.count] = static_cast<int32_t>(part);
+    const int64_t total = full + part;
     if (total == 0) continue;
     const hipError_t e = f(g0, tab, total < slots ? total : slots);
     if (e != hipSuccess) return e;
@@ -678,15 +930,15 @@ hipError_t for_each_gram_launch(int n, const int64_t* dims, int K, F&& f) {
 }
 
 template <int NB>
-hipError_t launch_gram_table_nb(const float* const* ptrs, int n, const SegTable& tab,
+hipError_t launch_gram_table_nb(const float* const* ptrs, int n, const GramSegs& tab,
                                 int64_t groups, const int32_t* ref, int64_t base, int64_t tiles,
                                 double* partial, hipStream_t s) {
   if (n < 16 * NB)
     launch("dist_gram_table", k_dist_gram_table<NB, true>, dim3(static_cast<unsigned>(groups)),
-           dim3(kBlock), 0, s, ptrs, tab, n, ref, base, tiles, partial);
+           dim3(kGramThreads), 0, s, ptrs, tab, n, ref, base, tiles, partial);
   else
     launch("dist_gram_table", k_dist_gram_table<NB, false>, dim3(static_cast<unsigned>(groups)),
-           dim3(kBlock), 0, s, ptrs, tab, n, ref, base, tiles, partial);
+           dim3(kGramThreads), 0, s, ptrs, tab, n, ref, base, tiles, partial);
   return hipGetLastError();
 }
 
@@ -696,7 +948,7 @@ int g_direct_max_n = 20;
 
 int64_t table_gram_tiles(const int64_t* dims, int K, int n) {
   int64_t tiles = 0;
-  const hipError_t e = for_each_gram_launch(n, dims, K, [&](int, const SegTable&, int64_t groups) {
+  const hipError_t e = for_each_gram_launch(n, dims, K, [&](int, const GramSegs&, int64_t groups) {
     tiles += groups;
     return hipSuccess;
   });
@@ -740,7 +992,7 @@ hipError_t enqueue_distances_table_gram(const float* const* ptrs, int n, const i
   const int32_t* ref = table_reference_slot(probe_space);
   int64_t base = 0;
   const int nb = (n + 15) / 16;
-  return for_each_gram_launch(n, dims, K, [&](int g0, const SegTable& tab, int64_t groups) {
+  return for_each_gram_launch(n, dims, K, [&](int g0, const GramSegs& tab, int64_t groups) {
     const float* const* p = ptrs + static_cast<int64_t>(g0) * n;
     hipError_t r;
     switch (nb) {
@@ -788,15 +1040,14 @@ DistPlan plan_distances(int n, int64_t d, const float* x) {
     p.engine = kEngineGram;
     p.width = 4;  // 16-byte loads of 1 KB row runs
     // As many workgroups as the device holds resident (at most one per
-    // stage); workgroup b takes stages b, b + tiles, ...
+    // stage); workgroup b takes stages b, b + tiles, ... (the partial last
+    // stage, if any, among them).
     const int nb = (n + 15) / 16;
-    // The partial last stage, if any, takes one workgroup of its own.
     const int64_t slots = static_cast<int64_t>(device_cus()) * gram_blocks_per_cu(nb);
-    const int64_t full = d / kGramStage;
-    const int64_t tail = full * kGramStage < d ? 1 : 0;
+    const int64_t stages = (d + kGramStage - 1) / kGramStage;
     p.chunk = kGramStage;
     p.entries = nb * (nb + 1) / 2 * 256;
-    p.tiles = (full < slots - tail ? full : slots - tail) + tail;
+    p.tiles = stages < slots ? stages : slots;
     return p;
   }
   p.tiles = (d + p.chunk - 1) / p.chunk;

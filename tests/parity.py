@@ -7,13 +7,19 @@ rounding inside a tile (everything across tiles is fp64). Per entry:
   an fp32 accumulator with one fused multiply-add each, after one rounded
   fp32 subtraction; for positive terms that is a relative error of at most
   (16 + 2) u, u = 2^-24.
-* Gram engine: Y = X - x_ref is rounded once (relative u on every y), and each
-  fp32 accumulator sums at most 8 MFMA k-slices of 4 products (P = 32
-  products, counted as up to P roundings, each at most u times the running
-  sum of absolute products) before it is added in fp64. With
-  N_i = ||x_i - x_ref||^2 and sum |y_i y_j| <= (N_i + N_j)/2:
-  |dG_ij| <= (P/2) u (N_i + N_j) + u (N_i + N_j) and |dN_i| <= P u N_i + 2u N_i,
-  so |dD_ij| <= (2P + 4) u (N_i + N_j).
+* Gram engine: y = fl(x - x_ref) is rounded once (|error| <= u |y|), and each
+  row's y over a stage of 256 coordinates (counted from the start of the
+  vector, or of each segment of a segment table) is rounded to a multiple of
+  2^-k, k = min(21 - E, 127) with E the exponent of the stage's largest |y|
+  (-126 when that is 0 or subnormal): an error of at most 2^-k / 2. With
+  e_i = || u |y_i| + 2^-k / 2 || (over all coordinates), the products of the
+  quantized values are exact, so the stage sums are the exact Gram entries of
+  the quantized rows and D~_ij = ||y~_i - y~_j||^2 exactly, up to the fp64
+  accumulation: |D~_ij - D_ij| <= 2 sqrt(D_ij) (e_i + e_j) + (e_i + e_j)^2.
+  The fp64 sums over stages and tiles and the final G_ii + G_jj - 2 G_ij add
+  at most (S + 1203) 2^-53 * 2 (N~_i + N~_j), S the number of stages,
+  N~_i = (sqrt(N_i) + e_i)^2 and N_i = ||x_i - x_ref||^2 (the oracle's
+  D[i][ref]).
 
 Gram reference row. The Gram engine shifts every row by one input row, chosen
 by a probe over a sample of the coordinates: 4 runs of 256 consecutive
@@ -41,8 +47,7 @@ import numpy as np
 U = 2.0 ** -24
 DIRECT_LANE_COORDS = 16
 EPS_DIRECT = (DIRECT_LANE_COORDS + 2) * U
-GRAM_PRODUCTS = 32
-EPS_GRAM = (2 * GRAM_PRODUCTS + 4) * U
+GRAM_STAGE = 256
 
 
 PROBE_RUNS = 4
@@ -108,15 +113,57 @@ def agg_close(got, want):
     return bad.size == 0, (int(bad[0]) if bad.size else -1), float(err.max(initial=0.0))
 
 
-def dist_bounds(D, engine, ref=None):
+def gram_error_norms(x, ref, segments=None):
+    """(e, stages): per row, the 2-norm over all coordinates of the bound on the
+    Gram engine's per-coordinate error u |y| + 2^-k / 2 (y = fl(x - x_ref),
+    k per row and stage as the kernel chooses it), and the number of stages.
+    `segments`: lengths of the consecutive segments whose stages start anew
+    (a segment table); default one segment of all of x."""
+    x = np.asarray(x, dtype=np.float32)
+    n, d = x.shape
+    segments = [d] if segments is None else list(segments)
+    assert sum(segments) == d
+    e2 = np.zeros(n)
+    stages = 0
+    xr = x[ref]
+    start = 0
+    for length in segments:
+        if length == 0:
+            continue
+        S = -(-length // GRAM_STAGE)
+        stages += S
+        for i in range(n):
+            y = np.abs(x[i, start:start + length] - xr[start:start + length])  # fp32, as the kernel
+            pad = np.zeros(S * GRAM_STAGE, dtype=np.float32)
+            pad[:length] = y
+            st = pad.reshape(S, GRAM_STAGE)
+            mx = st.max(axis=1)
+            _, ex = np.frexp(mx)
+            E = np.where(mx < np.float32(2.0 ** -126), -126, ex.astype(np.int64) - 1)
+            k = np.minimum(21 - E, 127)
+            half = np.ldexp(1.0, -k - 1)[:, None]        # per stage
+            eps = U * st.astype(np.float64) + half        # padding: |y| = 0, counted as 0
+            eps[-1, length - (S - 1) * GRAM_STAGE:] = 0.0
+            e2[i] += float((eps * eps).sum())
+        start += length
+    return np.sqrt(e2), stages
+
+
+def dist_bounds(D, engine, ref=None, x=None, segments=None):
     """n x n absolute error bounds on the library's D entries, from the oracle's
-    D (for the Gram engine N_i = ||x_i - x_ref||^2 is the oracle's D[i][ref])."""
+    D (and, for the Gram engine, the input x and the reference row `ref`, which
+    set the quantization steps; segments as in gram_error_norms)."""
     n = D.shape[0]
     if engine == "direct":
         B = EPS_DIRECT * D
     elif engine == "gram":
+        assert x is not None and ref is not None
+        e, stages = gram_error_norms(x, ref, segments)
         N = D[:, ref]
-        B = EPS_GRAM * (N[:, None] + N[None, :])
+        Nq = (np.sqrt(N) + e) ** 2
+        es = e[:, None] + e[None, :]
+        fp64 = (stages + 1203) * 2.0 ** -53 * 2.0 * (Nq[:, None] + Nq[None, :])
+        B = (2.0 * np.sqrt(D) * es + es * es + fp64) * (1.0 + 1e-9)
     else:  # no distance kernel ran: D is exactly 0
         B = np.zeros_like(D)
     B = B + 1e-300
