@@ -154,7 +154,7 @@ def test_variance_stats(engine, h, d):
         D = oracle.pairwise_sqdist(g)
         eng = gf.distance_engine(h, d)
         ref = parity.checked_reference(g, gf.gram_reference(gt)) if eng == "gram" else None
-        B = parity.dist_bounds(D, eng, ref)
+        B = parity.dist_bounds(D, eng, ref, g)
         tol0 = np.triu(B, 1).sum() / (h * (h - 1)) + 1e-12 * want[0]
         assert abs(got[0] - want[0]) <= tol0, (got[0], want[0], tol0)
         assert abs(got[1] - want[1]) <= 4 * d * 2.0 ** -53 * want[1]

@@ -74,7 +74,7 @@ def test_step_matches_the_oracle(rule, f, m, n, q, d):
     want, want_sel = oracle.contract_step(rule, x, peers, f, m)
     eng = gf.distance_engine(n, d)
     ref = parity.checked_reference(x, gf.gram_reference(xt)) if eng == "gram" else None
-    B = parity.dist_bounds(oracle.pairwise_sqdist(x), eng, ref)
+    B = parity.dist_bounds(oracle.pairwise_sqdist(x), eng, ref, x)
     pinned = _pinned_nodes(rule, x, peers, f, m, B)
     assert sum(pinned) >= n // 2, "too few pinned nodes to test"
     for v in range(n):

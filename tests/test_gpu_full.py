@@ -77,36 +77,36 @@ def test_full_size_workload(key):
         want, pinned = {}, True
         if w.rules == ("krum", "median"):
             oo, so, sc, Do = oracle.multikrum(x, f, 1, return_scores=True, return_distances=True)
-            B = parity.dist_bounds(Do, eng, ref)
+            B = parity.dist_bounds(Do, eng, ref, x)
             pinned, margin = parity.krum_pinned(sc, Do, B, f, 1, parity.identical_rows(Do))
             want["krum"] = (oo, so)
             want["median"] = (oracle.median(x, f), None)
         elif w.rules == ("multikrum",):
             oo, so, sc, Do = oracle.multikrum(x, f, w.m, return_scores=True, return_distances=True)
-            B = parity.dist_bounds(Do, eng, ref)
+            B = parity.dist_bounds(Do, eng, ref, x)
             pinned, margin = parity.krum_pinned(sc, Do, B, f, w.m, parity.identical_rows(Do))
             want["multikrum"] = (oo, so)
         elif w.rules == ("multikrum_iterated",):
             oo, so, picks, rs, Do = oracle.multikrum_iterated(x, f, w.m, return_rounds=True,
                                                               return_distances=True)
-            B = parity.dist_bounds(Do, eng, ref)
+            B = parity.dist_bounds(Do, eng, ref, x)
             pinned, margin = parity.bulyan_pinned(picks, rs, Do, B, w.n, f,
                                                   parity.identical_rows(Do))
             want["multikrum_iterated"] = (oo, so)
         elif w.rules == ("bulyan",):
             oo, so, picks, rs, Do = oracle.bulyan(x, f, return_rounds=True, return_distances=True)
-            B = parity.dist_bounds(Do, eng, ref)
+            B = parity.dist_bounds(Do, eng, ref, x)
             pinned, margin = parity.bulyan_pinned(picks, rs, Do, B, w.n, f,
                                                   parity.identical_rows(Do))
             want["bulyan"] = (oo, so)
         elif w.rules == ("mda",):
             oo, so, Do = oracle.mda(x, f, return_distances=True)
-            B = parity.dist_bounds(Do, eng, ref)
+            B = parity.dist_bounds(Do, eng, ref, x)
             pinned, margin = parity.mda_pinned(Do, B, w.n, f, so)
             want["mda"] = (oo, so)
         else:
             _, so, sc, Do = oracle.multikrum(x, f, w.m, return_scores=True, return_distances=True)
-            B = parity.dist_bounds(Do, eng, ref)
+            B = parity.dist_bounds(Do, eng, ref, x)
             pinned, margin = parity.krum_pinned(sc, Do, B, f, w.m, parity.identical_rows(Do))
             _log("oracle selection done; median over the selection")
             want["multikrum-median"] = (oracle.median(x, f, rows=so), so)

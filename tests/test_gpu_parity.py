@@ -54,7 +54,7 @@ def _bounds(x, xt, Do, byzantine=()):
     ref = None
     if eng == "gram":
         ref = parity.checked_reference(x, gf.gram_reference(xt), byzantine)
-    return parity.dist_bounds(Do, eng, ref), eng
+    return parity.dist_bounds(Do, eng, ref, x), eng
 
 
 # --- distances -------------------------------------------------------------------

@@ -45,7 +45,7 @@ def _bounds(x, segs):
         xs = s.cpu().numpy()
         eng = gf.distance_engine(n, xs.shape[1])
         ref = parity.checked_reference(xs, gf.gram_reference(s)) if eng == "gram" else None
-        B += parity.dist_bounds(oracle.pairwise_sqdist(xs), eng, ref)
+        B += parity.dist_bounds(oracle.pairwise_sqdist(xs), eng, ref, xs)
     return B
 
 

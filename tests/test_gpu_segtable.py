@@ -230,7 +230,7 @@ def test_gram_table_matches_the_oracle(rule, n, f, m):
         off = int(sum(sizes[:big]))
         ref = parity.checked_reference(np.ascontiguousarray(x[:, off:off + sizes[big]]),
                                        gf.table_gram_reference(table))
-        B = parity.dist_bounds(D, "gram", ref)
+        B = parity.dist_bounds(D, "gram", ref, x, segments=sizes)
         if not _pinned(rule, x, f, m, D, B):
             continue
         seg = gf.Segmented(rule, n, f, m)
