@@ -17,9 +17,9 @@ Alongside the metric the line carries:
     adds on top (e.g. column sums written for a later pass) are reported apart
     as design_bytes_per_launch;
   * rooflines: the same figure for every kernel that has an algorithmic byte
-    count, and for the Gram distance kernel also its useful matrix-core rate
-    (n (n + 1) d flops of the upper-triangle Gram matrix per launch) against the
-    fp32 MFMA peak;
+    count, and for the Gram distance kernel also its integer matrix-core rate
+    (the int8 digit products it executes per launch) against the int8 MFMA
+    peak;
   * cpu_baseline: the CPU oracle timed on this host's cores on a bounded
     sample of the same input, with the host's CPU model, its processor count
     and the OpenMP team the oracle ran with.
@@ -35,7 +35,7 @@ import time
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
 INPUT_RING_BYTES = 4 << 30   # inputs smaller than this are alternated between two copies
-FP32_MFMA_PEAK_TFLOPS = 157.3
+INT8_MFMA_PEAK_TOPS = 5000.0  # MI355X dense int8 matrix peak, 5.0 POP/s
 
 
 def _parse():
@@ -211,10 +211,14 @@ def algorithmic(kernel, w):
     return None, None, None
 
 
-def gram_useful_flops(w):
-    """Useful flops of one Gram distance launch: the upper triangle of
-    G = Y Y^T with its diagonal, n (n + 1) / 2 dot products of length d."""
-    return float(w.n * (w.n + 1)) * w.d
+def gram_mfma_ops(w):
+    """Integer matrix-core operations of one Gram distance launch: every
+    16 x 16 block pair of the upper block triangle (NB(NB+1)/2 of them, NB =
+    ceil(n / 16)) times 9 products of int8 digits, a multiply and an add each,
+    per coordinate (d rounded up to whole 256-coordinate stages)."""
+    nb = -(-w.n // 16)
+    stages = -(-w.d // 256)
+    return float(nb * (nb + 1) // 2 * 256 * 9 * 2) * stages * 256
 
 
 def source_digest(path):
@@ -439,11 +443,11 @@ def bench_workload(key, args):
             r["design_bytes_per_launch"] = design
             r["design_GBps"] = round(design / (avg_ms * 1e-3) / 1e9, 2)
         if kern.startswith("dist_gram") and args.segments == 1:
-            flops = gram_useful_flops(w)
-            tf = flops / (avg_ms * 1e-3) / 1e12
-            r["mfma"] = {"useful_flops_per_launch": flops, "achieved": round(tf, 2),
-                         "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                         "frac": round(tf / FP32_MFMA_PEAK_TFLOPS, 4)}
+            ops = gram_mfma_ops(w)
+            tops = ops / (avg_ms * 1e-3) / 1e12
+            r["mfma"] = {"int8_ops_per_launch": ops, "achieved": round(tops, 1),
+                         "peak": INT8_MFMA_PEAK_TOPS, "unit": "TOP/s",
+                         "frac": round(tops / INT8_MFMA_PEAK_TOPS, 4)}
         return r
 
     roofline = kernel_roofline(dominant)

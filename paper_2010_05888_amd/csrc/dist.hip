@@ -830,19 +830,6 @@ hipError_t launch_gram_nb(const float* x, const DistPlan& p, const int32_t* ref,
 
 size_t align256(size_t b) { return (b + 255) & ~static_cast<size_t>(255); }
 
-// Compute units of the current device (256 on MI355X; also the fallback when
-// no device is available, e.g. when only planning on a host without a GPU).
-int device_cus() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      cus <= 0) {
-    (void)hipGetLastError();
-    return 256;
-  }
-  return cus;
-}
-
 template <int NB>
 int gram_blocks_per_cu_nb() {
   int blocks = 0, blocks_pad = 0;
@@ -945,6 +932,19 @@ hipError_t launch_gram_table_nb(const float* const* ptrs, int n, const GramSegs&
 int g_direct_max_n = 20;
 
 }  // namespace
+
+// Compute units of the current device (256 on MI355X; also the fallback when
+// no device is available, e.g. when only planning on a host without a GPU).
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  return cus;
+}
 
 int64_t table_gram_tiles(const int64_t* dims, int K, int n) {
   int64_t tiles = 0;

@@ -35,6 +35,10 @@ int direct_max_n();
 void set_direct_max_n(int n);
 
 DistPlan plan_distances(int n, int64_t d, const float* x);
+
+// Compute units of the current device (256 on MI355X; also the fallback when
+// no device is available, e.g. when only planning on a host without a GPU).
+int device_cus();
 // Direct engine: coordinates per tile for a segment of length d read with
 // `width`-float loads.
 int64_t direct_chunk(int64_t d, int width);
