@@ -264,6 +264,16 @@ garfield_status garfield_variance_stats(const float* g, int h, int64_t d, const 
 double garfield_delta(int rule, int n, int f);
 
 /*
+ * The condition's margin for rule, n, f from the statistics above, copied to
+ * HOST memory by the caller (stats_host[0] = sigma^2, stats_host[1] =
+ * ||grad||^2): sqrt(stats_host[1]) / (Delta * sqrt(stats_host[0])); the
+ * condition holds for some kappa > 1 iff the margin exceeds 1. +inf when
+ * Delta * sigma is 0 (and ||grad|| is not), NaN where garfield_delta is NaN,
+ * stats_host is NULL or a statistic is negative or NaN. Host function.
+ */
+double garfield_variance_margin(int rule, int n, int f, const double* stats_host);
+
+/*
  * Segmented aggregation (per-layer aggregation, Section 4.2). A squared
  * distance is a sum over coordinates, so the distances between the n full
  * vectors are the sums of the distances between their segments (for

@@ -105,6 +105,8 @@ def load():
     lib.garfield_variance_stats.restype = st
     lib.garfield_delta.argtypes = [i32, i32, i32]
     lib.garfield_delta.restype = ctypes.c_double
+    lib.garfield_variance_margin.argtypes = [i32, i32, i32, ctypes.POINTER(ctypes.c_double)]
+    lib.garfield_variance_margin.restype = ctypes.c_double
     lib.garfield_workspace_bytes.argtypes = [i32, i32, i32, i64, i32]
     lib.garfield_workspace_bytes.restype = ctypes.c_size_t
     lib.garfield_release.argtypes = []
@@ -366,13 +368,13 @@ def variance_condition(g: torch.Tensor, grad: torch.Tensor, n: int, f: int) -> d
     """For each rule with a Delta: whether kappa * Delta * sigma <= ||grad||
     can hold for some kappa > 1, i.e. ||grad|| / (Delta * sigma) > 1, with
     sigma estimated from the honest gradient estimates g."""
-    var, sq = (float(v) for v in variance_stats(g, grad).cpu())
-    sigma, norm = var ** 0.5, sq ** 0.5
-    res = {"sigma": sigma, "grad_norm": norm}
+    stats = variance_stats(g, grad).cpu()
+    host = (ctypes.c_double * 2)(float(stats[0]), float(stats[1]))
+    res = {"sigma": float(stats[0]) ** 0.5, "grad_norm": float(stats[1]) ** 0.5}  # for display
     for rule in ("mda", "krum", "median"):
         dl = delta(rule, n, f)
-        ratio = norm / (dl * sigma) if dl == dl and dl * sigma > 0 else float("inf")
-        res[rule] = {"delta": dl, "ratio": ratio, "holds": ratio > 1.0 if dl == dl else None}
+        ratio = load().garfield_variance_margin(RULE_IDS[rule], n, f, host)
+        res[rule] = {"delta": dl, "ratio": ratio, "holds": ratio > 1.0 if ratio == ratio else None}
     return res
 
 

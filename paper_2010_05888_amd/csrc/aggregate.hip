@@ -240,9 +240,10 @@ hipError_t bulyan_dispatch(int theta, int beta, int width, const float* x, int n
 }  // namespace
 
 // Load/store width of the streaming kernels: 16-byte accesses whenever x and
-// out are float-aligned, whatever d (see f4u).
+// out are float-aligned, whatever d (see f4u); one float at a time only for
+// an output that is not float-aligned.
 int stream_width(const float* x, const float* out) {
-  return (vector_width(x) == 4 && vector_width(out) == 4) ? 4 : 1;
+  return (load_width(x) == 4 && load_width(out) == 4) ? 4 : 1;
 }
 
 hipError_t enqueue_mean_rows(const float* x, int n, int64_t d, const int32_t* rows, int k,

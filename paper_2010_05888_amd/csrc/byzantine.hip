@@ -281,7 +281,7 @@ hipError_t launch_attack_scale(const float* x, int h, int64_t d, double param, i
 hipError_t enqueue_attack(int kind, const float* honest, int h, int64_t d, double param,
                           uint64_t seed, float* byz, int nbyz, hipStream_t s) {
   if (d == 0 || nbyz == 0) return hipSuccess;
-  const bool wide = vector_width(byz) == 4 && (honest == nullptr || vector_width(honest) == 4);
+  const bool wide = load_width(byz) == 4 && (honest == nullptr || load_width(honest) == 4);
   switch (kind) {
     case kAttackReverse:
       return wide ? launch_attack_scale<4>(honest, h, d, param, nbyz, byz, s)
@@ -309,7 +309,7 @@ hipError_t enqueue_attack(int kind, const float* honest, int h, int64_t d, doubl
 }
 
 int64_t sqnorm_parts(int64_t d, const float* t) {
-  const int64_t per = static_cast<int64_t>(kSqnormSteps) * kBlock * vector_width(t);
+  const int64_t per = static_cast<int64_t>(kSqnormSteps) * kBlock * load_width(t);
   return (d + per - 1) / per;
 }
 
@@ -317,7 +317,7 @@ hipError_t enqueue_variance_stats(const DistSums& ds, int h, const float* grad, 
                                   double* partial, double* stats, hipStream_t s) {
   const int64_t parts = d > 0 ? sqnorm_parts(d, grad) : 0;
   if (parts > 0) {
-    if (vector_width(grad) == 4)
+    if (load_width(grad) == 4)
       launch("sqnorm", k_sqnorm_partials<4>, dim3(static_cast<unsigned>(parts)), dim3(kBlock), 0,
              s, grad, d, partial);
     else

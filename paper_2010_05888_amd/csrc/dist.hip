@@ -166,10 +166,10 @@ __global__ __launch_bounds__(kPickThreads) void k_pick_ref(const double* __restr
 // row (lane l: coordinates 4l .. 4l+3, so one instruction reads 1 KB of one
 // row), quantizes them into one of two LDS stage buffers, and keeps the next
 // two stages' loads in flight in two register sets (each row's next load is
-// issued as soon as the row is written). Waves 4-7 consume: they multiply
-// the stage in the other buffer. One barrier per stage hands the buffers
-// over, so quantizing (VALU) and multiplying (matrix cores) overlap on every
-// SIMD, which holds one wave of each role.
+// issued as soon as the row is written). Waves 4-7
+// consume: they multiply the stage in the other buffer. One barrier per
+// stage hands the buffers over, so quantizing (VALU) and multiplying (matrix
+// cores) overlap on every SIMD, which holds one wave of each role.
 //
 // Quantizing. y = fl(x - x_ref) in fp32 (one rounding). Per row and stage,
 // with E the exponent of the largest |y| (-126 for a zero or subnormal
@@ -217,6 +217,9 @@ struct GramShape {
   static constexpr int PLANE = ROWS * kPlanePitch;  // bytes per digit plane
   static constexpr int BUF = 3 * PLANE + 4 * ROWS;  // three planes, then k per row
   static constexpr int LDS = 2 * BUF;               // two stage buffers
+  // stages a producer keeps in flight (register sets of RPW + 1 loads; four
+  // measured no faster than two at n = 19)
+  static constexpr int DEPTH = 2;
 };
 
 __host__ __device__ constexpr int pair_b1(int nb, int q) {
@@ -568,13 +571,15 @@ __device__ __forceinline__ void gram_consume(const uint8_t* __restrict__ lds, in
   for (int i = 0; i < S::PPW; ++i)
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc64[i][e] = 0.0;
+  constexpr int D = S::DEPTH;
   int64_t t = 0;
-  if (nf >= 2) {
-    for (; t + 1 < nf; t += 2) {
-      if (t >= 1) gram_multiply<NB, CV>(lds + S::BUF, g, r, acc64);  // entry t - 1
-      lds_barrier();
-      gram_multiply<NB, CV>(lds, g, r, acc64);                       // entry t
-      lds_barrier();
+  if (nf >= D) {
+    for (; t + D - 1 < nf; t += D) {
+#pragma unroll
+      for (int u = 0; u < D; ++u) {  // iteration t + u: entry t + u - 1, buffer (u + 1) % 2
+        if (u > 0 || t >= 1) gram_multiply<NB, CV>(lds + ((u + 1) & 1) * S::BUF, g, r, acc64);
+        lds_barrier();
+      }
     }
   }
   for (int64_t i = t; i <= cnt; ++i) {
@@ -590,26 +595,30 @@ __device__ __forceinline__ void gram_produce(uint8_t* __restrict__ lds, int64_t 
                                              int n, int ref, int pw, const List& list) {
   using S = GramShape<NB>;
   const int lane = threadIdx.x & 63;
-  f4 va[S::RPW], vb[S::RPW];
-  f4 ra, rb;
+  constexpr int D = S::DEPTH;
+  f4 v[D][S::RPW];
+  f4 vr[D];
   int64_t t = 0;
-  if (nf >= 2) {
-    // entries past the last full one load that one again (not used)
+  if (nf >= D) {
+    // D stages in flight, one register set each; entries past the last full
+    // one load that one again (not used)
     auto whole = [&](int64_t i) { return list.entry(i < nf ? i : nf - 1); };
-    gram_issue<NB, PAD, true>(whole(0), n, ref, pw, lane, va, ra);
-    gram_issue<NB, PAD, true>(whole(1), n, ref, pw, lane, vb, rb);
-    for (; t + 1 < nf; t += 2) {
-      gram_put<NB, PAD, true>(lds, n, pw, lane, va, ra, ref, whole(t + 2));
-      lds_barrier();
-      gram_put<NB, PAD, true>(lds + S::BUF, n, pw, lane, vb, rb, ref, whole(t + 3));
-      lds_barrier();
+#pragma unroll
+    for (int u = 0; u < D; ++u) gram_issue<NB, PAD, true>(whole(u), n, ref, pw, lane, v[u], vr[u]);
+    for (; t + D - 1 < nf; t += D) {
+#pragma unroll
+      for (int u = 0; u < D; ++u) {  // iteration t + u: buffer u % 2 (t and D even)
+        gram_put<NB, PAD, true>(lds + (u & 1) * S::BUF, n, pw, lane, v[u], vr[u], ref,
+                                whole(t + u + D));
+        lds_barrier();
+      }
     }
   }
   for (int64_t i = t; i <= cnt; ++i) {
     if (i < cnt) {
       const auto st = list.entry(i);
-      gram_issue<NB, PAD, false>(st, n, ref, pw, lane, va, ra);
-      gram_put<NB, PAD, false>(lds + (i & 1) * S::BUF, n, pw, lane, va, ra, ref, st);
+      gram_issue<NB, PAD, false>(st, n, ref, pw, lane, v[0], vr[0]);
+      gram_put<NB, PAD, false>(lds + (i & 1) * S::BUF, n, pw, lane, v[0], vr[0], ref, st);
     }
     lds_barrier();
   }
@@ -1010,7 +1019,7 @@ hipError_t enqueue_distances_table_gram(const float* const* ptrs, int n, const i
 int direct_max_n() { return __atomic_load_n(&g_direct_max_n, __ATOMIC_RELAXED); }
 void set_direct_max_n(int n) { __atomic_store_n(&g_direct_max_n, n, __ATOMIC_RELAXED); }
 
-int vector_width(const float* p) { return reinterpret_cast<uintptr_t>(p) % 4 == 0 ? 4 : 1; }
+int load_width(const float* p) { return reinterpret_cast<uintptr_t>(p) % 4 == 0 ? 4 : 1; }
 
 // Coordinates per tile of the direct engine: at most kDirectLaneCoords per lane
 // (each fp32 accumulator sums at most that many squares before the tile is
@@ -1032,7 +1041,7 @@ DistPlan plan_distances(int n, int64_t d, const float* x) {
   if (n < 2 || d == 0) return p;  // D is all zeros
   if (n <= direct_max_n()) {
     p.engine = kEngineDirect;
-    p.width = vector_width(x);
+    p.width = load_width(x);
     if (p.width > direct_width_cap(n)) p.width = direct_width_cap(n);
     p.chunk = direct_chunk(d, p.width);
     p.entries = n * (n - 1) / 2;

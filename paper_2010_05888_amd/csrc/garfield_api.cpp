@@ -412,6 +412,17 @@ double garfield_delta(int rule, int n, int f) {
   }
 }
 
+double garfield_variance_margin(int rule, int n, int f, const double* stats_host) {
+  const double nan = std::nan("");
+  const double delta = garfield_delta(rule, n, f);
+  if (!stats_host || std::isnan(delta)) return nan;
+  const double var = stats_host[0], sq = stats_host[1];
+  if (!(var >= 0.0) || !(sq >= 0.0)) return nan;  // also NaN
+  const double denom = delta * std::sqrt(var), norm = std::sqrt(sq);
+  if (denom == 0.0) return norm > 0.0 ? HUGE_VAL : nan;
+  return norm / denom;
+}
+
 garfield_status garfield_contract_step(int rule, const float* x, int n, int64_t d,
                                        const int32_t* peers, int q, int f, int m, float* y,
                                        void* stream) {
@@ -638,8 +649,8 @@ garfield_status garfield_seg_destroy(garfield_segmented* seg) {
 
 size_t garfield_workspace_bytes(int rule, int n, int f, int64_t d, int m) {
   if (n < 1 || n > GARFIELD_NMAX || f < 0 || d < 0) return 0;
-  // Plan for 4-byte-aligned rows: the narrowest loads give the most tiles, so
-  // this bounds every alignment of x.
+  // Plan for float-aligned rows, as every accepted input is: the same plan as
+  // every call of the rule with these sizes.
   const float* narrow = reinterpret_cast<const float*>(uintptr_t{4});
   switch (rule) {
     case GARFIELD_RULE_MULTIKRUM:

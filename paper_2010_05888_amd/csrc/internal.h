@@ -176,10 +176,12 @@ hipError_t enqueue_median(const float* x, int n, int64_t d, const int32_t* rows,
 hipError_t enqueue_bulyan_aggregate(const float* x, int n, int f, int64_t d, const int32_t* sel,
                                     float* out, hipStream_t s);
 
-// Widest vector load (4, 2 or 1 floats) every row of x supports.
 // Width of the register loads of the streaming kernels and the distance
-// engines: 4 (16-byte accesses at dword alignment) for float-aligned pointers.
-int vector_width(const float* p);
+// engines: 4 (16-byte accesses at dword alignment, f4u) for a float-aligned
+// pointer, 1 otherwise. Every input the entry points accept is float-aligned
+// (check_common), so inputs always get 4; the 1-float paths of the streaming
+// kernels serve only an output that is not float-aligned.
+int load_width(const float* p);
 
 // Segmented aggregation: acc[i*n + j] += D[i][j] of one segment (all i, j < n;
 // the diagonal stays 0), and acc[0 .. count) = 0.

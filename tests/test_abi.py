@@ -191,3 +191,26 @@ def test_segmented_validation_codes(lib):
     assert lib.garfield_seg_aggregate(NULL, FAKE, 10, FAKE, NULL) == gf.EINVAL
     assert lib.garfield_seg_reset(NULL, NULL) == gf.EINVAL
     assert lib.garfield_seg_destroy(NULL) == gf.OK
+
+
+def test_variance_margin_on_the_host(lib):
+    # ||grad|| / (Delta sigma) from host statistics (no GPU): checked against the
+    # oracle's Delta; +inf when Delta sigma is 0, NaN without a Delta
+    import math
+
+    import oracle
+
+    lib.garfield_variance_margin.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                             ctypes.POINTER(ctypes.c_double)]
+    lib.garfield_variance_margin.restype = ctypes.c_double
+    stats = (ctypes.c_double * 2)(0.25, 9.0)  # sigma = 0.5, ||grad|| = 3
+    for rule, rid in (("mda", gf.RULE_IDS["mda"]), ("krum", gf.RULE_IDS["krum"]),
+                      ("median", gf.RULE_IDS["median"])):
+        for n, f in ((7, 1), (11, 2), (19, 4)):
+            want = 3.0 / (oracle.delta(rule, n, f) * 0.5)
+            assert lib.garfield_variance_margin(rid, n, f, stats) == pytest.approx(want, rel=1e-12)
+    zero = (ctypes.c_double * 2)(0.0, 9.0)
+    assert math.isinf(lib.garfield_variance_margin(gf.RULE_IDS["median"], 7, 1, zero))
+    assert math.isnan(lib.garfield_variance_margin(gf.RULE_IDS["bulyan"], 7, 1, stats))
+    assert math.isnan(lib.garfield_variance_margin(gf.RULE_IDS["krum"], 4, 1, stats))  # n < 2f+3
+    assert math.isnan(lib.garfield_variance_margin(gf.RULE_IDS["krum"], 7, 1, None))

@@ -85,8 +85,8 @@ def test_workspace_includes_the_column_sums():
 
 @pytest.mark.parametrize("d", [4099, 4100])
 def test_rows_at_an_odd_float_offset(d):
-    # rows starting one float past 16-byte alignment: both kernels take their
-    # one-float loads and stores
+    # rows starting one float past 16-byte alignment: both kernels still load
+    # 16 bytes per lane, from addresses that are only float-aligned (f4u)
     n, f, m = 11, 2, 9
     x, rng = _rows(n, d, 5 + d)
     x += rng.standard_normal((n, d)).astype(np.float32)
