@@ -96,6 +96,11 @@ garfield_status garfield_pairwise_sqdist(const float* x, int n, int64_t d, doubl
  * every such sum is provably exact (the coordinate's exponents span at most
  * 23 binades), summing the selected vectors elsewhere: the same bits from
  * fewer bytes read.
+ * Short inputs (n <= 12, out float-aligned, d up to about 10^5 coordinates)
+ * take two launches instead of three or four: the distance pass, then one
+ * kernel whose workgroups each add the distance partials, make the selection
+ * and write the mean of their 1,024 coordinates -- the same selection and
+ * the same bits.
  */
 garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int m, float* out,
                                    int32_t* sel, void* stream);

@@ -15,7 +15,8 @@ extern "C" {
 
 /*
  * Largest n for which pairwise distances use the direct-difference VALU
- * engine; above it they use the MFMA Gram engine (Y = X - x_ref, fp32 MFMA).
+ * engine; above it they use the MFMA Gram engine (Y = X - x_ref quantized per
+ * 256-coordinate stage, exact int8 MFMA).
  * Valid range 1..GARFIELD_DIRECT_MAX_N_LIMIT (1 means: always MFMA for
  * n >= 2). Returns the previous value, or -1 (and changes nothing) if the
  * value is out of range. Process-wide; not synchronised with calls in flight.
@@ -24,8 +25,21 @@ extern "C" {
 #define GARFIELD_DIRECT_MAX_N_DEFAULT 20
 int garfield_tuning_set_direct_max_n(int n);
 
+/*
+ * Whether garfield_krum and garfield_multikrum (and the no-allocation
+ * variant) may make the selection and the mean in one kernel on short inputs:
+ * n <= 12 rows, a float-aligned out, the distance pass in at most 256 tiles,
+ * and at most 8 MiB of distance partials read again by the combined kernel
+ * (each of its workgroups, one per 1,024 coordinates, adds all of them): d up
+ * to about 228,000 at n = 7 and 129,000 at n = 12. The combined kernel makes the same selection and
+ * writes the same bits as the separate selection and mean kernels. on = 0
+ * turns it off; 1 (the default) allows it. Returns the previous setting.
+ * Process-wide; not synchronised with calls in flight.
+ */
+int garfield_tuning_set_fused(int on);
+
 /* Engine the distance step would use for (n, d): 0 none (n < 2 or d == 0),
- * 1 direct differences (VALU), 2 Gram (MFMA). */
+ * 1 direct differences (VALU), 2 Gram (exact integer MFMA). */
 int garfield_tuning_distance_engine(int n, long long d);
 
 /* The reference row the Gram engine would shift the n x d device input x by

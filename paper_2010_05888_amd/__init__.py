@@ -117,6 +117,8 @@ def load():
     lib.garfield_version.restype = ctypes.c_char_p
     lib.garfield_tuning_set_direct_max_n.argtypes = [i32]
     lib.garfield_tuning_set_direct_max_n.restype = i32
+    lib.garfield_tuning_set_fused.argtypes = [i32]
+    lib.garfield_tuning_set_fused.restype = i32
     lib.garfield_tuning_distance_engine.argtypes = [i32, ctypes.c_longlong]
     lib.garfield_tuning_distance_engine.restype = i32
     lib.garfield_tuning_gram_reference.argtypes = [vp, i32, ctypes.c_longlong, vp]
@@ -529,6 +531,12 @@ def set_direct_max_n(n: int) -> int:
     if old < 0:
         raise ValueError(f"direct_max_n out of range: {n}")
     return old
+
+
+def set_fused(on: bool) -> bool:
+    """Allow (True, the default) or forbid the one-launch Krum / Multi-Krum of
+    short inputs; returns the previous setting."""
+    return bool(load().garfield_tuning_set_fused(1 if on else 0))
 
 
 def gram_reference(x: torch.Tensor) -> int:

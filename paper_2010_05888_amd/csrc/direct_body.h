@@ -13,8 +13,10 @@ namespace garfield {
 // Block-wide reduction of P per-thread fp32 accumulators into P fp64 sums,
 // through LDS in chunks of 32 columns (33-float row stride: conflict-free).
 // Every sum is formed in the same order (eight fixed groups of 32 threads,
-// each summed in ascending thread order), whatever the pair.
-template <int P>
+// each summed in ascending thread order), whatever the pair. The sums are
+// stored by lanes 0..31 of wave 0; COHERENT: as device-coherent (agent-scope
+// atomic) stores, for a reader in another workgroup of the same launch.
+template <int P, bool COHERENT = false>
 __device__ __forceinline__ void block_reduce_pairs(const float* acc, double* __restrict__ out,
                                                    int64_t stride) {
   __shared__ float cols[kBlock * 33];
@@ -38,7 +40,11 @@ __device__ __forceinline__ void block_reduce_pairs(const float* acc, double* __r
       double a = part[0][t];
 #pragma unroll
       for (int g = 1; g < 8; ++g) a += part[g][t];
-      out[(base + t) * stride] = a;
+      if constexpr (COHERENT)
+        __hip_atomic_store(out + (base + t) * stride, a, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      else
+        out[(base + t) * stride] = a;
     }
     __syncthreads();
   }
@@ -71,6 +77,39 @@ struct ColSum {
   }
 };
 
+// The W coordinates c .. c+W-1 (c < end) of rows 0..N-1 into v; coordinates
+// at or beyond end read as 0.
+template <int N, int W, class Src>
+__device__ __forceinline__ void direct_load(const Src& src, int64_t c, int64_t end,
+                                            float (&v)[N][W]) {
+  if (c + W <= end) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) load_w<W>(src.row(i) + c, v[i]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < N; ++i) load_w_tail<W>(src.row(i) + c, end - c, v[i]);
+  }
+}
+
+// acc[p] += (v[i][e] - v[j][e])^2 for every pair p = (i < j), row-major over
+// i, coordinate by coordinate.
+template <int N, int W>
+__device__ __forceinline__ void direct_add(const float (&v)[N][W], float* acc) {
+#pragma unroll
+  for (int e = 0; e < W; ++e) {
+    int p = 0;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+#pragma unroll
+      for (int j = i + 1; j < N; ++j) {
+        const float t = v[i][e] - v[j][e];
+        acc[p] = __builtin_fmaf(t, t, acc[p]);
+        ++p;
+      }
+    }
+  }
+}
+
 // Lane t takes W consecutive coordinates every kBlock * W in [start, end) of
 // rows 0..N-1 of `src`, adding (x_i - x_j)^2 for every pair into acc (pairs
 // in row-major order over i < j). With SUM, it also writes the column sums
@@ -80,26 +119,8 @@ __device__ __forceinline__ void direct_accumulate(const Src& src, int64_t start,
                                                   float* acc, double* __restrict__ colsum = nullptr) {
   for (int64_t c = start + static_cast<int64_t>(threadIdx.x) * W; c < end; c += kBlock * W) {
     float v[N][W];
-    if (c + W <= end) {
-#pragma unroll
-      for (int i = 0; i < N; ++i) load_w<W>(src.row(i) + c, v[i]);
-    } else {
-#pragma unroll
-      for (int i = 0; i < N; ++i) load_w_tail<W>(src.row(i) + c, end - c, v[i]);
-    }
-#pragma unroll
-    for (int e = 0; e < W; ++e) {
-      int p = 0;
-#pragma unroll
-      for (int i = 0; i < N; ++i) {
-#pragma unroll
-        for (int j = i + 1; j < N; ++j) {
-          const float t = v[i][e] - v[j][e];
-          acc[p] = __builtin_fmaf(t, t, acc[p]);
-          ++p;
-        }
-      }
-    }
+    direct_load<N, W>(src, c, end, v);
+    direct_add<N, W>(v, acc);
     if constexpr (SUM) {
       double o[W];
 #pragma unroll

@@ -233,6 +233,12 @@ garfield_status garfield_multikrum(const float* x, int n, int f, int64_t d, int 
   if (m > n - f) return GARFIELD_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   DistSums ds;
+  const DistPlan plan = plan_distances(n, d, x);
+  if (krum_fusable(plan, out)) {  // short input: selection and mean in one kernel
+    st = run_distances(x, n, d, 0, &ds, nullptr, s, plan.entries);
+    if (st != GARFIELD_OK) return st;
+    return to_status(enqueue_krum_select_mean(x, ds, d, f, m, sel, out, s));
+  }
   const bool cs = out && use_colsum(x, n, d, m);
   void* colsum = nullptr;
   st = run_distances(x, n, d, colsum_bytes(cs, d), &ds, &colsum, s, kFoldSelect, cs);
@@ -262,6 +268,11 @@ garfield_status garfield_multikrum_noalloc(const float* x, int n, int f, int64_t
   // every scratch byte a kernel reads here is written earlier in the same call
   // (tile partials, entry sums, probe matrices, reference row), so nothing
   // needs clearing; the mean reads the selected rows (no column sums)
+  if (krum_fusable(plan, out)) {
+    st = run_distances_on(plan, base, x, 0, &ds, nullptr, s, plan.entries, false);
+    if (st != GARFIELD_OK) return st;
+    return to_status(enqueue_krum_select_mean(x, ds, d, f, m, sel, out, s));
+  }
   st = run_distances_on(plan, base, x, 0, &ds, nullptr, s, kFoldSelect, false);
   if (st != GARFIELD_OK) return st;
   st = to_status(enqueue_krum_select(ds, f, m, sel, s));
@@ -708,6 +719,12 @@ int garfield_tuning_set_direct_max_n(int n) {
   if (n < 1 || n > GARFIELD_DIRECT_MAX_N_LIMIT) return -1;
   const int old = direct_max_n();
   set_direct_max_n(n);
+  return old;
+}
+
+int garfield_tuning_set_fused(int on) {
+  const int old = fused_enabled() ? 1 : 0;
+  set_fused(on != 0);
   return old;
 }
 

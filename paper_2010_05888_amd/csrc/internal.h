@@ -78,6 +78,21 @@ DistSums dist_sums(const DistPlan& p, const DistWorkspace& ws);
 // Write D (n x n fp64, device) from the entry sums.
 hipError_t enqueue_write_dist(const DistSums& ds, double* dist, hipStream_t s);
 
+// Multi-Krum's selection and mean in one kernel (select.hip) for short
+// inputs: direct-engine plans of 3 <= n <= kFusedMaxN rows with 16-byte loads
+// whose distance step leaves its tile partials folded (at most kFoldTiles
+// tiles), a float-aligned out, and a repeated read of the partials (every one
+// of the kernel's workgroups, one per 1,024 coordinates, adds all of them) of
+// at most kFusedRereadBytes. ds: the folded distance sums of x. The selection
+// and the output are bit-identical to k_krum_select's and k_mean_rows'.
+constexpr int kFusedMaxN = 12;
+constexpr double kFusedRereadBytes = 8.0 * 1024 * 1024;
+bool fused_enabled();
+void set_fused(bool on);
+bool krum_fusable(const DistPlan& p, const float* out);
+hipError_t enqueue_krum_select_mean(const float* x, const DistSums& ds, int64_t d, int f, int m,
+                                    int32_t* sel, float* out, hipStream_t s);
+
 // Selection on D (one workgroup each).
 hipError_t enqueue_krum_select(const DistSums& ds, int f, int m, int32_t* sel, hipStream_t s);
 hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStream_t s);

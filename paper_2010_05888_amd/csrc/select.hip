@@ -6,6 +6,7 @@
 // towards the lower index and every sum is added in a fixed order.
 
 #include "device_common.h"
+#include "direct_body.h"
 #include "dist_layout.h"
 #include "internal.h"
 #include "timing.h"
@@ -107,6 +108,171 @@ __global__ __launch_bounds__(kSelectThreads) void k_krum_select(DistSums ds, int
   if (threadIdx.x >= 64) return;
   const uint64_t mask = __ballot(static_cast<int>(threadIdx.x) < n && flag[threadIdx.x]);
   write_selected(mask, n, nullptr, sel);
+}
+
+// ---------------------------------------------------------------------------
+// Multi-Krum's selection and mean in one kernel, for short inputs (n <=
+// kFusedMaxN rows, 16-byte loads) whose distance step left its tile partials
+// folded: a launch and the full-size selection workgroup cost more than the
+// work itself at such sizes. Every workgroup takes 1,024 coordinates: it loads
+// them from all n rows first, adds the tiles while those loads are in flight,
+// makes the selection in one wave, and writes the mean of the selected rows
+// from its registers. Each step keeps the arithmetic of the separate kernels
+// (load_dist's tile sums, krum_flags' scores and ranking, k_mean_rows' mean),
+// so the selection and the output are bit-identical to theirs.
+
+// The folded tile partials of all P entries (entry-major, `tiles` <= 256 per
+// entry) summed into esum, every load issued before the first addition: wave
+// w takes entries w, w + 4, ...; each sum is formed in the tile-sum kernel's
+// order, exactly as load_dist forms it.
+template <int P>
+__device__ __forceinline__ void fold_tiles(const double* __restrict__ partial, int64_t tiles,
+                                           double* esum) {
+  constexpr int kWaves = kBlock / 64;
+  constexpr int E = (P + kWaves - 1) / kWaves;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // unconditional loads from clamped addresses (all in flight at once); the
+  // values of slots past `tiles` are replaced by 0
+  double v[E];
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    const int e = wave + k * kWaves;
+    const double* row = partial + static_cast<int64_t>(e < P ? e : P - 1) * tiles;
+    double s[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int t = lane + 64 * u;
+      const double val = row[t < tiles ? t : 0];
+      s[u] = t < tiles ? val : 0.0;
+    }
+    v[k] = (s[0] + s[2]) + (s[1] + s[3]);
+  }
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    const int e = wave + k * kWaves;
+    if (e < P) {
+#pragma unroll
+      for (int m = 32; m > 0; m >>= 1) v[k] += __shfl_xor(v[k], m, 64);
+      if (lane == 0) esum[e] = v[k];
+    }
+  }
+  __syncthreads();
+}
+
+// Multi-Krum's selection from the N x N distances (entry sums esum, direct
+// layout), by the 64 lanes of one wave without LDS traffic or barriers: lane
+// i < N sorts its row's N-1 distances, adds the k = N-f-2 smallest as the
+// butterfly of krum_flags adds them (a balanced tree in ascending order, the
+// other slots 0: the same bits), and ranks its (score, i) against every
+// lane's. Returns the lane-uniform mask of the m selected rows.
+template <int N>
+__device__ __forceinline__ uint64_t krum_mask_wave(const double* esum, int f, int m) {
+  constexpr int M = N - 1;
+  const int i = threadIdx.x & 63;
+  const int k = N - f - 2;
+  double score = 0.0;
+  if (i < N) {
+    double r[M];
+#pragma unroll
+    for (int q = 0; q < M; ++q) {
+      const int j = q < i ? q : q + 1;
+      r[q] = esum[direct_entry(N, i < j ? i : j, i < j ? j : i)];
+    }
+#pragma unroll
+    for (int a = 0; a < M; ++a)  // bubble network: ascending
+#pragma unroll
+      for (int b = 0; b + 1 < M - a; ++b) {
+        const double lo = __builtin_fmin(r[b], r[b + 1]);
+        r[b + 1] = __builtin_fmax(r[b], r[b + 1]);
+        r[b] = lo;
+      }
+    double t[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) t[q] = (q < M && q < k) ? r[q < M ? q : 0] : 0.0;
+#pragma unroll
+    for (int h = 1; h < 16; h <<= 1)
+#pragma unroll
+      for (int q = 0; q < 16; q += 2 * h) t[q] = t[q] + t[q + h];
+    score = t[0];
+  }
+  const int64_t bits = __double_as_longlong(score);
+  const int lo = static_cast<int>(bits), hi = static_cast<int>(bits >> 32);
+  int rank = 0;
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    const uint64_t sj_bits =
+        (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readlane(hi, j))) << 32) |
+        static_cast<uint32_t>(__builtin_amdgcn_readlane(lo, j));
+    const double sj = __longlong_as_double(static_cast<int64_t>(sj_bits));
+    rank += (sj < score) | ((sj == score) & (j < i));
+  }
+  return __ballot(i < N && rank < m);
+}
+
+template <int N>
+__global__ __launch_bounds__(kBlock) void k_krum_select_mean(const float* __restrict__ x,
+                                                             int64_t d,
+                                                             const double* __restrict__ partial,
+                                                             int64_t tiles, int f, int m,
+                                                             int32_t* __restrict__ sel,
+                                                             float* __restrict__ out) {
+  constexpr int W = 4, P = N * (N - 1) / 2;
+  __shared__ double esum[P];
+  __shared__ uint64_t mask_s;
+  const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W;
+  float v[N][W];
+  if (c < d) direct_load<N, W>(MatrixRows{x, d}, c, d, v);
+  fold_tiles<P>(partial, tiles, esum);
+  if (threadIdx.x < 64) {
+    const uint64_t mask = krum_mask_wave<N>(esum, f, m);
+    if (threadIdx.x == 0) mask_s = mask;
+    if (blockIdx.x == 0) write_selected(mask, N, nullptr, sel);
+  }
+  __syncthreads();
+  if (c >= d) return;
+  const uint64_t mask = mask_s;
+  double s[W] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    if ((mask >> i) & 1) {
+#pragma unroll
+      for (int e = 0; e < W; ++e) s[e] += static_cast<double>(v[i][e]);
+    }
+  }
+  const double count = static_cast<double>(m);
+  float o[W];
+#pragma unroll
+  for (int e = 0; e < W; ++e) o[e] = static_cast<float>(s[e] / count);
+  if (c + W <= d) {
+    store_w<W>(out + c, o);
+  } else {
+    for (int e = 0; e < W && c + e < d; ++e) out[c + e] = o[e];
+  }
+}
+
+// Workgroups of k_krum_select_mean for d coordinates.
+int64_t select_mean_groups(int64_t d) {
+  const int64_t per = static_cast<int64_t>(kBlock) * 4;
+  return (d + per - 1) / per;
+}
+
+template <int N>
+hipError_t launch_select_mean(const float* x, int64_t d, const DistSums& ds, int f, int m,
+                              int32_t* sel, float* out, hipStream_t s) {
+  launch("krum_select_mean", k_krum_select_mean<N>, dim3(static_cast<unsigned>(select_mean_groups(d))),
+         dim3(kBlock), 0, s, x, d, ds.partial, ds.tiles, f, m, sel, out);
+  return hipGetLastError();
+}
+
+template <int N>
+hipError_t select_mean_dispatch(int n, const float* x, int64_t d, const DistSums& ds, int f,
+                                int m, int32_t* sel, float* out, hipStream_t s) {
+  if constexpr (N > kFusedMaxN) {
+    return hipErrorInvalidValue;
+  } else {
+    if (n == N) return launch_select_mean<N>(x, d, ds, f, m, sel, out, s);
+    return select_mean_dispatch<N + 1>(n, x, d, ds, f, m, sel, out, s);
+  }
 }
 
 // Iterated Krum, Bulyan's selection (theta = n-2f rounds) and the iterated
@@ -600,6 +766,28 @@ size_t mda_scratch_bytes(int n, int f) {
 hipError_t enqueue_krum_select(const DistSums& ds, int f, int m, int32_t* sel, hipStream_t s) {
   launch("krum_select", k_krum_select, dim3(1), dim3(kSelectThreads), 0, s, ds, f, m, sel);
   return hipGetLastError();
+}
+
+namespace {
+bool g_fused = true;
+}  // namespace
+
+bool fused_enabled() { return __atomic_load_n(&g_fused, __ATOMIC_RELAXED); }
+void set_fused(bool on) { __atomic_store_n(&g_fused, on, __ATOMIC_RELAXED); }
+
+bool krum_fusable(const DistPlan& p, const float* out) {
+  if (!fused_enabled() || p.engine != kEngineDirect || p.n < 3 || p.n > kFusedMaxN ||
+      p.width != 4 || p.tiles > kFoldTiles || !out || load_width(out) != 4)
+    return false;
+  // every workgroup reads all tile partials: keep that repeated read small
+  const double reread = static_cast<double>(select_mean_groups(p.d)) * p.entries * p.tiles * 8.0;
+  return reread <= kFusedRereadBytes;
+}
+
+hipError_t enqueue_krum_select_mean(const float* x, const DistSums& ds, int64_t d, int f, int m,
+                                    int32_t* sel, float* out, hipStream_t s) {
+  if (!ds.partial || ds.engine != kEngineDirect || !sel || !out) return hipErrorInvalidValue;
+  return select_mean_dispatch<3>(ds.n, x, d, ds, f, m, sel, out, s);
 }
 
 hipError_t enqueue_bulyan_select(const DistSums& ds, int f, int32_t* sel, hipStream_t s) {
