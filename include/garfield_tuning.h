@@ -38,6 +38,17 @@ int garfield_tuning_set_direct_max_n(int n);
  */
 int garfield_tuning_set_fused(int on);
 
+/*
+ * MDA's search: from this many candidate subsets C(n, f) on (default 2^20),
+ * the least diameter and the lexicographically first subset attaining it are
+ * found through vertex covers of the graph of pairs farther apart than a
+ * threshold (one workgroup; work grows with 2^f, not with C(n, f)); below it
+ * every subset is enumerated. Both give the same subset. Returns the previous
+ * value; a negative argument changes nothing. Process-wide; not synchronised
+ * with calls in flight.
+ */
+long long garfield_tuning_set_mda_cover_min(long long subsets);
+
 /* Engine the distance step would use for (n, d): 0 none (n < 2 or d == 0),
  * 1 direct differences (VALU), 2 Gram (exact integer MFMA). */
 int garfield_tuning_distance_engine(int n, long long d);

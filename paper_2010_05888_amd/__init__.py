@@ -119,6 +119,8 @@ def load():
     lib.garfield_tuning_set_direct_max_n.restype = i32
     lib.garfield_tuning_set_fused.argtypes = [i32]
     lib.garfield_tuning_set_fused.restype = i32
+    lib.garfield_tuning_set_mda_cover_min.argtypes = [ctypes.c_longlong]
+    lib.garfield_tuning_set_mda_cover_min.restype = ctypes.c_longlong
     lib.garfield_tuning_distance_engine.argtypes = [i32, ctypes.c_longlong]
     lib.garfield_tuning_distance_engine.restype = i32
     lib.garfield_tuning_gram_reference.argtypes = [vp, i32, ctypes.c_longlong, vp]
@@ -537,6 +539,12 @@ def set_fused(on: bool) -> bool:
     """Allow (True, the default) or forbid the one-launch Krum / Multi-Krum of
     short inputs; returns the previous setting."""
     return bool(load().garfield_tuning_set_fused(1 if on else 0))
+
+
+def set_mda_cover_min(subsets: int) -> int:
+    """MDA searches by vertex covers from this many subsets C(n, f) on, by
+    enumeration below; returns the previous threshold."""
+    return int(load().garfield_tuning_set_mda_cover_min(subsets))
 
 
 def gram_reference(x: torch.Tensor) -> int:

@@ -85,7 +85,7 @@ garfield_status check_common(const float* x, int n, int f, int64_t d) {
 // waves that reads D through load_dist, so a direct-engine step with few
 // tiles and at most fold_entries entries skips the tile-sum kernel (the
 // selection kernel adds the tiles in the same order).
-constexpr int kFoldSelect = 4 * 16;  // k_krum_select, k_bulyan_select: 16 waves
+constexpr int kFoldSelect = 4 * 16;  // k_krum_select, k_bulyan_select, k_mda_cover: 16 waves
 constexpr int kFoldMda = 4 * 4;      // k_mda_search: 4 waves
 // colsum: the scratch begins with d doubles that receive the column sums
 // (enqueue_distances' colsum).
@@ -349,7 +349,8 @@ garfield_status garfield_mda(const float* x, int n, int f, int64_t d, float* out
   // scratch: the column sums (if used), then the search's per-block results
   const bool cs = out && use_colsum(x, n, d, n - f);
   const size_t cs_bytes = align256(colsum_bytes(cs, d));
-  st = run_distances(x, n, d, cs_bytes + mda_scratch_bytes(n, f), &ds, &scratch, s, kFoldMda, cs);
+  const int fold = mda_uses_cover(n, f) ? kFoldSelect : kFoldMda;
+  st = run_distances(x, n, d, cs_bytes + mda_scratch_bytes(n, f), &ds, &scratch, s, fold, cs);
   if (st != GARFIELD_OK) return st;
   st = to_status(enqueue_mda_select(ds, f, static_cast<char*>(scratch) + cs_bytes, sel, s));
   if (st != GARFIELD_OK || !out) return st;
@@ -719,6 +720,12 @@ int garfield_tuning_set_direct_max_n(int n) {
   if (n < 1 || n > GARFIELD_DIRECT_MAX_N_LIMIT) return -1;
   const int old = direct_max_n();
   set_direct_max_n(n);
+  return old;
+}
+
+long long garfield_tuning_set_mda_cover_min(long long subsets) {
+  const long long old = mda_cover_min();
+  if (subsets >= 0) set_mda_cover_min(subsets);
   return old;
 }
 

@@ -163,7 +163,12 @@ int64_t sqnorm_parts(int64_t d, const float* grad);
 hipError_t enqueue_variance_stats(const DistSums& ds, int h, const float* grad, int64_t d,
                                   double* partial, double* stats, hipStream_t s);
 
-// MDA subset search. Scratch: mda_blocks(n, f) x 16 bytes.
+// MDA subset search: C(n, f) at or above mda_cover_min() subsets by vertex
+// covers of the "farther than" graphs (one workgroup, no scratch), below it
+// by enumeration (scratch: mda_blocks(n, f) x 16 bytes).
+int64_t mda_cover_min();
+void set_mda_cover_min(int64_t subsets);
+bool mda_uses_cover(int n, int f);
 int64_t binomial(int a, int b);  // exact, or -1 if above 2^62
 int mda_blocks(int n, int f);
 size_t mda_scratch_bytes(int n, int f);

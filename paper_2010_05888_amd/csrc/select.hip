@@ -724,6 +724,180 @@ __global__ __launch_bounds__(kBlock) void k_mda_pick(const double* __restrict__ 
   if (static_cast<int>(threadIdx.x) < s) sel[threadIdx.x] = idx[threadIdx.x];
 }
 
+// ---------------------------------------------------------------------------
+// MDA without enumerating the subsets, for large C(n, f). A subset S of s =
+// n - f vectors has diameter at most delta exactly when the f vectors outside
+// it touch every pair farther apart than delta: they form a vertex cover of
+// the graph of those pairs. So the least diameter delta* is the smallest pair
+// distance (or 0) whose "farther than" graph has a vertex cover of at most f
+// vertices -- a binary search over the distances sorted in descending order
+// -- and the winner, the lexicographically first subset of diameter delta*,
+// is built vertex by vertex: v joins S (its far neighbours leave it) whenever
+// the vertices still undecided can then be covered within what is left of the
+// budget, else v leaves. Including the smallest possible vertex at every step
+// gives the lexicographically first subset, and every step keeps a completion
+// of exactly s vertices available, so the result is the enumeration's.
+constexpr int kCoverThreads = 1024;
+
+__device__ __forceinline__ uint64_t low_bits(int n) {
+  return n >= 64 ? ~uint64_t{0} : (uint64_t{1} << n) - 1;
+}
+
+// One root-to-leaf path of the bounded search tree for a cover of at most k
+// more vertices than c: at step t the first uncovered pair (u, v) (u the
+// lowest vertex with an uncovered pair, v its lowest such neighbour) puts v
+// in the cover if bit t of `path` is set, else u. True if the path covers
+// every pair.
+__device__ bool cover_path(const uint64_t* adj, uint64_t U, uint64_t c, int k, int64_t path) {
+  for (int step = 0;; ++step) {
+    int u = -1;
+    uint64_t nb = 0;
+    for (uint64_t cand = U & ~c; cand; cand &= cand - 1) {
+      const int w = __builtin_ctzll(cand);
+      const uint64_t e = adj[w] & ~c;
+      if (e) {
+        u = w;
+        nb = e;
+        break;
+      }
+    }
+    if (u < 0) return true;
+    if (step >= k) return false;
+    const int v = __builtin_ctzll(nb);
+    c |= ((path >> step) & 1) ? (uint64_t{1} << v) : (uint64_t{1} << u);
+  }
+}
+
+// Whether at most f - |F| of the vertices outside S and F cover every pair
+// among them farther apart than delta (the pairs reaching S or F are settled
+// by the caller). All threads of the workgroup call it with the same
+// arguments and get the same answer. First the vertices with more uncovered
+// pairs than the budget go into the cover, all of them at once and again
+// until none is left (any cover within the budget contains each of them):
+// every wave does this alone, lane u holding vertex u's neighbours, so the
+// waves agree without a barrier. Then, unless no pair is left or more pairs
+// are left than the budget's vertices can touch, the 2^k paths of the search
+// tree are spread over the threads, a round of them at a time, until one
+// covers everything.
+__device__ bool cover_feasible(const double* D, int n, double delta, uint64_t S, uint64_t F, int f,
+                               uint64_t* adj) {
+  const uint64_t U = low_bits(n) & ~S & ~F;
+  int k = f - __popcll(F);
+  if (k < 0 || k > 40) return false;  // f <= 16 under the subset limit of the entry points
+  const int t = threadIdx.x, lane = t & 63;
+  const bool live = lane < n && ((U >> lane) & 1);
+  uint64_t a = 0;
+  if (live) {
+    const double* row = D + lane * n;
+    for (int v = 0; v < n; ++v)
+      a |= static_cast<uint64_t>(v != lane && ((U >> v) & 1) && row[v] > delta) << v;
+  }
+  if (t < 64) adj[t] = a;
+  uint64_t C = 0;
+  for (;;) {
+    const uint64_t forced = __ballot(live && __popcll(a & ~C) > k && !((C >> lane) & 1));
+    if (!forced) break;
+    C |= forced;
+    k -= __popcll(forced);
+    if (k < 0) break;
+  }
+  bool found = false;
+  if (k >= 0) {
+    const bool rest = live && !((C >> lane) & 1);
+    const int deg = rest ? __popcll(a & ~C) : 0;
+    int edges = deg, dmax = deg;
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1) {
+      edges += __shfl_xor(edges, m, 64);
+      const int o = __shfl_xor(dmax, m, 64);
+      dmax = o > dmax ? o : dmax;
+    }
+    edges /= 2;
+    if (edges == 0) {
+      found = true;
+    } else if (edges <= k * dmax) {
+      __syncthreads();  // adj written
+      const int64_t paths = int64_t{1} << k;
+      const int64_t rounds = (paths + kCoverThreads - 1) / kCoverThreads;
+      for (int64_t r = 0; r < rounds; ++r) {
+        const int64_t path = r * kCoverThreads + t;
+        const bool mine = path < paths && cover_path(adj, U, C, k, path);
+        if (__syncthreads_or(mine)) {
+          found = true;
+          break;
+        }
+      }
+    }
+  }
+  __syncthreads();  // adj is rebuilt by the next call
+  return found;
+}
+
+__global__ __launch_bounds__(kCoverThreads) void k_mda_cover(DistSums ds, int f,
+                                                             int32_t* __restrict__ sel) {
+  __shared__ double D[kNmax * kNmax];
+  __shared__ double dv[kNmax * (kNmax - 1) / 2 + 1];
+  __shared__ uint64_t adj[kNmax];
+  const int n = ds.n, s = n - f, P = n * (n - 1) / 2;
+  load_dist(ds, D);
+  // the pair distances in descending order (equal ones by pair index), then 0
+  for (int p = threadIdx.x; p < P; p += blockDim.x) {
+    int i = 0, rem = p;
+    while (rem >= n - 1 - i) {
+      rem -= n - 1 - i;
+      ++i;
+    }
+    const double v = D[i * n + i + 1 + rem];
+    int rank = 0, q = 0;
+    for (int a = 0; a < n; ++a)
+      for (int b = a + 1; b < n; ++b, ++q) {
+        const double w = D[a * n + b];
+        rank += (w > v) | ((w == v) & (q < p));
+      }
+    dv[rank] = v;
+  }
+  if (threadIdx.x == 0) dv[P] = 0.0;
+  __syncthreads();
+  // largest j whose distance dv[j] admits a cover (j = 0 always does: no pair
+  // is farther apart than the largest distance)
+  int lo = 0, hi = P;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cover_feasible(D, n, dv[mid], 0, 0, f, adj)) lo = mid;
+    else hi = mid - 1;
+  }
+  const double delta = dv[lo];
+  uint64_t S = 0, F = 0;
+  for (int v = 0; v < n; ++v) {
+    const uint64_t rest = low_bits(n) & ~S & ~F;
+    if (__popcll(S) == s) {
+      F |= rest;
+      break;
+    }
+    if (__popcll(F) == f) {
+      S |= rest;
+      break;
+    }
+    const int lane = threadIdx.x & 63;  // every wave forms the same mask
+    const uint64_t far = __ballot(lane < n && lane != v && D[v * n + lane] > delta);
+    const uint64_t bit = uint64_t{1} << v;
+    if (far & S) {
+      F |= bit;
+      continue;
+    }
+    const uint64_t S2 = S | bit, F2 = F | (far & rest & ~bit);
+    if (__popcll(F2) <= f && cover_feasible(D, n, delta, S2, F2, f, adj)) {
+      S = S2;
+      F = F2;
+    } else {
+      F |= bit;
+    }
+  }
+  // S has exactly s members; the clamp only guards the sel writes
+  while (__popcll(S) > s) S &= ~(uint64_t{1} << (63 - __builtin_clzll(S)));
+  if (threadIdx.x < 64) write_selected(S, n, nullptr, sel);
+}
+
 // Dynamic LDS above 64 KB (n near 64 with large s) is requested from the
 // runtime first.
 hipError_t allow_lds(const void* kernel, size_t bytes) {
@@ -760,6 +934,7 @@ int mda_blocks(int n, int f) {
 }
 
 size_t mda_scratch_bytes(int n, int f) {
+  if (mda_uses_cover(n, f)) return 0;
   return static_cast<size_t>(mda_blocks(n, f)) * (sizeof(double) + sizeof(int64_t));
 }
 
@@ -821,9 +996,27 @@ hipError_t enqueue_peer_mda(const DistSums& ds, int nodes, const int32_t* peers,
   return hipGetLastError();
 }
 
+namespace {
+int64_t g_mda_cover_min = int64_t{1} << 20;
+}  // namespace
+
+int64_t mda_cover_min() { return __atomic_load_n(&g_mda_cover_min, __ATOMIC_RELAXED); }
+void set_mda_cover_min(int64_t subsets) {
+  __atomic_store_n(&g_mda_cover_min, subsets, __ATOMIC_RELAXED);
+}
+
+bool mda_uses_cover(int n, int f) {
+  const int64_t total = binomial(n, f);
+  return total < 0 || total >= mda_cover_min();
+}
+
 hipError_t enqueue_mda_select(const DistSums& ds, int f, void* scratch, int32_t* sel,
                               hipStream_t s) {
   const int n = ds.n;
+  if (mda_uses_cover(n, f)) {
+    launch("mda_cover", k_mda_cover, dim3(1), dim3(kCoverThreads), 0, s, ds, f, sel);
+    return hipGetLastError();
+  }
   int64_t total, per;
   int blocks;
   mda_split(n, f, &total, &per, &blocks);

@@ -317,10 +317,16 @@ def test_mda_branch_and_bound(n, f, d, lim):
     # with a wide range the distances spread, so most prefixes exceed the bound
     # and are skipped with all their completions, also from a thread's first
     # subset in the middle of a block.
+    # (the enumeration is forced: from 2^20 subsets on the library searches by
+    # vertex covers, which tests/test_gpu_mda_cover.py checks)
     assert comb(n, f) > 4096 * 256
     rng = np.random.default_rng(n + f + d)
     x = rng.integers(-lim, lim + 1, size=(n, d)).astype(np.float32)
-    out, sel = gf.mda(_to_dev(x), f)
+    old = gf.set_mda_cover_min(1 << 62)
+    try:
+        out, sel = gf.mda(_to_dev(x), f)
+    finally:
+        gf.set_mda_cover_min(old)
     oo, so = oracle.mda(x, f)
     assert sel.cpu().numpy().tolist() == so.tolist()
     assert np.array_equal(out.cpu().numpy(), oo)
