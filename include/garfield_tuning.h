@@ -49,6 +49,18 @@ int garfield_tuning_set_fused(int on);
  */
 long long garfield_tuning_set_mda_cover_min(long long subsets);
 
+/*
+ * Workgroups per compute unit of the gathering aggregation kernels, capped by
+ * reserving LDS the kernels do not use: fewer loads in flight stream faster
+ * from HBM. 0 (the default) applies each kernel's own rule -- the median's
+ * 16-byte path and Bulyan's beta = 3 path take two to four workgroups per CU
+ * (about 100 to 140 KB of loads in flight per CU), the other gathers no cap;
+ * a positive value caps the median and Bulyan at that many; a negative one
+ * removes every cap. Results do not depend on it. Returns the
+ * previous setting. Process-wide; not synchronised with calls in flight.
+ */
+int garfield_tuning_set_stream_residency(int wgs_per_cu);
+
 /* Engine the distance step would use for (n, d): 0 none (n < 2 or d == 0),
  * 1 direct differences (VALU), 2 Gram (exact integer MFMA). */
 int garfield_tuning_distance_engine(int n, long long d);

@@ -119,6 +119,8 @@ def load():
     lib.garfield_tuning_set_direct_max_n.restype = i32
     lib.garfield_tuning_set_fused.argtypes = [i32]
     lib.garfield_tuning_set_fused.restype = i32
+    lib.garfield_tuning_set_stream_residency.argtypes = [i32]
+    lib.garfield_tuning_set_stream_residency.restype = i32
     lib.garfield_tuning_set_mda_cover_min.argtypes = [ctypes.c_longlong]
     lib.garfield_tuning_set_mda_cover_min.restype = ctypes.c_longlong
     lib.garfield_tuning_distance_engine.argtypes = [i32, ctypes.c_longlong]
@@ -539,6 +541,12 @@ def set_fused(on: bool) -> bool:
     """Allow (True, the default) or forbid the one-launch Krum / Multi-Krum of
     short inputs; returns the previous setting."""
     return bool(load().garfield_tuning_set_fused(1 if on else 0))
+
+
+def set_stream_residency(wgs_per_cu: int) -> int:
+    """Workgroups per CU of the gathering aggregation kernels (0: automatic,
+    < 0: uncapped); returns the previous setting."""
+    return int(load().garfield_tuning_set_stream_residency(wgs_per_cu))
 
 
 def set_mda_cover_min(subsets: int) -> int:

@@ -16,6 +16,11 @@
 // Row indices come from device memory (the selection kernels write them), so
 // no host round trip separates selection from aggregation.
 
+#include <map>
+#include <mutex>
+#include <set>
+#include <utility>
+
 #include "aggregate_body.h"
 #include "device_common.h"
 #include "internal.h"
@@ -154,6 +159,83 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_agg(const float* __restrict__
     bulyan_at<T, W>(src, n, d, sel, beta, cc, sorted + threadIdx.x, out);
 }
 
+// Residency of the gathers. Each lane issues its rows' loads back to back;
+// with as many workgroups per CU as the registers allow, so many loads are in
+// flight that HBM serves them less well. Measured on the median (W = 4, k = 5
+// to 35 rows of 25.6 M floats) and on Bulyan's band path (T = 5 to 19), two to
+// four workgroups per CU -- about 100 to 140 KB of loads in flight per CU --
+// stream 3 to 10 % faster than no cap (k = 11: 0.728 -> 0.773 of 8 TB/s,
+// T = 11: 0.711 -> 0.763); the mean (whose lanes also divide in fp64),
+// Bulyan's general LDS path and the 2-float paths lose with a cap, and the
+// 49-row median is held at two by its registers anyway. The cap is set by
+// reserving LDS that the kernels never touch.
+int g_stream_cap = 0;  // 0: each kernel's rule; > 0: that many workgroups per CU; < 0: none
+
+// The rule: the number of workgroups whose in-flight loads come nearest
+// `target` bytes per CU from below, between 2 and 4.
+int cap_for(int64_t inflight, int64_t target) {
+  const int64_t c = target / inflight;
+  return c < 2 ? 2 : (c > 4 ? 4 : static_cast<int>(c));
+}
+
+std::mutex g_lds_mutex;
+std::map<int, int> g_lds_per_cu;        // device -> LDS bytes per CU
+std::set<std::pair<int, const void*>> g_lds_raised;  // (device, kernel) allowed > 64 KB
+
+int lds_per_cu(int dev) {
+  std::lock_guard<std::mutex> lock(g_lds_mutex);
+  auto it = g_lds_per_cu.find(dev);
+  if (it != g_lds_per_cu.end()) return it->second;
+  int v = 0;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+          hipSuccess || v <= 0) {
+    (void)hipGetLastError();
+    v = 160 * 1024;
+  }
+  g_lds_per_cu.emplace(dev, v);
+  return v;
+}
+
+// Dynamic LDS for a launch of `kernel` (static LDS static_lds bytes) that
+// holds it to rule_cap workgroups per CU (none if negative), unless the
+// tuning setting overrides the rule; 0 when no cap applies. *e receives an
+// error of the attribute call, if any.
+size_t residency_lds(const void* kernel, size_t static_lds, int rule_cap, hipError_t* e) {
+  *e = hipSuccess;
+  const int set = __atomic_load_n(&g_stream_cap, __ATOMIC_RELAXED);
+  const int cap = set == 0 ? rule_cap : set;
+  if (cap <= 0) return 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  const size_t per_cu = static_cast<size_t>(lds_per_cu(dev));
+  // just over a (cap + 1)-th of the CU's LDS: at most `cap` workgroups fit
+  const size_t want = per_cu / (cap + 1) + 1024;
+  const size_t dyn = want > static_lds ? want - static_lds : 0;
+  if (dyn > 65536) {
+    std::lock_guard<std::mutex> lock(g_lds_mutex);
+    if (!g_lds_raised.count({dev, kernel})) {
+      *e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               static_cast<int>(dyn));
+      if (*e != hipSuccess) return 0;
+      g_lds_raised.insert({dev, kernel});
+    }
+  }
+  return dyn;
+}
+
+template <typename K>
+size_t static_lds_of(K kernel) {
+  hipFuncAttributes a{};
+  if (hipFuncGetAttributes(&a, reinterpret_cast<const void*>(kernel)) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return a.sharedSizeBytes;
+}
+
 // ---------------------------------------------------------------------------
 // One pass: a workgroup per kBlock items, so every lane handles one item (the
 // grid-stride loops in the kernels only matter beyond 2^31 - 1 workgroups).
@@ -184,8 +266,12 @@ hipError_t launch_mean_complement(const float* x, int n, int64_t d, const int32_
 template <int K, int W>
 hipError_t launch_median_kw(const float* x, int n, int64_t d, const int32_t* rows, float* out,
                             hipStream_t s) {
-  launch("median", k_median<K, W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s, x, n,
-    d, rows, out);
+  hipError_t e;
+  const int rule = W == 4 ? cap_for(int64_t{kBlock} * W * 4 * K, 100 * 1024) : -1;
+  const size_t lds = residency_lds(reinterpret_cast<const void*>(k_median<K, W>), 0, rule, &e);
+  if (e != hipSuccess) return e;
+  launch("median", k_median<K, W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock),
+         static_cast<uint32_t>(lds), s, x, n, d, rows, out);
   return hipGetLastError();
 }
 
@@ -213,8 +299,16 @@ hipError_t median_dispatch(int k, int width, const float* x, int n, int64_t d,
 template <int T, int W>
 hipError_t launch_bulyan_tw(int beta, const float* x, int n, int64_t d, const int32_t* sel,
                             float* out, hipStream_t s) {
-  launch("bulyan_agg", k_bulyan_agg<T, W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s,
-    x, n, d, sel, beta, out);
+  static const size_t static_lds = static_lds_of(k_bulyan_agg<T, W>);
+  hipError_t e;
+  // the band path only (beta = 3, odd theta: registers, no LDS column)
+  const int rule = (W == 4 && beta == 3 && T % 2 == 1) ? cap_for(int64_t{kBlock} * W * 4 * T, 140 * 1024)
+                                                        : -1;
+  const size_t lds =
+      residency_lds(reinterpret_cast<const void*>(k_bulyan_agg<T, W>), static_lds, rule, &e);
+  if (e != hipSuccess) return e;
+  launch("bulyan_agg", k_bulyan_agg<T, W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock),
+         static_cast<uint32_t>(lds), s, x, n, d, sel, beta, out);
   return hipGetLastError();
 }
 
@@ -244,6 +338,11 @@ hipError_t bulyan_dispatch(int theta, int beta, int width, const float* x, int n
 // an output that is not float-aligned.
 int stream_width(const float* x, const float* out) {
   return (load_width(x) == 4 && load_width(out) == 4) ? 4 : 1;
+}
+
+int stream_residency() { return __atomic_load_n(&g_stream_cap, __ATOMIC_RELAXED); }
+void set_stream_residency(int wgs_per_cu) {
+  __atomic_store_n(&g_stream_cap, wgs_per_cu, __ATOMIC_RELAXED);
 }
 
 hipError_t enqueue_mean_rows(const float* x, int n, int64_t d, const int32_t* rows, int k,

@@ -110,44 +110,78 @@ __device__ __forceinline__ void direct_add(const float (&v)[N][W], float* acc) {
   }
 }
 
+// The column sums (ColSum) of the W coordinates c .. c+W-1 (those before
+// end) of the N rows in v, written to colsum.
+template <int N, int W>
+__device__ __forceinline__ void direct_colsum(const float (&v)[N][W], int64_t c, int64_t end,
+                                              double* __restrict__ colsum) {
+  double o[W];
+#pragma unroll
+  for (int e = 0; e < W; ++e) {
+    ColSum cs;
+#pragma unroll
+    for (int i = 0; i < N; ++i) cs.add(v[i][e]);
+    o[e] = cs.value();
+  }
+  // ordinary (L2-allocating) stores, two doubles at a time: the lanes' halves
+  // of each cache line meet in L2 before it goes to HBM
+  if constexpr (W >= 2) {
+    if (c + W <= end) {
+#pragma unroll
+      for (int e = 0; e < W; e += 2) {
+        d2 t;
+        t.x = o[e];
+        t.y = o[e + 1];
+        *reinterpret_cast<d2*>(colsum + c + e) = t;
+      }
+      return;
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < W; ++e)
+    if (c + e < end) colsum[c + e] = o[e];
+}
+
 // Lane t takes W consecutive coordinates every kBlock * W in [start, end) of
 // rows 0..N-1 of `src`, adding (x_i - x_j)^2 for every pair into acc (pairs
 // in row-major order over i < j). With SUM, it also writes the column sums
-// (ColSum) of its coordinates to colsum.
+// (ColSum) of its coordinates to colsum. The passes that lie wholly before
+// `end` for every lane of the block are software-pipelined: the next pass's
+// loads are issued before this pass's arithmetic, so the rows stream while
+// the VALU works; the sums are formed in the same order either way.
 template <int N, int W, bool SUM = false, class Src>
 __device__ __forceinline__ void direct_accumulate(const Src& src, int64_t start, int64_t end,
                                                   float* acc, double* __restrict__ colsum = nullptr) {
-  for (int64_t c = start + static_cast<int64_t>(threadIdx.x) * W; c < end; c += kBlock * W) {
+  constexpr int64_t kStride = static_cast<int64_t>(kBlock) * W;
+  const int64_t off = static_cast<int64_t>(threadIdx.x) * W;
+  const int64_t full = end > start ? (end - start) / kStride : 0;  // block-uniform
+  int64_t base = start;
+  if (full > 0) {
+    float v[N][W];
+#pragma unroll
+    for (int i = 0; i < N; ++i) load_w<W>(src.row(i) + base + off, v[i]);
+    for (int64_t p = 1; p < full; ++p) {
+      float nv[N][W];
+#pragma unroll
+      for (int i = 0; i < N; ++i) load_w<W>(src.row(i) + base + kStride + off, nv[i]);
+      direct_add<N, W>(v, acc);
+      if constexpr (SUM) direct_colsum<N, W>(v, base + off, end, colsum);
+      base += kStride;
+#pragma unroll
+      for (int i = 0; i < N; ++i)
+#pragma unroll
+        for (int e = 0; e < W; ++e) v[i][e] = nv[i][e];
+    }
+    direct_add<N, W>(v, acc);
+    if constexpr (SUM) direct_colsum<N, W>(v, base + off, end, colsum);
+    base += kStride;
+  }
+  const int64_t c = base + off;  // the partial pass at the end, if any
+  if (c < end) {
     float v[N][W];
     direct_load<N, W>(src, c, end, v);
     direct_add<N, W>(v, acc);
-    if constexpr (SUM) {
-      double o[W];
-#pragma unroll
-      for (int e = 0; e < W; ++e) {
-        ColSum cs;
-#pragma unroll
-        for (int i = 0; i < N; ++i) cs.add(v[i][e]);
-        o[e] = cs.value();
-      }
-      // ordinary (L2-allocating) stores, two doubles at a time: the lanes'
-      // halves of each cache line meet in L2 before it goes to HBM
-      if constexpr (W >= 2) {
-        if (c + W <= end) {
-#pragma unroll
-          for (int e = 0; e < W; e += 2) {
-            d2 t;
-            t.x = o[e];
-            t.y = o[e + 1];
-            *reinterpret_cast<d2*>(colsum + c + e) = t;
-          }
-          continue;
-        }
-      }
-#pragma unroll
-      for (int e = 0; e < W; ++e)
-        if (c + e < end) colsum[c + e] = o[e];
-    }
+    if constexpr (SUM) direct_colsum<N, W>(v, c, end, colsum);
   }
 }
 

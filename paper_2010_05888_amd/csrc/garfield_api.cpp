@@ -729,6 +729,12 @@ long long garfield_tuning_set_mda_cover_min(long long subsets) {
   return old;
 }
 
+int garfield_tuning_set_stream_residency(int wgs_per_cu) {
+  const int old = stream_residency();
+  set_stream_residency(wgs_per_cu < 0 ? -1 : wgs_per_cu);
+  return old;
+}
+
 int garfield_tuning_set_fused(int on) {
   const int old = fused_enabled() ? 1 : 0;
   set_fused(on != 0);

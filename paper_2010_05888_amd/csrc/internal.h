@@ -175,6 +175,13 @@ size_t mda_scratch_bytes(int n, int f);
 hipError_t enqueue_mda_select(const DistSums& ds, int f, void* scratch, int32_t* sel,
                               hipStream_t s);
 
+// Workgroups per CU of the gathering aggregation kernels (aggregate.hip): 0
+// (the default) applies each kernel's rule (median and Bulyan's band path
+// capped at 2 to 4, the rest uncapped), > 0 caps the median and Bulyan at
+// that many, < 0 leaves the residency to the registers.
+int stream_residency();
+void set_stream_residency(int wgs_per_cu);
+
 // Streaming aggregation kernels over the coordinates.
 // Row lists are device int32 arrays (nullptr = rows 0..k-1); an entry outside
 // [0, n) is clamped into it, so a bad list cannot make a kernel read outside x.

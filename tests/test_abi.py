@@ -214,3 +214,12 @@ def test_variance_margin_on_the_host(lib):
     assert math.isnan(lib.garfield_variance_margin(gf.RULE_IDS["bulyan"], 7, 1, stats))
     assert math.isnan(lib.garfield_variance_margin(gf.RULE_IDS["krum"], 4, 1, stats))  # n < 2f+3
     assert math.isnan(lib.garfield_variance_margin(gf.RULE_IDS["krum"], 7, 1, None))
+
+
+def test_tuning_switches_on_the_host(lib):
+    # host-side settings only: no device is touched
+    assert lib.garfield_tuning_set_mda_cover_min(-1) == 1 << 20  # the default, unchanged
+    assert lib.garfield_tuning_set_mda_cover_min(5) == 1 << 20
+    assert lib.garfield_tuning_set_mda_cover_min(1 << 20) == 5
+    assert lib.garfield_tuning_set_fused(0) == 1
+    assert lib.garfield_tuning_set_fused(1) == 0

@@ -70,3 +70,30 @@ def test_header_generation_is_deterministic(tmp_path):
     p1 = gen.write_header(str(tmp_path / "a.inc"), nmax=12)
     p2 = gen.write_header(str(tmp_path / "b.inc"), nmax=12)
     assert open(p1).read() == open(p2).read()
+
+
+@pytest.mark.parametrize("base", sorted(gen.BASES))
+@pytest.mark.parametrize("p", range(1, 7))
+def test_base_networks_sort(base, p):
+    # both base networks sort every 0/1 input (all of them up to 16 wires,
+    # 2^17 random ones above) and have Batcher's comparator count,
+    # (p^2 - p + 4) 2^(p-2) - 1 for n = 2^p wires
+    n = 2 ** p
+    cmps = gen.BASES[base](n)
+    assert len(cmps) == (p * p - p + 4) * 2 ** p // 4 - 1
+    assert all(0 <= i < j < n for i, j in cmps)
+    if n <= 16:
+        cols = _all_binary(n)
+    else:
+        rng = np.random.default_rng(n)
+        cols = [rng.integers(0, 2, 1 << 17).astype(np.float32) for _ in range(n)]
+    for i, j in cmps:
+        cols[i], cols[j] = np.minimum(cols[i], cols[j]), np.maximum(cols[i], cols[j])
+    a = np.stack(cols, axis=1)
+    assert np.all(a[:, :-1] <= a[:, 1:])
+
+
+def test_pairwise_prunes_the_large_medians():
+    # the generator keeps the cheaper base: the k = 49 median needs 512 operations
+    ops, _ = gen.network(49, "median")
+    assert gen._cost(ops) == 512
