@@ -203,6 +203,11 @@ def algorithmic(kernel, w):
         k = {"krum": 1, "multikrum": w.m, "multikrum_iterated": w.m,
              "mda": n - f}.get(w.rules[0], n)
         return "hbm", 4.0 * (k + 1) * d, None
+    if kernel == "krum_select_mean":
+        # the rule's mean reads the m selected rows and writes the output; this
+        # kernel reads every row's coordinates before the selection is known
+        k = 1 if w.rules[0] == "krum" else w.m
+        return "hbm", 4.0 * (k + 1) * d, 4.0 * (n + 1) * d
     if kernel == "median":
         k = w.m if w.rules == ("multikrum-median",) else n
         return "hbm", 4.0 * (k + 1) * d, None
