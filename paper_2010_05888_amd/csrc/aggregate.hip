@@ -37,10 +37,8 @@ __global__ __launch_bounds__(kBlock) void k_mean_rows(const float* __restrict__ 
                                                       int64_t d, const int32_t* __restrict__ rows,
                                                       int k, float* __restrict__ out) {
   const MatrixRows src{x, d};
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * W;
-  for (int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W; c < d;
-       c += stride)
-    mean_at<W>(src, n, d, rows, k, c, out);
+  const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W;
+  if (c < d) with_rows(rows, n, [&](const auto& r) { mean_at<W>(src, d, r, k, c, out); });
 }
 
 // Mean of the k distinct rows of sel from the distance step's column sums
@@ -117,8 +115,8 @@ __global__ __launch_bounds__(kBlock) void k_mean_complement(const float* __restr
     } else {
 #pragma unroll
       for (int e = 0; e < W; ++e) acc[e] = 0.0;
-      if (full) sum_rows_at<W, true, true>(src, n, d, sel, k, c, acc);
-      else sum_rows_at<W, false, true>(src, n, d, sel, k, c, acc);
+      if (full) sum_rows_at<W, true, true>(src, d, ListedRows{sel, n}, k, c, acc);
+      else sum_rows_at<W, false, true>(src, d, ListedRows{sel, n}, k, c, acc);
     }
     float o[W];
 #pragma unroll
@@ -139,10 +137,8 @@ __global__ __launch_bounds__(kBlock) void k_median(const float* __restrict__ x, 
                                                    const int32_t* __restrict__ rows,
                                                    float* __restrict__ out) {
   const MatrixRows src{x, d};
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * W;
-  for (int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W; c < d;
-       c += stride)
-    median_at<K, W>(src, n, d, rows, c, out);
+  const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W;
+  if (c < d) with_rows(rows, n, [&](const auto& r) { median_at<K, W>(src, d, r, c, out); });
 }
 
 // Bulyan aggregation for theta = T selected rows (bulyan_at); the sorted
@@ -153,10 +149,8 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_agg(const float* __restrict__
                                                        int beta, float* __restrict__ out) {
   __shared__ float sorted[T * kBlock];
   const MatrixRows src{x, d};
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * W;
-  for (int64_t cc = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W; cc < d;
-       cc += stride)
-    bulyan_at<T, W>(src, n, d, sel, beta, cc, sorted + threadIdx.x, out);
+  const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W;
+  if (c < d) bulyan_at<T, W>(src, d, ListedRows{sel, n}, beta, c, sorted + threadIdx.x, out);
 }
 
 // Residency of the gathers. Each lane issues its rows' loads back to back;
@@ -237,28 +231,33 @@ size_t static_lds_of(K kernel) {
 }
 
 // ---------------------------------------------------------------------------
-// One pass: a workgroup per kBlock items, so every lane handles one item (the
-// grid-stride loops in the kernels only matter beyond 2^31 - 1 workgroups).
-// A single pass streams measurably faster than a capped grid looping over d.
+// One pass: a workgroup per kBlock items, so every lane handles one item. A
+// single pass streams measurably faster than a capped grid looping over d,
+// and the gathers have no loop to hoist their per-row address arithmetic out
+// of (where it would hold one register pair per row). 2^31 - 1 workgroups of
+// kBlock lanes cover any d a device holds; beyond them grid_for returns 0 and
+// the launch is refused (mean_complement alone still loops).
 int grid_for(int64_t items) {
-  int64_t blocks = (items + kBlock - 1) / kBlock;
-  if (blocks > 0x7fffffff) blocks = 0x7fffffff;
-  if (blocks < 1) blocks = 1;
-  return static_cast<int>(blocks);
+  const int64_t blocks = (items + kBlock - 1) / kBlock;
+  if (blocks > 0x7fffffff) return 0;
+  return blocks < 1 ? 1 : static_cast<int>(blocks);
 }
 
 template <int W>
 hipError_t launch_mean(const float* x, int n, int64_t d, const int32_t* rows, int k, float* out,
                        hipStream_t s) {
-  launch("mean_rows", k_mean_rows<W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0, s, x, n,
-    d, rows, k, out);
+  const int grid = grid_for((d + W - 1) / W);
+  if (grid == 0) return hipErrorInvalidValue;
+  launch("mean_rows", k_mean_rows<W>, dim3(grid), dim3(kBlock), 0, s, x, n, d, rows, k, out);
   return hipGetLastError();
 }
 
 template <int W>
 hipError_t launch_mean_complement(const float* x, int n, int64_t d, const int32_t* sel, int k,
                                   const double* colsum, float* out, hipStream_t s) {
-  launch("mean_complement", k_mean_complement<W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock), 0,
+  const int grid = grid_for((d + W - 1) / W);
+  if (grid == 0) return hipErrorInvalidValue;
+  launch("mean_complement", k_mean_complement<W>, dim3(grid), dim3(kBlock), 0,
          s, x, n, d, sel, k, colsum, out);
   return hipGetLastError();
 }
@@ -270,8 +269,10 @@ hipError_t launch_median_kw(const float* x, int n, int64_t d, const int32_t* row
   const int rule = W == 4 ? cap_for(int64_t{kBlock} * W * 4 * K, 100 * 1024) : -1;
   const size_t lds = residency_lds(reinterpret_cast<const void*>(k_median<K, W>), 0, rule, &e);
   if (e != hipSuccess) return e;
-  launch("median", k_median<K, W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock),
-         static_cast<uint32_t>(lds), s, x, n, d, rows, out);
+  const int grid = grid_for((d + W - 1) / W);
+  if (grid == 0) return hipErrorInvalidValue;
+  launch("median", k_median<K, W>, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lds), s, x, n,
+         d, rows, out);
   return hipGetLastError();
 }
 
@@ -307,8 +308,10 @@ hipError_t launch_bulyan_tw(int beta, const float* x, int n, int64_t d, const in
   const size_t lds =
       residency_lds(reinterpret_cast<const void*>(k_bulyan_agg<T, W>), static_lds, rule, &e);
   if (e != hipSuccess) return e;
-  launch("bulyan_agg", k_bulyan_agg<T, W>, dim3(grid_for((d + W - 1) / W)), dim3(kBlock),
-         static_cast<uint32_t>(lds), s, x, n, d, sel, beta, out);
+  const int grid = grid_for((d + W - 1) / W);
+  if (grid == 0) return hipErrorInvalidValue;
+  launch("bulyan_agg", k_bulyan_agg<T, W>, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lds), s,
+         x, n, d, sel, beta, out);
   return hipGetLastError();
 }
 

@@ -2,8 +2,8 @@
 // kernels over one row-major matrix (aggregate.hip) and the kernels over a
 // table of segments (segtable.hip). Each body handles W consecutive
 // coordinates c .. c+W-1 of a segment of length d and writes them to out + c;
-// the rows come from a source (rows.h) and, when `rows` is given, only the
-// listed ones are used. NT: nontemporal loads (rows read once); kernels whose
+// the rows come from a source (rows.h) and a row rule (AllRows, ListedRows)
+// says which of them are used. NT: nontemporal loads (rows read once); kernels whose
 // workgroups share rows read them with ordinary loads, which stay in L2.
 #pragma once
 
@@ -21,6 +21,30 @@ __device__ __forceinline__ int64_t row_of(const int32_t* __restrict__ rows, int 
   return static_cast<int64_t>(r < 0 ? 0 : (r >= n ? n - 1 : r));
 }
 
+// The rows a body reads, as a type, so that its loop over the rows has no
+// branch: AllRows reads rows 0 .. k-1, ListedRows the listed ones, clamped
+// into [0, n). A kernel given an optional list branches once (with_rows); a
+// choice made per row made each row's load wait for the scalar load of its
+// own index, where branch-free indices are fetched ahead of the loads.
+struct AllRows {
+  __device__ __forceinline__ int64_t operator()(int t) const { return t; }
+};
+
+struct ListedRows {
+  const int32_t* list;
+  int n;
+  __device__ __forceinline__ int64_t operator()(int t) const {
+    const int r = list[t];
+    return static_cast<int64_t>(r < 0 ? 0 : (r >= n ? n - 1 : r));
+  }
+};
+
+template <class F>
+__device__ __forceinline__ void with_rows(const int32_t* rows, int n, const F& f) {
+  if (rows) f(ListedRows{rows, n});
+  else f(AllRows{});
+}
+
 template <int W>
 __device__ __forceinline__ void store_out(float* __restrict__ out, int64_t c, int64_t d,
                                           bool full, const float* o) {
@@ -34,16 +58,15 @@ __device__ __forceinline__ void store_out(float* __restrict__ out, int64_t c, in
 // ---------------------------------------------------------------------------
 // Mean of k rows: fp64 sum of the rows in the order listed, eight loads in
 // flight at a time, one rounding at the end.
-template <int W, bool FULL, bool NT, class Src>
-__device__ __forceinline__ void sum_rows_at(const Src& src, int n, int64_t d,
-                                            const int32_t* __restrict__ rows, int k, int64_t c,
-                                            double* acc) {
+template <int W, bool FULL, bool NT, class Src, class L>
+__device__ __forceinline__ void sum_rows_at(const Src& src, int64_t d, const L& rows, int k,
+                                            int64_t c, double* acc) {
   int t = 0;
   for (; t + 8 <= k; t += 8) {
     float v[8][W];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const float* p = src.row(row_of(rows, t + u, n)) + c;
+      const float* p = src.row(rows(t + u)) + c;
       if constexpr (FULL) load_w<W, NT>(p, v[u]); else load_w_tail<W>(p, d - c, v[u]);
     }
 #pragma unroll
@@ -53,23 +76,22 @@ __device__ __forceinline__ void sum_rows_at(const Src& src, int n, int64_t d,
   }
   for (; t < k; ++t) {
     float v[W];
-    const float* p = src.row(row_of(rows, t, n)) + c;
+    const float* p = src.row(rows(t)) + c;
     if constexpr (FULL) load_w<W, NT>(p, v); else load_w_tail<W>(p, d - c, v);
 #pragma unroll
     for (int e = 0; e < W; ++e) acc[e] += static_cast<double>(v[e]);
   }
 }
 
-template <int W, bool NT = true, class Src>
-__device__ __forceinline__ void mean_at(const Src& src, int n, int64_t d,
-                                        const int32_t* __restrict__ rows, int k, int64_t c,
-                                        float* __restrict__ out) {
+template <int W, bool NT = true, class Src, class L>
+__device__ __forceinline__ void mean_at(const Src& src, int64_t d, const L& rows, int k,
+                                        int64_t c, float* __restrict__ out) {
   double acc[W];
 #pragma unroll
   for (int e = 0; e < W; ++e) acc[e] = 0.0;
   const bool full = c + W <= d;
-  if (full) sum_rows_at<W, true, NT>(src, n, d, rows, k, c, acc);
-  else sum_rows_at<W, false, NT>(src, n, d, rows, k, c, acc);
+  if (full) sum_rows_at<W, true, NT>(src, d, rows, k, c, acc);
+  else sum_rows_at<W, false, NT>(src, d, rows, k, c, acc);
   const double count = static_cast<double>(k);
   float o[W];
 #pragma unroll
@@ -80,19 +102,18 @@ __device__ __forceinline__ void mean_at(const Src& src, int n, int64_t d,
 // ---------------------------------------------------------------------------
 // Coordinate-wise median of K rows: all K loads back to back, then the
 // selection network per coordinate.
-template <int K, int W, bool NT = true, class Src>
-__device__ __forceinline__ void median_at(const Src& src, int n, int64_t d,
-                                          const int32_t* __restrict__ rows, int64_t c,
+template <int K, int W, bool NT = true, class Src, class L>
+__device__ __forceinline__ void median_at(const Src& src, int64_t d, const L& rows, int64_t c,
                                           float* __restrict__ out) {
   using Net = MedianNet<K>;
   float v[K][W];
   const bool full = c + W <= d;
   if (full) {
 #pragma unroll
-    for (int t = 0; t < K; ++t) load_w<W, NT>(src.row(row_of(rows, t, n)) + c, v[t]);
+    for (int t = 0; t < K; ++t) load_w<W, NT>(src.row(rows(t)) + c, v[t]);
   } else {
 #pragma unroll
-    for (int t = 0; t < K; ++t) load_w_tail<W>(src.row(row_of(rows, t, n)) + c, d - c, v[t]);
+    for (int t = 0; t < K; ++t) load_w_tail<W>(src.row(rows(t)) + c, d - c, v[t]);
   }
   float o[W];
 #pragma unroll
@@ -160,10 +181,9 @@ __device__ __forceinline__ float bulyan3_of_band(const float* a) {
 // iff key(L_a) < key(R_{K+1-a}) (a missing R counts as +inf). The number of
 // left values taken is the count of such a. `col` is this thread's column of
 // a T x kBlock LDS array (col[r * kBlock]).
-template <int T, int W, bool NT = true, class Src>
-__device__ __forceinline__ void bulyan_at(const Src& src, int n, int64_t d,
-                                          const int32_t* __restrict__ sel, int beta, int64_t cc,
-                                          float* col, float* __restrict__ out) {
+template <int T, int W, bool NT = true, class Src, class L>
+__device__ __forceinline__ void bulyan_at(const Src& src, int64_t d, const L& sel, int beta,
+                                          int64_t cc, float* col, float* __restrict__ out) {
   using Net = SortNet<T>;
   constexpr bool kOdd = (T % 2) == 1;
   constexpr int c = kOdd ? (T - 1) / 2 : T / 2;
@@ -174,10 +194,10 @@ __device__ __forceinline__ void bulyan_at(const Src& src, int n, int64_t d,
   const bool full = cc + W <= d;
   if (full) {
 #pragma unroll
-    for (int t = 0; t < T; ++t) load_w<W, NT>(src.row(row_of(sel, t, n)) + cc, v[t]);
+    for (int t = 0; t < T; ++t) load_w<W, NT>(src.row(sel(t)) + cc, v[t]);
   } else {
 #pragma unroll
-    for (int t = 0; t < T; ++t) load_w_tail<W>(src.row(row_of(sel, t, n)) + cc, d - cc, v[t]);
+    for (int t = 0; t < T; ++t) load_w_tail<W>(src.row(sel(t)) + cc, d - cc, v[t]);
   }
   float o[W];
   if constexpr (kOdd && T >= 3) {

@@ -174,8 +174,8 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_nodes(const float* __restrict
   node_tile(nodes, &tile, &v);
   const int64_t c = (tile * kBlock + threadIdx.x) * W;
   if (c < d)
-    bulyan_at<T, W, false>(MatrixRows{x, d}, n, d, sel + static_cast<int64_t>(v) * T, beta, c,
-                           sorted + threadIdx.x, y + static_cast<int64_t>(v) * d);
+    bulyan_at<T, W, false>(MatrixRows{x, d}, d, ListedRows{sel + static_cast<int64_t>(v) * T, n},
+                           beta, c, sorted + threadIdx.x, y + static_cast<int64_t>(v) * d);
 }
 
 // Bulyan's width as the single-rule kernel chooses it for float-aligned rows

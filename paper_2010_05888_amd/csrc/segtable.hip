@@ -52,8 +52,9 @@ __global__ __launch_bounds__(kBlock) void k_mean_rows_seg(const float* const* __
   const int s = seg_of(tab, blockIdx.x);
   const int64_t c = seg_coord<W>(tab, s, blockIdx.x);
   if (c < tab.dims[s])
-    mean_at<W>(TableRows{ptrs + static_cast<int64_t>(s) * n}, n, tab.dims[s], rows, k, c,
-               tab.outs[s]);
+    with_rows(rows, n, [&](const auto& r) {
+      mean_at<W>(TableRows{ptrs + static_cast<int64_t>(s) * n}, tab.dims[s], r, k, c, tab.outs[s]);
+    });
 }
 
 template <int K, int W>
@@ -63,8 +64,10 @@ __global__ __launch_bounds__(kBlock) void k_median_seg(const float* const* __res
   const int s = seg_of(tab, blockIdx.x);
   const int64_t c = seg_coord<W>(tab, s, blockIdx.x);
   if (c < tab.dims[s])
-    median_at<K, W>(TableRows{ptrs + static_cast<int64_t>(s) * n}, n, tab.dims[s], rows, c,
-                    tab.outs[s]);
+    with_rows(rows, n, [&](const auto& r) {
+      median_at<K, W>(TableRows{ptrs + static_cast<int64_t>(s) * n}, tab.dims[s], r, c,
+                      tab.outs[s]);
+    });
 }
 
 template <int T, int W>
@@ -75,8 +78,8 @@ __global__ __launch_bounds__(kBlock) void k_bulyan_agg_seg(const float* const* _
   const int s = seg_of(tab, blockIdx.x);
   const int64_t c = seg_coord<W>(tab, s, blockIdx.x);
   if (c < tab.dims[s])
-    bulyan_at<T, W>(TableRows{ptrs + static_cast<int64_t>(s) * n}, n, tab.dims[s], sel, beta, c,
-                    sorted + threadIdx.x, tab.outs[s]);
+    bulyan_at<T, W>(TableRows{ptrs + static_cast<int64_t>(s) * n}, tab.dims[s],
+                    ListedRows{sel, n}, beta, c, sorted + threadIdx.x, tab.outs[s]);
 }
 
 // Cut a batch of K segments into launches of at most kSegMax segments and
