@@ -32,13 +32,16 @@ namespace {
 
 // The kernels over one row-major n x d matrix; the per-coordinate work is in
 // aggregate_body.h (shared with the segment-table kernels).
-template <int W>
+// LISTED: the rows listed in `rows` (ListedRows), else rows 0 .. k-1.
+template <int W, bool LISTED>
 __global__ __launch_bounds__(kBlock) void k_mean_rows(const float* __restrict__ x, int n,
                                                       int64_t d, const int32_t* __restrict__ rows,
                                                       int k, float* __restrict__ out) {
   const MatrixRows src{x, d};
   const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W;
-  if (c < d) with_rows(rows, n, [&](const auto& r) { mean_at<W>(src, d, r, k, c, out); });
+  if (c >= d) return;
+  if constexpr (LISTED) mean_at<W>(src, d, ListedRows{rows, n}, k, c, out);
+  else mean_at<W>(src, d, AllRows{}, k, c, out);
 }
 
 // Mean of the k distinct rows of sel from the distance step's column sums
@@ -132,13 +135,15 @@ __global__ __launch_bounds__(kBlock) void k_mean_complement(const float* __restr
 // registers of two waves per SIMD.
 constexpr int kMedianX4MaxK = 52;
 
-template <int K, int W>
+template <int K, int W, bool LISTED>
 __global__ __launch_bounds__(kBlock) void k_median(const float* __restrict__ x, int n, int64_t d,
                                                    const int32_t* __restrict__ rows,
                                                    float* __restrict__ out) {
   const MatrixRows src{x, d};
   const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * W;
-  if (c < d) with_rows(rows, n, [&](const auto& r) { median_at<K, W>(src, d, r, c, out); });
+  if (c >= d) return;
+  if constexpr (LISTED) median_at<K, W>(src, d, ListedRows{rows, n}, c, out);
+  else median_at<K, W>(src, d, AllRows{}, c, out);
 }
 
 // Bulyan aggregation for theta = T selected rows (bulyan_at); the sorted
@@ -248,7 +253,12 @@ hipError_t launch_mean(const float* x, int n, int64_t d, const int32_t* rows, in
                        hipStream_t s) {
   const int grid = grid_for((d + W - 1) / W);
   if (grid == 0) return hipErrorInvalidValue;
-  launch("mean_rows", k_mean_rows<W>, dim3(grid), dim3(kBlock), 0, s, x, n, d, rows, k, out);
+  if (rows)
+    launch("mean_rows", k_mean_rows<W, true>, dim3(grid), dim3(kBlock), 0, s, x, n, d, rows, k,
+           out);
+  else
+    launch("mean_rows", k_mean_rows<W, false>, dim3(grid), dim3(kBlock), 0, s, x, n, d, rows, k,
+           out);
   return hipGetLastError();
 }
 
@@ -262,18 +272,26 @@ hipError_t launch_mean_complement(const float* x, int n, int64_t d, const int32_
   return hipGetLastError();
 }
 
-template <int K, int W>
-hipError_t launch_median_kw(const float* x, int n, int64_t d, const int32_t* rows, float* out,
-                            hipStream_t s) {
+template <int K, int W, bool LISTED>
+hipError_t launch_median_kwl(const float* x, int n, int64_t d, const int32_t* rows, float* out,
+                             hipStream_t s) {
   hipError_t e;
   const int rule = W == 4 ? cap_for(int64_t{kBlock} * W * 4 * K, 100 * 1024) : -1;
-  const size_t lds = residency_lds(reinterpret_cast<const void*>(k_median<K, W>), 0, rule, &e);
+  const size_t lds =
+      residency_lds(reinterpret_cast<const void*>(k_median<K, W, LISTED>), 0, rule, &e);
   if (e != hipSuccess) return e;
   const int grid = grid_for((d + W - 1) / W);
   if (grid == 0) return hipErrorInvalidValue;
-  launch("median", k_median<K, W>, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lds), s, x, n,
-         d, rows, out);
+  launch("median", k_median<K, W, LISTED>, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lds),
+         s, x, n, d, rows, out);
   return hipGetLastError();
+}
+
+template <int K, int W>
+hipError_t launch_median_kw(const float* x, int n, int64_t d, const int32_t* rows, float* out,
+                            hipStream_t s) {
+  if (rows) return launch_median_kwl<K, W, true>(x, n, d, rows, out, s);
+  return launch_median_kwl<K, W, false>(x, n, d, rows, out, s);
 }
 
 template <int K>

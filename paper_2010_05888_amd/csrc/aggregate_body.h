@@ -22,28 +22,26 @@ __device__ __forceinline__ int64_t row_of(const int32_t* __restrict__ rows, int 
 }
 
 // The rows a body reads, as a type, so that its loop over the rows has no
-// branch: AllRows reads rows 0 .. k-1, ListedRows the listed ones, clamped
-// into [0, n). A kernel given an optional list branches once (with_rows); a
-// choice made per row made each row's load wait for the scalar load of its
-// own index, where branch-free indices are fetched ahead of the loads.
+// branch: AllRows reads rows 0 .. k-1, ListedRows the listed ones. Kernels
+// given an optional list come in both forms and the host picks one: a choice
+// made per row made each row's load wait for the scalar load of its own
+// index, where branch-free indices are fetched together ahead of the loads.
 struct AllRows {
   __device__ __forceinline__ int64_t operator()(int t) const { return t; }
 };
 
+// An index outside [0, n) breaks a precondition; it reads row n - 1 rather
+// than memory outside the input (one unsigned minimum, and the row offset is
+// then an unsigned 32 x 64-bit product: few scalar instructions per row).
 struct ListedRows {
   const int32_t* list;
   int n;
   __device__ __forceinline__ int64_t operator()(int t) const {
-    const int r = list[t];
-    return static_cast<int64_t>(r < 0 ? 0 : (r >= n ? n - 1 : r));
+    const uint32_t r = static_cast<uint32_t>(list[t]);
+    const uint32_t last = static_cast<uint32_t>(n - 1);
+    return static_cast<int64_t>(r < last ? r : last);
   }
 };
-
-template <class F>
-__device__ __forceinline__ void with_rows(const int32_t* rows, int n, const F& f) {
-  if (rows) f(ListedRows{rows, n});
-  else f(AllRows{});
-}
 
 template <int W>
 __device__ __forceinline__ void store_out(float* __restrict__ out, int64_t c, int64_t d,

@@ -640,7 +640,7 @@ garfield_status garfield_seg_aggregate_table(garfield_segmented* seg, const floa
     case GARFIELD_RULE_BULYAN:
       return to_status(enqueue_bulyan_table(ptrs, n, seg->f, dims, outs, K, seg->sel, s));
     case GARFIELD_RULE_MEDIAN:
-      return to_status(enqueue_median_table(ptrs, n, dims, outs, K, nullptr, n, s));
+      return to_status(enqueue_median_table(ptrs, n, dims, outs, K, s));
     default:  // Average
       return to_status(enqueue_mean_rows_table(ptrs, n, dims, outs, K, nullptr, n, s));
   }

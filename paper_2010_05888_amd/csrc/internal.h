@@ -129,9 +129,9 @@ int32_t* table_reference_slot(void* probe_space);
 hipError_t enqueue_mean_rows_table(const float* const* ptrs, int n, const int64_t* dims,
                                    float* const* outs, int K, const int32_t* rows, int k,
                                    hipStream_t s);
+// The coordinate-wise median over all n vectors of each segment.
 hipError_t enqueue_median_table(const float* const* ptrs, int n, const int64_t* dims,
-                                float* const* outs, int K, const int32_t* rows, int k,
-                                hipStream_t s);
+                                float* const* outs, int K, hipStream_t s);
 hipError_t enqueue_bulyan_table(const float* const* ptrs, int n, int f, const int64_t* dims,
                                 float* const* outs, int K, const int32_t* sel, hipStream_t s);
 

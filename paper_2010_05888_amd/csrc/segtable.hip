@@ -45,29 +45,28 @@ __device__ __forceinline__ int64_t seg_coord(const SegTable& tab, int s, int b) 
   return (static_cast<int64_t>(b - tab.first[s]) * kBlock + threadIdx.x) * W;
 }
 
-template <int W>
+// LISTED: the rows listed in `rows`, else rows 0 .. k-1.
+template <int W, bool LISTED>
 __global__ __launch_bounds__(kBlock) void k_mean_rows_seg(const float* const* __restrict__ ptrs,
                                                           int n, const int32_t* __restrict__ rows,
                                                           int k, SegTable tab) {
   const int s = seg_of(tab, blockIdx.x);
   const int64_t c = seg_coord<W>(tab, s, blockIdx.x);
-  if (c < tab.dims[s])
-    with_rows(rows, n, [&](const auto& r) {
-      mean_at<W>(TableRows{ptrs + static_cast<int64_t>(s) * n}, tab.dims[s], r, k, c, tab.outs[s]);
-    });
+  if (c >= tab.dims[s]) return;
+  const TableRows src{ptrs + static_cast<int64_t>(s) * n};
+  if constexpr (LISTED) mean_at<W>(src, tab.dims[s], ListedRows{rows, n}, k, c, tab.outs[s]);
+  else mean_at<W>(src, tab.dims[s], AllRows{}, k, c, tab.outs[s]);
 }
 
+// The median over all K = n vectors of each segment.
 template <int K, int W>
-__global__ __launch_bounds__(kBlock) void k_median_seg(const float* const* __restrict__ ptrs, int n,
-                                                       const int32_t* __restrict__ rows,
+__global__ __launch_bounds__(kBlock) void k_median_seg(const float* const* __restrict__ ptrs,
                                                        SegTable tab) {
   const int s = seg_of(tab, blockIdx.x);
   const int64_t c = seg_coord<W>(tab, s, blockIdx.x);
   if (c < tab.dims[s])
-    with_rows(rows, n, [&](const auto& r) {
-      median_at<K, W>(TableRows{ptrs + static_cast<int64_t>(s) * n}, tab.dims[s], r, c,
-                      tab.outs[s]);
-    });
+    median_at<K, W>(TableRows{ptrs + static_cast<int64_t>(s) * K}, tab.dims[s], AllRows{}, c,
+                    tab.outs[s]);
 }
 
 template <int T, int W>
@@ -139,18 +138,18 @@ hipError_t dist_seg_dispatch(int n, const float* const* ptrs, const int64_t* dim
 // Widths as the matrix kernels choose them: the K (or T) x W values of a lane
 // within the registers of two waves per SIMD.
 template <int K>
-hipError_t median_seg_dispatch(int k, const float* const* ptrs, int n, const int32_t* rows,
-                               const int64_t* dims, float* const* outs, int nseg, hipStream_t s) {
+hipError_t median_seg_dispatch(int n, const float* const* ptrs, const int64_t* dims,
+                               float* const* outs, int nseg, hipStream_t s) {
   if constexpr (K > kNmax) {
     return hipErrorInvalidValue;
   } else {
-    if (k != K) return median_seg_dispatch<K + 1>(k, ptrs, n, rows, dims, outs, nseg, s);
+    if (n != K) return median_seg_dispatch<K + 1>(n, ptrs, dims, outs, nseg, s);
     constexpr int W = K <= 52 ? 4 : 2;
     auto per = [](int64_t) { return static_cast<int64_t>(kBlock) * W; };
     return for_each_launch(dims, outs, nseg, per, [&](int g0, const SegTable& tab,
                                                       int64_t total) {
       launch("median_seg", k_median_seg<K, W>, dim3(static_cast<unsigned>(total)), dim3(kBlock), 0,
-             s, ptrs + static_cast<int64_t>(g0) * n, n, rows, tab);
+             s, ptrs + static_cast<int64_t>(g0) * K, tab);
       return hipGetLastError();
     });
   }
@@ -200,16 +199,19 @@ hipError_t enqueue_mean_rows_table(const float* const* ptrs, int n, const int64_
                                    hipStream_t s) {
   return for_each_launch(dims, outs, K, kAggSpan, [&](int g0, const SegTable& tab,
                                                         int64_t total) {
-    launch("mean_rows_seg", k_mean_rows_seg<4>, dim3(static_cast<unsigned>(total)), dim3(kBlock),
-           0, s, ptrs + static_cast<int64_t>(g0) * n, n, rows, k, tab);
+    if (rows)
+      launch("mean_rows_seg", k_mean_rows_seg<4, true>, dim3(static_cast<unsigned>(total)),
+             dim3(kBlock), 0, s, ptrs + static_cast<int64_t>(g0) * n, n, rows, k, tab);
+    else
+      launch("mean_rows_seg", k_mean_rows_seg<4, false>, dim3(static_cast<unsigned>(total)),
+             dim3(kBlock), 0, s, ptrs + static_cast<int64_t>(g0) * n, n, rows, k, tab);
     return hipGetLastError();
   });
 }
 
 hipError_t enqueue_median_table(const float* const* ptrs, int n, const int64_t* dims,
-                                float* const* outs, int K, const int32_t* rows, int k,
-                                hipStream_t s) {
-  return median_seg_dispatch<1>(k, ptrs, n, rows, dims, outs, K, s);
+                                float* const* outs, int K, hipStream_t s) {
+  return median_seg_dispatch<1>(n, ptrs, dims, outs, K, s);
 }
 
 hipError_t enqueue_bulyan_table(const float* const* ptrs, int n, int f, const int64_t* dims,
