@@ -15,12 +15,6 @@ namespace garfield {
 
 #include "networks.inc"
 
-__device__ __forceinline__ int64_t row_of(const int32_t* __restrict__ rows, int t, int n) {
-  if (!rows) return t;
-  const int r = rows[t];
-  return static_cast<int64_t>(r < 0 ? 0 : (r >= n ? n - 1 : r));
-}
-
 // The rows a body reads, as a type, so that its loop over the rows has no
 // branch: AllRows reads rows 0 .. k-1, ListedRows the listed ones. Kernels
 // given an optional list come in both forms and the host picks one: a choice
@@ -42,6 +36,12 @@ struct ListedRows {
     return static_cast<int64_t>(r < last ? r : last);
   }
 };
+
+// Row t of an optional list (rows 0 .. k-1 without one), by ListedRows' rule;
+// for code outside the gathers' loops (staging, masks).
+__device__ __forceinline__ int64_t row_of(const int32_t* __restrict__ rows, int t, int n) {
+  return rows ? ListedRows{rows, n}(t) : static_cast<int64_t>(t);
+}
 
 template <int W>
 __device__ __forceinline__ void store_out(float* __restrict__ out, int64_t c, int64_t d,
