@@ -368,6 +368,23 @@ __host__ __device__ constexpr int bit_reverse(int x, int bits) {
   return r;
 }
 
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// The two low digit planes of four words: bytes 0 of w (c) and bytes 1 of
+// w + 128 (b). The low halves of two words are paired first, so that one
+// packed 16-bit add takes the + 128 to both (no carry crosses between the
+// halves, and a carry out of a half would only reach byte 2, which is not
+// read here): six instructions where four adds and six byte selects were ten.
+__device__ __forceinline__ void pack_low_digits(const uint32_t* w, uint32_t* pc, uint32_t* pb) {
+  const uint32_t l01 = __builtin_amdgcn_perm(w[1], w[0], 0x05040100u);  // w0.lo16 | w1.lo16 << 16
+  const uint32_t l23 = __builtin_amdgcn_perm(w[3], w[2], 0x05040100u);
+  *pc = __builtin_amdgcn_perm(l23, l01, 0x06040200u);  // bytes 0 and 2 of each pair
+  const u16x2 k = {128, 128};
+  const uint32_t m01 = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, l01) + k);
+  const uint32_t m23 = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, l23) + k);
+  *pb = __builtin_amdgcn_perm(m23, m01, 0x07050301u);  // bytes 1 and 3 of each pair
+}
+
 // Bytes `byte` of four 32-bit words, packed low to high.
 __device__ __forceinline__ uint32_t pack_bytes(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
                                                uint32_t byte) {
@@ -422,8 +439,8 @@ __device__ __forceinline__ void gram_put(uint8_t* __restrict__ lds, int n, int p
     w[3] = __builtin_bit_cast(uint32_t, __builtin_fmaf(v[i].w, scale, kRoundMagic));
     // the low 22 bits of w are those of q (w = bits(1.5 * 2^23 + q)); the
     // constant's bit 22 is taken out where the third byte is read
-    const uint32_t pc = pack_bytes(w[0], w[1], w[2], w[3], 0);
-    const uint32_t pb = pack_bytes(w[0] + 128u, w[1] + 128u, w[2] + 128u, w[3] + 128u, 1);
+    uint32_t pc, pb;
+    pack_low_digits(w, &pc, &pb);
     constexpr uint32_t kA = 32896u - 4194304u;  // + 32896, minus the constant's 2^22
     const uint32_t pa = pack_bytes(w[0] + kA, w[1] + kA, w[2] + kA, w[3] + kA, 2);
     const int off = row * kPlanePitch + 4 * lane;
