@@ -203,7 +203,12 @@ constexpr int kGramStage = 256;                  // coordinates per stage
 // the multiply (16 rows x 4 column groups per instruction) hit no bank twice
 // on gfx950 (measured: 272, 304, 336 and 400 do).
 constexpr int kPlanePitch = kGramStage + 32;
-constexpr int kGramThreads = 512;                // 4 producer + 4 consumer waves
+// Producer waves (then 4 consumer waves): eight, so that each holds few rows
+// and three stages of loads fit beside the consumers' registers at three
+// waves per SIMD (four producers with two stages in flight streamed slower).
+constexpr int kGramProducers = 8;
+constexpr int kGramThreads = (kGramProducers + 4) * 64;
+constexpr int kGramWavesPerSimd = (kGramProducers + 4) / 4;
 constexpr float kRoundMagic = 12582912.0f;       // 1.5 * 2^23
 
 typedef int i4 __attribute__((ext_vector_type(4)));
@@ -212,14 +217,15 @@ template <int NB>
 struct GramShape {
   static constexpr int ROWS = 16 * NB;
   static constexpr int NBP = NB * (NB + 1) / 2;   // block pairs b1 <= b2
-  static constexpr int RPW = ROWS / 4;            // rows loaded per wave
+  static constexpr int RPW = ROWS / kGramProducers;  // rows loaded per producer wave
   static constexpr int PPW = (NBP + 3) / 4;       // pairs per wave (q = w, w + 4, ...)
   static constexpr int PLANE = ROWS * kPlanePitch;  // bytes per digit plane
   static constexpr int BUF = 3 * PLANE + 4 * ROWS;  // three planes, then k per row
   static constexpr int LDS = 2 * BUF;               // two stage buffers
-  // stages a producer keeps in flight (register sets of RPW + 1 loads; four
-  // measured no faster than two at n = 19)
-  static constexpr int DEPTH = 2;
+  // stages a producer keeps in flight (register sets of RPW + 1 loads): at
+  // n = 64 three stages of 64 KB per CU stream 7% faster than two, and four
+  // exceed the registers of three waves per SIMD
+  static constexpr int DEPTH = 3;
 };
 
 __host__ __device__ constexpr int pair_b1(int nb, int q) {
@@ -593,8 +599,9 @@ __device__ __forceinline__ void gram_consume(const uint8_t* __restrict__ lds, in
   if (nf >= D) {
     for (; t + D - 1 < nf; t += D) {
 #pragma unroll
-      for (int u = 0; u < D; ++u) {  // iteration t + u: entry t + u - 1, buffer (u + 1) % 2
-        if (u > 0 || t >= 1) gram_multiply<NB, CV>(lds + ((u + 1) & 1) * S::BUF, g, r, acc64);
+      for (int u = 0; u < D; ++u) {  // iteration t + u: entry t + u - 1, buffer (t + u + 1) % 2
+        if (u > 0 || t >= 1)
+          gram_multiply<NB, CV>(lds + ((t + u + 1) & 1) * S::BUF, g, r, acc64);
         lds_barrier();
       }
     }
@@ -624,8 +631,8 @@ __device__ __forceinline__ void gram_produce(uint8_t* __restrict__ lds, int64_t 
     for (int u = 0; u < D; ++u) gram_issue<NB, PAD, true>(whole(u), n, ref, pw, lane, v[u], vr[u]);
     for (; t + D - 1 < nf; t += D) {
 #pragma unroll
-      for (int u = 0; u < D; ++u) {  // iteration t + u: buffer u % 2 (t and D even)
-        gram_put<NB, PAD, true>(lds + (u & 1) * S::BUF, n, pw, lane, v[u], vr[u], ref,
+      for (int u = 0; u < D; ++u) {  // iteration t + u: buffer (t + u) % 2
+        gram_put<NB, PAD, true>(lds + ((t + u) & 1) * S::BUF, n, pw, lane, v[u], vr[u], ref,
                                 whole(t + u + D));
         lds_barrier();
       }
@@ -648,11 +655,11 @@ __device__ __forceinline__ void gram_run(uint8_t* __restrict__ lds, int64_t cnt,
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   // the roles are compile-time per wave, so that every consumer's block
   // pairs, and with them its fragment registers, are constants
-  switch (wave) {
-    case 4: gram_consume<NB, 0>(lds, cnt, nf, out, stride); break;
-    case 5: gram_consume<NB, 1>(lds, cnt, nf, out, stride); break;
-    case 6: gram_consume<NB, 2>(lds, cnt, nf, out, stride); break;
-    case 7: gram_consume<NB, 3>(lds, cnt, nf, out, stride); break;
+  switch (wave - kGramProducers) {
+    case 0: gram_consume<NB, 0>(lds, cnt, nf, out, stride); break;
+    case 1: gram_consume<NB, 1>(lds, cnt, nf, out, stride); break;
+    case 2: gram_consume<NB, 2>(lds, cnt, nf, out, stride); break;
+    case 3: gram_consume<NB, 3>(lds, cnt, nf, out, stride); break;
     default: gram_produce<NB, PAD>(lds, cnt, nf, n, ref, wave, list); break;
   }
 }
@@ -679,7 +686,7 @@ struct MatrixStages {
 };
 
 template <int NB, bool PAD>
-__global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(kGramWavesPerSimd)))
 void k_dist_gram(const float* __restrict__ x, int n, int64_t d,
                  const int32_t* __restrict__ ref_idx, double* __restrict__ partial) {
   using S = GramShape<NB>;
@@ -736,7 +743,7 @@ struct TableStages {
 };
 
 template <int NB, bool PAD>
-__global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(kGramWavesPerSimd)))
 void k_dist_gram_table(const float* const* __restrict__ ptrs, GramSegs segs, int n,
                        const int32_t* __restrict__ ref_idx, int64_t tile_base, int64_t tiles,
                        double* __restrict__ partial) {
