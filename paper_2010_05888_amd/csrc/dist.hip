@@ -664,11 +664,24 @@ __device__ __forceinline__ void gram_run(uint8_t* __restrict__ lds, int64_t cnt,
   }
 }
 
-// Entries of workgroup b among `total` list entries of which the first
-// `nfull` are full stages: (count, full count).
+// The workgroup's slot among the G of a launch: list entry slot + i * G is
+// its i-th stage. Workgroups are dealt to the 8 XCDs round-robin (block b to
+// XCD b % 8), so slot (b % 8) * (G / 8) + b / 8 gives each XCD a contiguous
+// run of slots, and stages next to each other, which share the cache lines
+// at the ends of their 1 KB row runs, meet in one XCD's L2 at about the same
+// time instead of being fetched by two XCDs. (A bijection on [0, G) when 8
+// divides G; other grids keep b.)
+__device__ __forceinline__ int64_t gram_slot() {
+  const int64_t b = blockIdx.x, G = gridDim.x;
+  if (G % 8 != 0) return b;
+  return (b % 8) * (G / 8) + b / 8;
+}
+
+// Entries of this workgroup's slot b among `total` list entries of which the
+// first `nfull` are full stages: (count, full count).
 __device__ __forceinline__ void gram_share(int64_t total, int64_t nfull, int64_t* cnt,
                                            int64_t* nf) {
-  const int64_t b = blockIdx.x, G = gridDim.x;
+  const int64_t b = gram_slot(), G = gridDim.x;
   *cnt = total > b ? (total - b + G - 1) / G : 0;
   *nf = nfull > b ? (nfull - b + G - 1) / G : 0;
 }
@@ -680,7 +693,7 @@ struct MatrixStages {
   int64_t d;
   int64_t nfull;
   __device__ __forceinline__ StageRef<MatrixRows> entry(int64_t i) const {
-    const int64_t li = blockIdx.x + i * gridDim.x;  // list index (the partial stage is last)
+    const int64_t li = gram_slot() + i * gridDim.x;  // list index (the partial stage is last)
     return StageRef<MatrixRows>{MatrixRows{x, d}, li * kGramStage, d, li < nfull};
   }
 };
@@ -726,7 +739,7 @@ struct TableStages {
   const GramSegs* segs;
   __device__ __forceinline__ StageRef<TableRows> entry(int64_t i) const {
     const GramSegs& t = *segs;
-    const int64_t li = blockIdx.x + i * gridDim.x;
+    const int64_t li = gram_slot() + i * gridDim.x;
     const int64_t nfull = t.ffirst[t.count];
     if (li < nfull) {
       const int sg = last_le(t.ffirst, t.count, li);
