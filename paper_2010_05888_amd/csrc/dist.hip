@@ -5,7 +5,8 @@
 //
 // Every workgroup of the distance kernel is a tile: the direct engine cuts the
 // coordinates into tiles of `chunk` consecutive coordinates, the Gram engine
-// gives workgroup b the 256-coordinate stages b, b + G, b + 2G, ... Each tile
+// gives each workgroup the 256-coordinate stages s, s + G, s + 2G, ... of its
+// slot s (gram_slot: a permutation of the workgroups by XCD). Each tile
 // writes one fp64 partial sum per entry (entry-major: partial[entry * tiles +
 // tile]); k_sum_tiles then adds the tiles of each entry in a fixed order, so D
 // is deterministic and depends only on (n, d), never on scheduling. The
@@ -195,9 +196,9 @@ __global__ __launch_bounds__(kPickThreads) void k_pick_ref(const double* __restr
 // B alike).
 //
 // Partials. Each consumer wave writes the fp64 sums of its pairs as this
-// workgroup's partials; workgroup b takes stages b, b + G, ... (G = grid
-// size, one workgroup per CU), so at any time the grid streams one compact
-// window of every row.
+// workgroup's partials; the workgroup of slot s takes stages s, s + G, ...
+// (G = grid size, one workgroup per CU), so at any time the grid streams one
+// compact window of every row.
 constexpr int kGramStage = 256;                  // coordinates per stage
 // Bytes per LDS row of a digit plane: with 288 the 16-byte fragment reads of
 // the multiply (16 rows x 4 column groups per instruction) hit no bank twice
@@ -570,16 +571,17 @@ struct GramSegs {
   int64_t dims[kSegMax];
 };
 
-// The schedule of a workgroup. Its stages are entries b, b + G, ... of a list
-// that holds every full stage first and then the partial ones (G = grid
-// size, one workgroup per CU), `cnt` entries of which the first `nf` are
-// full. In iteration i the producers quantize entry i into buffer i % 2 and
-// the consumers multiply entry i - 1 from buffer (i - 1) % 2; a barrier
-// ends every iteration. Iterations run two at a time while both entries are
-// full stages, with every load unconditional (so the compiler keeps the
-// next stages' loads in flight across the quantizing); the rest (the last
-// full stage when nf is odd, the partial stages and the final multiply) go
-// one at a time with guarded loads.
+// The schedule of a workgroup. Its stages are entries s, s + G, ... (s its
+// slot) of a list that holds every full stage first and then the partial
+// ones (G = grid size, one workgroup per CU), `cnt` entries of which the
+// first `nf` are full. In iteration i the producers quantize entry i into
+// buffer i % 2 and the consumers multiply entry i - 1 from buffer
+// (i - 1) % 2; a barrier ends every iteration. Iterations run DEPTH at a
+// time while all those entries are full stages, with every load
+// unconditional (so the compiler keeps the next DEPTH stages' loads in
+// flight across the quantizing); the rest (the full stages past the last
+// multiple of DEPTH, the partial stages and the final multiply) go one at a
+// time with guarded loads.
 
 // Consumer wave CV, then its partials.
 template <int NB, int CV>
@@ -719,7 +721,8 @@ void k_dist_gram(const float* __restrict__ x, int n, int64_t d,
 // stages of all its segments in segment order (segment s owns list entries
 // ffirst[s] .. ffirst[s+1]-1), then the partial last stage of every segment
 // whose length 256 does not divide (entries nfull + pfirst[s] for those),
-// and workgroup b takes entries b, b + G, ..., each with its segment's rows.
+// and the workgroup of slot s takes entries s, s + G, ..., each with its
+// segment's rows.
 // One reference row index serves every segment (D is the same whatever row
 // each coordinate is shifted by). Tile b of the launch writes column
 // tile_base + b of partials with `tiles` columns in all.
@@ -1086,8 +1089,8 @@ DistPlan plan_distances(int n, int64_t d, const float* x) {
     p.engine = kEngineGram;
     p.width = 4;  // 16-byte loads of 1 KB row runs
     // As many workgroups as the device holds resident (at most one per
-    // stage); workgroup b takes stages b, b + tiles, ... (the partial last
-    // stage, if any, among them).
+    // stage); slot s takes stages s, s + tiles, ... (the partial last stage,
+    // if any, among them).
     const int nb = (n + 15) / 16;
     const int64_t slots = static_cast<int64_t>(device_cus()) * gram_blocks_per_cu(nb);
     const int64_t stages = (d + kGramStage - 1) / kGramStage;
