@@ -53,7 +53,8 @@ typedef enum garfield_status {
   GARFIELD_OK = 0,
   GARFIELD_EINVAL = 1,  /* null pointer, n < 1, f < 0, d < 0, m or k out of range */
   GARFIELD_EREQ = 2,    /* n below the rule's requirement in f (Section 3.1) */
-  GARFIELD_ETOOBIG = 3, /* n > GARFIELD_NMAX, or C(n, f) > GARFIELD_MDA_MAX_SUBSETS */
+  GARFIELD_ETOOBIG = 3, /* n > GARFIELD_NMAX, C(n, f) > GARFIELD_MDA_MAX_SUBSETS, or
+                           d > (2^31 - 1) * 256 (beyond one launch) */
   GARFIELD_ENOMEM = 4,  /* the workspace could not be allocated */
   GARFIELD_EHIP = 5     /* a HIP call or kernel launch failed */
 } garfield_status;

@@ -75,6 +75,9 @@ garfield_status check_common(const float* x, int n, int f, int64_t d) {
   if (n < 1 || f < 0 || d < 0) return GARFIELD_EINVAL;
   if (d > 0 && (!x || reinterpret_cast<uintptr_t>(x) % sizeof(float) != 0)) return GARFIELD_EINVAL;
   if (n > GARFIELD_NMAX) return GARFIELD_ETOOBIG;
+  // every kernel covers d in one launch of at most 2^31 - 1 workgroups of
+  // kBlock lanes, each lane at least one coordinate
+  if (d > int64_t{0x7fffffff} * kBlock) return GARFIELD_ETOOBIG;
   return GARFIELD_OK;
 }
 
@@ -707,7 +710,7 @@ const char* garfield_strerror(garfield_status s) {
     case GARFIELD_OK: return "success";
     case GARFIELD_EINVAL: return "invalid argument (null pointer, n < 1, f < 0, d < 0, m or k out of range)";
     case GARFIELD_EREQ: return "n is below the rule's requirement in f";
-    case GARFIELD_ETOOBIG: return "problem too large (n > GARFIELD_NMAX or too many MDA subsets)";
+    case GARFIELD_ETOOBIG: return "problem too large (n > GARFIELD_NMAX, too many MDA subsets, or d beyond one launch)";
     case GARFIELD_ENOMEM: return "device workspace allocation failed";
     case GARFIELD_EHIP: return "HIP runtime error";
   }

@@ -88,6 +88,13 @@ def test_validation_codes(lib):
     # distances / average
     assert lib.garfield_pairwise_sqdist(FAKE, 5, 10, NULL, NULL) == gf.EINVAL
     assert lib.garfield_average(FAKE, 0, 10, FAKE, NULL) == gf.EINVAL
+    # d beyond one launch ((2^31 - 1) workgroups of 256 coordinates): refused
+    # before anything is enqueued, whatever the rule
+    huge = (2 ** 31 - 1) * 256 + 1
+    assert lib.garfield_average(FAKE, 3, huge, FAKE, NULL) == gf.ETOOBIG
+    assert lib.garfield_median(FAKE, 3, 0, huge, NULL, 0, FAKE, NULL) == gf.ETOOBIG
+    assert lib.garfield_krum(FAKE, 7, 1, huge, FAKE, FAKE, NULL) == gf.ETOOBIG
+    assert lib.garfield_bulyan(FAKE, 7, 1, huge, FAKE, FAKE, NULL) == gf.ETOOBIG
 
 
 def test_strerror_and_version(lib):
