@@ -162,15 +162,15 @@ __global__ __launch_bounds__(kPickThreads) void k_pick_ref(const double* __restr
 // not loaded; their Y rows are 0) times kGramStage = 256 consecutive
 // coordinates: 1 KB of every row, the shortest run that streams well from
 // rows whose starts are not cache-line aligned (row i starts at i * d
-// floats). A workgroup is eight waves in two roles. Waves 0-3 produce: wave
-// w loads rows w*4NB .. w*4NB + 4NB - 1 with one 16-byte load per lane per
-// row (lane l: coordinates 4l .. 4l+3, so one instruction reads 1 KB of one
-// row), quantizes them into one of two LDS stage buffers, and keeps the next
-// two stages' loads in flight in two register sets (each row's next load is
-// issued as soon as the row is written). Waves 4-7
-// consume: they multiply the stage in the other buffer. One barrier per
-// stage hands the buffers over, so quantizing (VALU) and multiplying (matrix
-// cores) overlap on every SIMD, which holds one wave of each role.
+// floats). A workgroup is twelve waves in two roles. Waves 0-7 produce:
+// wave w loads rows w*2NB .. w*2NB + 2NB - 1 with one 16-byte load per lane
+// per row (lane l: coordinates 4l .. 4l+3, so one instruction reads 1 KB of
+// one row), quantizes them into one of two LDS stage buffers, and keeps the
+// next DEPTH stages' loads in flight in DEPTH register sets (each row's next
+// load is issued as soon as the row is written). Waves 8-11 consume: they
+// multiply the stage in the other buffer. One barrier per stage hands the
+// buffers over, so quantizing (VALU) and multiplying (matrix cores) overlap
+// on every SIMD, which holds two producer waves and one consumer.
 //
 // Quantizing. y = fl(x - x_ref) in fp32 (one rounding). Per row and stage,
 // with E the exponent of the largest |y| (-126 for a zero or subnormal
