@@ -218,6 +218,9 @@ def test_zero_dimension_selects_lowest_indices():
     assert sel.cpu().tolist() == [0, 1, 2] and out.numel() == 0
     D = gf.pairwise_sqdist(x).cpu().numpy()
     assert np.all(D == 0)
+    out, sel = gf.krum(x, 1)
+    assert sel.cpu().tolist() == [0] and out.numel() == 0
+    assert gf.average(x).numel() == 0
 
 
 def test_single_vector():
