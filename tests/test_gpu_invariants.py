@@ -91,3 +91,25 @@ def test_permutation_scaling_negation(rule, n, f, engine):
             assert torch.equal(outn, -out)
     finally:
         gf.set_direct_max_n(old)
+
+
+@pytest.mark.parametrize("n,f,engine", CASES + [(64, 15, "gram")])
+def test_distance_matrix_permutes_and_scales_exactly(n, f, engine):
+    # D of the permuted rows is D permuted, bit for bit (each entry depends on
+    # its two rows only: per pair in the direct engine; through exact integer
+    # products of rows shifted by the same reference row in the Gram engine),
+    # and D of 2^s x is 4^s D exactly
+    old = gf.set_direct_max_n(20 if engine == "direct" else 1)
+    try:
+        x, rng = _data(n, f, 9100 + n)
+        xt = torch.from_numpy(x).to(DEV)
+        D = gf.pairwise_sqdist(xt).cpu().numpy()
+        perm = rng.permutation(n)
+        Dp = gf.pairwise_sqdist(torch.from_numpy(x[perm]).to(DEV)).cpu().numpy()
+        assert np.array_equal(Dp, D[np.ix_(perm, perm)])
+        for s in (-3, 5):
+            Ds = gf.pairwise_sqdist(xt * float(2.0 ** s)).cpu().numpy()
+            assert np.array_equal(Ds, D * 4.0 ** s), f"scaling by 2^{s}"
+        assert np.array_equal(gf.pairwise_sqdist(-xt).cpu().numpy(), D)
+    finally:
+        gf.set_direct_max_n(old)
